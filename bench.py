@@ -1,0 +1,205 @@
+#!/usr/bin/env python3
+"""Throughput of the xPress refine + verify hot path on one MI355X.
+
+One step = one xp_refine_block (base readout through the target LM head,
+seed selection, K Jacobi passes of the refiner) plus one xp_verify_block over
+a batch of synthetic draft blocks whose inputs are already resident in HBM.
+The default workload is the Qwen3-8B shape at batch 1 (H = 4096, V = 151936,
+r = 256, block 16, greedy, K = 6).
+
+Prints one JSON line.  `value` is refined draft blocks per second; `roofline`
+rates the dominant kernel (the LM-head stream) by its algorithmic bytes over
+its own duration, measured with HIP events recorded by the library on the
+stream the kernel runs on; `cpu_baseline` times the fp64 oracle on one block.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+    python bench.py --copy-probe BYTES      (a plain device copy, for counter scaling)
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "refined draft blocks/sec (refine+LM-head+verify), Qwen3-8B shape; % HBM/MFMA peak"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc", "xp_stream.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def committed_traffic():
+    """HBM bytes per LM-head launch from the committed counter summary, if it
+    was taken on the current kernel source; otherwise None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    txt = open(TRAFFIC_FILE).read()
+    m = re.search(r"source_sha256_16:\s*([0-9a-f]{16})", txt)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m or not t or m.group(1) != kernel_source_hash():
+        return None
+    return float(t.group(1))
+
+
+def copy_probe(nbytes: int):
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": src.numel() * 4, "dispatches": 3}), flush=True)
+
+
+def cpu_baseline(wl, weights, inp):
+    """The oracle, as it stands, on one block of the workload (refine + verify)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle as O
+    t0 = time.perf_counter()
+    P = O.Params.from_arrays(weights)
+    res = O.refine_batch(P, inp.h[:1], inp.anchor[:1], inp.temp[:1], inp.u_draft[:1], wl.K,
+                         seed_ids=None if inp.seed_ids is None else inp.seed_ids[:1],
+                         early_exit=False)
+    r0 = res.refined[0]
+    tid = inp.target_ids(r0.ids[None, :])
+    if inp.temp[0]:
+        O.verify_sample(r0.logits, r0.ids, inp.target_logits[0].astype(np.float64),
+                        inp.r_accept[0], float(inp.u_res[0]))
+    else:
+        O.verify_greedy(r0.ids, tid[0])
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": 1.0 / dt, "unit": "blocks/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 block (batch row 0) of {wl.name}: fp64 base readout, {wl.K} Jacobi "
+                      f"passes and verification, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3-8b-bf16-B16-b1-greedy")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this path runs on one GPU; multi-GPU runs are not part of it "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}).", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_02438_amd.xpress import device_tensor, refiner_from_arrays
+
+    wl = synth.BY_NAME[args.workload]
+    log(f"[bench] workload {wl.name}: generating inputs")
+    weights = synth.make_weights(wl)
+    inp = synth.make_inputs(wl)
+    log("[bench] uploading and creating the handle")
+    ref = refiner_from_arrays(weights, wl.H, wl.r, wl.V, wl.B, wl.batch)
+    hid = device_tensor(inp.h)
+    anchor = device_tensor(inp.anchor)
+    seed = device_tensor(inp.seed_ids) if inp.seed_ids is not None else None
+    sample_rows = bool(inp.temp.any())
+    temp = device_tensor(inp.temp) if sample_rows else None
+    u_draft = device_tensor(inp.u_draft) if sample_rows else None
+    tl = device_tensor(inp.target_logits) if sample_rows else None
+    r_acc = device_tensor(inp.r_accept)
+    u_res = device_tensor(inp.u_res)
+
+    out = ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=wl.K)
+    torch.cuda.synchronize()
+    # greedy targets are built around the refined block (fixed by the inputs)
+    tids = device_tensor(inp.target_ids(out.ids.cpu().numpy()))
+    vout = ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
+                            u_resample=u_res)
+
+    def step():
+        ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=wl.K, out=out)
+        ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
+                         u_resample=u_res, out=vout)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-stage breakdown (all stages timed), outside the measured region
+    ref.timing_enable(("prep", "lmhead", "select", "rspace", "read", "verify"), capacity=4096)
+    for _ in range(3):
+        step()
+    breakdown = ref.timing_read()
+
+    # the measured region: only the LM-head launch carries an event pair
+    ref.timing_enable(("lmhead",), capacity=max(args.steps, 1))
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    tm = ref.timing_read()
+    ref.timing_enable((), 1)
+    elapsed = t1 - t0
+    ms_step = elapsed * 1e3 / args.steps
+    blocks_s = wl.batch * args.steps / elapsed
+    lm_ms, lm_n = tm["lmhead"]
+    lm_us = lm_ms * 1e3 / max(lm_n, 1)
+    M = wl.batch * wl.B
+    es = 2 if wl.dtype == "bf16" else 4
+    # algorithmic bytes of one LM-head launch: W_lm once, h once, s written once
+    lm_bytes = wl.V * wl.H * es + M * wl.H * es + M * wl.V * 4
+    achieved = lm_bytes / (lm_us * 1e-6) / 1e9
+    n_acc = vout[0].cpu().numpy()
+    log(f"[bench] {ms_step:.3f} ms/step, LM head {lm_us:.1f} us ({achieved:.0f} GB/s)")
+
+    line = {
+        "metric": METRIC, "value": blocks_s, "unit": "blocks/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic: seeded N(0,0.02^2) bf16 weights of the Qwen3-8B-shaped LM head and "
+                "rank-256 refiner, N(0,1) drafter hidden states, uniform anchors",
+        "config": {"workload": wl.name, "batch": wl.batch, "block": wl.B, "K": wl.K,
+                   "H": wl.H, "V": wl.V, "r": wl.r, "temperature": wl.temp},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": committed_traffic(),
+                     "kernel": "k_lmhead (base readout s = W_lm h)",
+                     "algorithmic_bytes_per_launch": lm_bytes, "launch_us": lm_us},
+        "refined_tokens_per_s": blocks_s * wl.B,
+        "stage_ms_per_step": {k: v[0] / max(1, 3) for k, v in breakdown.items()},
+        "accepted_mean": float(np.mean(n_acc)),
+    }
+    if not args.no_cpu:
+        log("[bench] CPU oracle baseline (one block)")
+        line["cpu_baseline"] = cpu_baseline(wl, weights, inp)
+    else:
+        line["cpu_baseline"] = None
+    ref.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

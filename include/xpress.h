@@ -1,0 +1,197 @@
+/*
+ * xpress.h -- C ABI of the xPress refine + verify hot path on MI355X (gfx950).
+ *
+ * The path (paper sections 3.1 and 4):
+ *   base readout   s_k = W_lm h_k                         (section 4.1, Fig. 2a)
+ *   seed           Y0_k = select(s_k)                      (Algorithm 1, first step)
+ *   K Jacobi passes of the refiner, each one
+ *     Fuse  a_k = W_in [W_h h_k || W_g g || W_e[x_{k-1}]], g = mean_j h_j   (eq. fuse)
+ *     Mix   c^(d) = (I + L^(d)) a^(d), L^(d) strictly lower-triangular       (eq. mix)
+ *     Trans z_k = c_k + W_2 silu(W_1 c_k)                                      (eq. mlp)
+ *     Read + Correct  l_k = s_k + W_r z_k                            (eqs. read, correct)
+ *     select y_k = argmax_v l_k (greedy) or inverse-CDF sample of softmax(l_k)
+ *     stop at the fixed point Y^(j+1) = Y^(j)             (Algorithm 1, Theorem 1)
+ *   verification: greedy longest matching prefix plus bonus token, or
+ *     speculative accept/reject with residual resampling (section 3.1)
+ *
+ * Conventions
+ *   - Every pointer argument is a DEVICE pointer unless marked "host".  All
+ *     buffers are caller-owned, row-major, densely packed.  Weight buffers
+ *     must stay alive and unchanged for the life of the handle.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream).  The host does argument validation only, before any HIP call;
+ *     nothing is copied back to the host inside refine or verify.
+ *   - A handle is not thread-safe.  Calls on one handle must be ordered on one
+ *     stream (the handle's workspace is shared between calls).
+ *   - On a non-XP_OK return nothing has been enqueued, except for XP_EHIP,
+ *     after which outputs are unspecified.  xp_last_error() names the problem.
+ *   - Token ids read from device memory (anchor, seed ids, draft ids, target
+ *     ids) that fall outside [0, V) are replaced by 0 and recorded in the
+ *     handle's device error word (XP_DEVERR_TOKEN); see xp_device_errors().
+ */
+#ifndef XPRESS_H
+#define XPRESS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  XP_OK = 0,
+  XP_EINVAL = -1,        /* bad argument (null pointer, size, flag combination)  */
+  XP_EUNSUPPORTED = -2,  /* valid per the paper but not built here (e.g. r != 256) */
+  XP_EHIP = -3,          /* a HIP runtime call failed                              */
+  XP_ENOMEM = -4         /* device allocation of the workspace failed              */
+} xp_status;
+
+typedef enum { XP_F32 = 0, XP_BF16 = 1 } xp_dtype;
+
+/* flags of xp_refine_block */
+#define XP_EARLY_EXIT   1u  /* skip the remaining passes once every sequence is at its fixed point */
+#define XP_WRITE_LOGITS 2u  /* write the refined logits l of the last executed pass to out_logits   */
+
+/* bits of the device error word */
+#define XP_DEVERR_TOKEN 1u  /* a token id outside [0, V) was read and replaced by 0 */
+
+typedef struct xp_handle xp_handle;
+
+/*
+ * Weights (device pointers, element type `dtype`, row-major).  The paper's
+ * shapes (section 4.1) with rows as output units:
+ *   W_lm [V][H]   target LM head (base readout s_k = W_lm h_k)
+ *   W_h  [r][H]   down-projection of h_k
+ *   W_g  [r][H]   down-projection of g
+ *   W_e  [V][r]   token embedding, one row per token (the paper's r x V W_e, transposed)
+ *   W_in [r][3r]  fusion projection; column blocks [h | g | token] in eq. fuse order
+ *   L    [r][B][B] per-channel mixer; entry [d][k][i] is read only for i < k
+ *   W_1  [2r][r], W_2 [r][2r]   r-space MLP of eq. mlp
+ *   W_r  [V][r]   readout head
+ * r must be 256 (the paper's rank); H a multiple of 256 up to 8192; 1 <= B <= 32;
+ * 16 <= V < 2^31.
+ */
+typedef struct {
+  int32_t H, r, V, B;
+  int32_t dtype;                     /* xp_dtype */
+  const void* W_lm;
+  const void* W_h;
+  const void* W_g;
+  const void* W_e;
+  const void* W_in;
+  const void* L;
+  const void* W_1;
+  const void* W_2;
+  const void* W_r;
+} xp_weights;
+
+/*
+ * Create a handle for one weight set on the current HIP device.
+ * Allocates the workspace for up to `max_batch` sequences (device memory, freed
+ * by xp_destroy) and precomputes, once, weight-only products in fp32: the token
+ * table T = W_e W_in[:, 2r:3r]^T ([V][r]) and the folded down-projections
+ * W_in[:, 0:r] W_h and W_in[:, r:2r] W_g ([r][H] each); L is repacked to its
+ * strictly lower part.  Synchronous (returns after the precompute finished).
+ * Errors: XP_EINVAL (null, sizes), XP_EUNSUPPORTED (r != 256, H, B, dtype),
+ * XP_ENOMEM, XP_EHIP.  *out is NULL on error.
+ */
+xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle** out);
+
+/* Free the handle and its workspace.  Waits for the device first.  NULL is a no-op. */
+void xp_destroy(xp_handle* h);
+
+/* Message for the last error on `h` (or of the last failed xp_create when h is NULL). */
+const char* xp_last_error(const xp_handle* h);
+
+/* Name of a status code. */
+const char* xp_status_string(xp_status s);
+
+/*
+ * Refine a batch of draft blocks: base readout, seed, K Jacobi passes.
+ *
+ *   batch      number of sequences, 1 <= batch <= max_batch
+ *   hidden     [batch][B][H] dtype     drafter hidden states h_{1:B}
+ *   anchor     [batch] int32           x_0, the token before the block
+ *   seed_ids   [batch][B] int32 or NULL  Y^(0); NULL: select from the base logits
+ *   temp       [batch] uint8 or NULL   per sequence 0 = greedy (argmax, ties to the
+ *              lowest index), nonzero = temperature-1 sampling; NULL = all greedy
+ *   u_draft    [batch][B] float in [0,1), required iff temp != NULL: the uniform of
+ *              each position; a sampled position takes the smallest v whose
+ *              cumulative softmax mass exceeds u (fixed across passes)
+ *   K          number of Jacobi passes, 0 <= K <= 64 (K = 0 returns Y^(0))
+ *   flags      XP_EARLY_EXIT | XP_WRITE_LOGITS
+ *   out_ids    [batch][B] int32        refined block
+ *   out_iters  [batch] int32 or NULL   passes until Y^(j+1) = Y^(j) held (K if never)
+ *   out_logits [batch][B][V] float, required iff XP_WRITE_LOGITS: l of the last
+ *              executed pass (s when K = 0)
+ *   out_traj   [K+1][batch][B] int32 or NULL: Y^(0) .. Y^(K) (a skipped pass
+ *              repeats the previous iterate)
+ * The refined distributions of the last pass stay in the handle for a following
+ * xp_verify_block on the same stream, until the next xp_refine_block.
+ */
+xp_status xp_refine_block(xp_handle* h, int32_t batch,
+                          const void* hidden, const int32_t* anchor,
+                          const int32_t* seed_ids, const uint8_t* temp,
+                          const float* u_draft, int32_t K, uint32_t flags,
+                          int32_t* out_ids, int32_t* out_iters,
+                          float* out_logits, int32_t* out_traj, void* stream);
+
+/*
+ * Verify refined blocks against the target (section 3.1).
+ *
+ *   batch          must equal the batch of the preceding xp_refine_block
+ *   draft_ids      [batch][B] int32, the block being verified (normally out_ids)
+ *   temp           [batch] uint8 or NULL, as given to that refine
+ *   target_ids     [batch][B+1] int32: greedy rows' target tokens t_1..t_{B+1}
+ *                  (t_k is the target's choice after the draft prefix y_{<k});
+ *                  always required (only greedy rows read it)
+ *   target_logits  [batch][B+1][V] float: sampled rows' target logits after each
+ *                  prefix (temperature 1); required iff temp != NULL
+ *   r_accept       [batch][B] float in [0,1), required iff temp != NULL
+ *   u_resample     [batch] float in [0,1), required iff temp != NULL
+ *   out_accept_len [batch] int32 n in [0, B] (the paper's tau counts n + 1)
+ *   out_next_token [batch] int32 correction token at the first rejection, or
+ *                  the bonus token when all B are accepted
+ * Greedy rows: n = longest prefix with y_i = t_i, next = t_{n+1}.
+ * Sampled rows: accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k the refined
+ * distribution of refine's last pass and p_k = softmax(target logits k); at the
+ * first rejection next is the inverse-CDF sample at u_resample of max(0, p_k - q_k)
+ * (of p_k if that has no mass); if all are accepted next samples p_{B+1}.
+ */
+xp_status xp_verify_block(xp_handle* h, int32_t batch,
+                          const int32_t* draft_ids, const uint8_t* temp,
+                          const int32_t* target_ids, const float* target_logits,
+                          const float* r_accept, const float* u_resample,
+                          int32_t* out_accept_len, int32_t* out_next_token,
+                          void* stream);
+
+/*
+ * Stage timing with HIP events, for benchmarks.  While a stage's bit is set in
+ * `stage_mask`, every call records one event pair on its stream around that
+ * stage's kernels (up to `capacity` pairs per stage; later ones are not
+ * recorded).  Stages: XP_STAGE_PREP (g and the static Fuse part), LMHEAD (base
+ * readout s = W_lm h), SELECT (token selection of every pass), RSPACE (Fuse
+ * gather, Mix, Trans), READ (Read + Correct stream), VERIFY.  A mask of 0
+ * disables timing.  xp_timing_read synchronizes the device, writes the summed
+ * milliseconds and the number of recorded pairs per stage (host arrays of
+ * XP_NSTAGES entries) and clears the record.
+ */
+typedef enum {
+  XP_STAGE_PREP = 0, XP_STAGE_LMHEAD = 1, XP_STAGE_SELECT = 2,
+  XP_STAGE_RSPACE = 3, XP_STAGE_READ = 4, XP_STAGE_VERIFY = 5, XP_NSTAGES = 6
+} xp_stage;
+
+xp_status xp_timing_enable(xp_handle* h, uint32_t stage_mask, int32_t capacity);
+xp_status xp_timing_read(xp_handle* h, float* ms_total, int32_t* pairs);
+
+/*
+ * Read and clear the handle's device error word (XP_DEVERR_* bits) into *out
+ * (host).  Synchronizes `stream`.
+ */
+xp_status xp_device_errors(xp_handle* h, uint32_t* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XPRESS_H */

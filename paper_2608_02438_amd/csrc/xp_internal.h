@@ -1,0 +1,94 @@
+// Host-side internals: the handle, its workspace, and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/xpress.h"
+#include "xp_device.h"
+
+namespace xp {
+
+// Launch shapes of the two vocabulary streams (tuned for 256 CUs).
+constexpr int kLmWaves = 16;    // A1: waves per workgroup, each owning H/16 of the k range
+constexpr int kReadWaves = 16;  // A7: waves per workgroup, each streaming its own tiles
+constexpr int kMaxK = 64;
+
+struct Workspace {
+  float* s = nullptr;         // [Mmax][ldS]   base logits s_k
+  float* T = nullptr;         // [V][r]        token table W_e W_in[:, 2r:3r]^T
+  float* Fh = nullptr;        // [r][H]        W_in[:, 0:r] W_h
+  float* Fg = nullptr;        // [r][H]        W_in[:, r:2r] W_g
+  void* Lp = nullptr;         // [npairs][r]   L[d][k][i] (i < k) at pair k(k-1)/2 + i
+  float* g = nullptr;         // [max_batch][H]
+  float* uh = nullptr;        // [Mmax][r]     Fh h_k
+  float* ug = nullptr;        // [max_batch][r] Fg g
+  float* c = nullptr;         // [Mmax][r]     Mix output
+  float* h1 = nullptr;        // [Mmax][2r]    silu(W_1 c)
+  void* z = nullptr;          // [Mmax][r]     Trans output (dtype)
+  int32_t* Y[2] = {nullptr, nullptr};   // [Mmax] iterates, ping-pong by pass parity
+  uint64_t* keys = nullptr;   // [max chunks][Mmax]  greedy partials
+  Stat* stats = nullptr;      // [max units][Mmax]   sampling partials
+  double* lse = nullptr;      // [Mmax]        log-sum-exp of the last pass (sampled rows)
+  int32_t* iters = nullptr;   // [max_batch]
+  int32_t* ctrl = nullptr;    // [0] converged-sequence count, [1] all-converged flag
+  uint32_t* err = nullptr;    // device error word
+  // verification scratch
+  double* vstat = nullptr;    // [max_batch][B+1][2] target (max, log-sum-exp) per row
+  int32_t* vpos = nullptr;    // [max_batch][2] rejected position (or B), state
+  double* vmass = nullptr;    // [max units][max_batch] residual / bonus mass per unit
+};
+
+}  // namespace xp
+
+struct xp_timing_state {
+  uint32_t mask = 0;
+  int capacity = 0;
+  std::vector<hipEvent_t> ev[XP_NSTAGES];   // 2 * capacity events per stage
+  int n[XP_NSTAGES] = {0, 0, 0, 0, 0, 0};
+};
+
+struct xp_handle {
+  int device = 0;
+  int H = 0, r = 0, V = 0, B = 0, dtype = 0, max_batch = 0;
+  const void *W_lm = nullptr, *W_h = nullptr, *W_g = nullptr, *W_e = nullptr, *W_in = nullptr,
+             *L = nullptr, *W_1 = nullptr, *W_2 = nullptr, *W_r = nullptr;
+  int ldS = 0, ntiles = 0;
+  int cus = 0;
+  int lm_chunks = 0;           // A1 workgroups along the vocabulary (= units)
+  int read_wgs = 0;            // A7 workgroups along the vocabulary
+  int read_units = 0;          // read_wgs * kReadWaves
+  xp::Workspace ws;
+  int last_batch = -1;         // batch of the last refine (verify state)
+  bool state_valid = false;
+  bool state_k0 = false;       // last refine ran K = 0 passes (q = softmax(s))
+  bool state_temp = false;     // last refine was given per-row temperatures
+  std::string err;
+  xp_timing_state tm;
+};
+
+namespace xp {
+
+// launchers (each returns hipGetLastError() of its launch)
+hipError_t launch_fold(xp_handle* h, hipStream_t st);
+hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t st);
+hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t* temp, hipStream_t st);
+hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
+                         const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
+                         int32_t* out_traj, hipStream_t st);
+hipError_t launch_fuse_mix_w1(xp_handle* h, int batch, int pass, uint32_t flags,
+                              const int32_t* anchor, hipStream_t st);
+hipError_t launch_w2(xp_handle* h, int batch, int pass, uint32_t flags, hipStream_t st);
+hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
+                       float* out_logits, hipStream_t st);
+hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,
+                         int32_t* out_iters, float* out_logits, hipStream_t st);
+hipError_t launch_verify(xp_handle* h, int batch, const int32_t* draft_ids, const uint8_t* temp,
+                         const int32_t* target_ids, const float* target_logits,
+                         const float* r_accept, const float* u_res, int32_t* out_n,
+                         int32_t* out_next, hipStream_t st);
+
+}  // namespace xp

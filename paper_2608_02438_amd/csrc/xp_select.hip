@@ -1,0 +1,251 @@
+// Token selection from the per-unit partials of a vocabulary stream, and the
+// Jacobi bookkeeping of Algorithm 1 (fixed-point test, iteration count).
+//
+// Greedy rows: the maximum 64-bit key over the stream's workgroups gives
+// argmax_v l_v with ties to the lowest index.
+// Sampled rows (temperature 1): y = min{v : sum_{w<=v} e^{l_w - m} > u Z}.
+//   1. m = max over units, Z = in-order fp64 scan of the unit masses
+//      sum_u e^{max_u - m};
+//   2. the same scan again finds the unit whose inclusive prefix exceeds u Z;
+//   3. that unit's rows are recomputed with the stream's own MFMA tile code
+//      (same fp32 logits) and scanned in vocabulary order in fp64.
+// The log-sum-exp m + log Z of the chosen pass is kept for verification.
+#include "xp_internal.h"
+#include "xp_tiles.h"
+
+namespace xp {
+
+__device__ __forceinline__ double wave_incl_scan(double x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double y = __shfl_up(x, off, kWave);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
+  return x;
+}
+
+// Mass of unit i for position p relative to the global max m (0 for empty units).
+__device__ __forceinline__ double unit_mass(const Stat* __restrict__ stats, int i, int U, int M,
+                                            int p, float m) {
+  if (i >= U) return 0.0;
+  const Stat s = stats[(size_t)i * M + p];
+  return s.s > 0.f ? (double)s.s * exp((double)s.m - (double)m) : 0.0;
+}
+
+// Inverse-CDF selection for position p (one wave).  mode 0 reads l = s from
+// memory, mode 1 recomputes l = s + W_r z for the crossing unit.
+template <typename T>
+__device__ int sample_position(int mode, int p, float u, const float* __restrict__ S, int ldS,
+                               const T* __restrict__ W_r, const T* __restrict__ Z, int M, int V,
+                               const Stat* __restrict__ stats, int ntiles, int U, double* lse_out,
+                               bool pick) {
+  const int lane = threadIdx.x & 63;
+  float m = -INFINITY;
+  for (int i = lane; i < U; i += 64) {
+    const Stat s = stats[(size_t)i * M + p];
+    if (s.s > 0.f) m = fmaxf(m, s.m);
+  }
+  m = wave_max(m);
+  double carry = 0.0;
+  for (int base = 0; base < U; base += 64) {
+    const double incl = wave_incl_scan(unit_mass(stats, base + lane, U, M, p, m), lane);
+    carry += __shfl(incl, 63, kWave);
+  }
+  const double Zs = carry;
+  if (lane == 0 && lse_out) *lse_out = (double)m + log(Zs);
+  if (!pick) return 0;
+  const double target = (double)u * Zs;
+
+  // crossing unit: first i with (carry + incl_i) > target, same arithmetic as Zs
+  carry = 0.0;
+  int ustar = U - 1;
+  double pre = 0.0;                       // mass of units before ustar
+  for (int base = 0; base < U; base += 64) {
+    const double incl = wave_incl_scan(unit_mass(stats, base + lane, U, M, p, m), lane);
+    const double tot = carry + incl;
+    const unsigned long long hit = __ballot(base + lane < U && tot > target);
+    if (hit) {
+      const int first = __ffsll((long long)hit) - 1;
+      const double prev = __shfl_up(tot, 1, kWave);
+      const double excl = (lane == 0) ? carry : prev;
+      ustar = base + first;
+      pre = __shfl(excl, first, kWave);
+      break;
+    }
+    carry += __shfl(incl, 63, kWave);
+    pre = carry;
+  }
+
+  // rescan the unit's rows in vocabulary order
+  const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
+  const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
+  int chosen = -1, last_pos = -1;
+  double cum = pre;
+  for (int base = rlo; base < rhi; base += 64) {
+    const int row = base + lane;
+    float l = 0.f;
+    if (mode == 0) {
+      if (row < rhi) l = S[(size_t)p * ldS + row];
+    } else {
+      // four 16-row tiles cover these 64 rows; lane (r/4)*16 + p%16 holds row r
+      constexpr int NU = ReadTile<T>::NU;
+      u32x4 bf[NU], a[NU];
+      ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
+      float mine = 0.f;
+      const int rr = lane & 15, src = (rr >> 2) * 16 + (p & 15), comp = rr & 3;
+      for (int tt = 0; tt < 4; ++tt) {
+        const int t = (base - rlo) / kTile + tlo + tt;
+        if (t >= thi) break;                         // wave-uniform
+        ReadTile<T>::load_w(W_r, V, t, lane, a);
+        const floatx4 acc = ReadTile<T>::chain(a, bf);
+        const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
+        const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
+        const float v = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
+        if ((lane >> 4) == tt) mine = v;
+      }
+      if (row < rhi) l = mine + S[(size_t)p * ldS + row];
+    }
+    const double w = (row < rhi) ? exp((double)l - (double)m) : 0.0;
+    const double tot = cum + wave_incl_scan(w, lane);
+    const unsigned long long hit = __ballot(row < rhi && tot > target);
+    const unsigned long long nz = __ballot(row < rhi && w > 0.0);
+    if (nz) last_pos = base + 63 - __clzll((long long)nz);
+    if (hit) {
+      chosen = base + __ffsll((long long)hit) - 1;
+      break;
+    }
+    cum = __shfl(tot, 63, kWave);
+  }
+  if (chosen < 0) chosen = last_pos >= 0 ? last_pos : rlo;   // rounding left no crossing
+  return chosen;
+}
+
+// One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
+// caller's seed ids); mode 1: the selection of Jacobi pass `pass`.
+template <typename T>
+__global__ __launch_bounds__(256) void k_select(
+    int mode, int pass, int batch, int B, int V, int M, const float* __restrict__ S, int ldS,
+    const T* __restrict__ W_r, const T* __restrict__ Z, const uint64_t* __restrict__ keys,
+    int nkeys, const Stat* __restrict__ stats, int ntiles, int U,
+    const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
+    const float* __restrict__ u_draft, const int32_t* __restrict__ Yprev, int32_t* __restrict__ Ynew,
+    int32_t* __restrict__ traj, double* __restrict__ lse, int32_t* __restrict__ iters,
+    int32_t* __restrict__ ctrl, uint32_t* __restrict__ err, int early_exit) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ int changed;
+  if (threadIdx.x == 0) changed = 0;
+  __syncthreads();
+  const bool sample = temp != nullptr && temp[b] != 0;
+  const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
+  for (int k = wave; k < B; k += 4) {
+    const int p = b * B + k;
+    int y = 0;
+    if (skip) {
+      y = Yprev[p];
+    } else if (mode == 0 && seed_ids != nullptr) {
+      y = seed_ids[p];
+      if (y < 0 || y >= V) {
+        if (lane == 0) atomicOr(err, XP_DEVERR_TOKEN);
+        y = 0;
+      }
+      if (sample)
+        sample_position<T>(0, p, 0.f, S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p, false);
+    } else if (!sample) {
+      uint64_t best = kKeyMin;
+      for (int i = lane; i < nkeys; i += 64) best = umax64(best, keys[(size_t)i * M + p]);
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
+      y = (int)key_index(best);
+    } else {
+      y = sample_position<T>(mode, p, u_draft[p], S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p,
+                             true);
+    }
+    if (lane == 0) {
+      Ynew[p] = y;
+      if (traj) traj[p] = y;
+      if (mode == 1 && y != Yprev[p]) atomicOr(&changed, 1);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && mode == 1 && !skip && changed == 0 && iters[b] == 0) {
+    iters[b] = pass + 1;
+    if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
+  }
+}
+
+__global__ void k_reset(int batch, int32_t* __restrict__ iters, int32_t* __restrict__ ctrl) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < batch) iters[i] = 0;
+  if (i < 2) ctrl[i] = 0;
+}
+
+__global__ void k_finish(int M, int batch, int K, const int32_t* __restrict__ Yfin,
+                         const int32_t* __restrict__ iters, int32_t* __restrict__ out_ids,
+                         int32_t* __restrict__ out_iters) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < M) out_ids[i] = Yfin[i];
+  if (out_iters && i < batch) out_iters[i] = iters[i] ? iters[i] : K;
+}
+
+__global__ void k_copy_logits(int M, int V, const float* __restrict__ S, int ldS,
+                              float* __restrict__ out) {
+  const size_t n = (size_t)M * V;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const size_t p = i / V, v = i % V;
+    out[i] = S[p * ldS + v];
+  }
+}
+
+// ---------------------------------------------------------------------------
+hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
+                         const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
+                         int32_t* out_traj, hipStream_t st) {
+  (void)K;
+  const int M = batch * h->B;
+  const int mode = pass < 0 ? 0 : 1;
+  int32_t* Yprev = h->ws.Y[(pass + 2) % 2];      // pass j reads Y[j % 2]
+  int32_t* Ynew = h->ws.Y[(pass + 1) % 2];       // and writes Y[(j+1) % 2]
+  int32_t* traj = out_traj ? out_traj + (size_t)(pass + 1) * M : nullptr;
+  if (mode == 0) {
+    hipLaunchKernelGGL(k_reset, dim3((batch + 255) / 256), dim3(256), 0, st, batch, h->ws.iters,
+                       h->ws.ctrl);
+  }
+  const int nkeys = mode == 0 ? h->lm_chunks : h->read_wgs;
+  const int U = mode == 0 ? h->lm_chunks : h->read_units;
+  const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
+  if (h->dtype == XP_BF16)
+    hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(256), 0, st, mode, pass, batch,
+                       h->B, h->V, M, h->ws.s, h->ldS, (const uint16_t*)h->W_r,
+                       (const uint16_t*)h->ws.z, h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
+                       mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
+                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early);
+  else
+    hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(256), 0, st, mode, pass, batch, h->B,
+                       h->V, M, h->ws.s, h->ldS, (const float*)h->W_r, (const float*)h->ws.z,
+                       h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
+                       mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
+                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,
+                         int32_t* out_iters, float* out_logits, hipStream_t st) {
+  const int M = batch * h->B;
+  const int n = M > batch ? M : batch;
+  hipLaunchKernelGGL(k_finish, dim3((n + 255) / 256), dim3(256), 0, st, M, batch, K,
+                     h->ws.Y[K % 2], h->ws.iters, out_ids, out_iters);
+  if (K == 0 && (flags & XP_WRITE_LOGITS) && out_logits)
+    hipLaunchKernelGGL(k_copy_logits, dim3(1024), dim3(256), 0, st, M, h->V, h->ws.s, h->ldS,
+                       out_logits);
+  return hipGetLastError();
+}
+
+}  // namespace xp

@@ -1,0 +1,245 @@
+// Vocabulary streams: the base readout s = W_lm h (the target LM head read out
+// on the drafter states, section 4.1 / Fig. 2a) and Read + Correct
+// l = s + W_r z (eqs. read, correct), each fused with the first stage of token
+// selection so that no logit row is ever written on the fast path.
+//
+// Both kernels stream their weight matrix exactly once per 16-position block,
+// row tile by row tile (16 vocabulary rows), straight from HBM into MFMA
+// operand registers; the 16 positions' activations stay in registers for the
+// whole kernel.  Selection partials leave the kernel per vocabulary unit:
+//   greedy rows   -> 64-bit argmax keys per workgroup (ties to the lowest index)
+//   sampled rows  -> (max, sum exp(l - max)) per unit, for the inverse-CDF pass.
+#include "xp_internal.h"
+#include "xp_tiles.h"
+
+namespace xp {
+
+// ---------------------------------------------------------------------------
+// A1: s = W_lm h.  Split-K across the waves of a workgroup: wave w owns k in
+// [w*KS, (w+1)*KS) and keeps the 16 positions' h for that slice in registers;
+// the per-wave 16x16 partial tiles are summed in LDS in a fixed wave order
+// (deterministic), then written as fp32 s and folded into the selection state.
+// One workgroup owns one vocabulary unit (a contiguous run of tiles).
+// ---------------------------------------------------------------------------
+template <typename T, int NU>
+__global__ __launch_bounds__(1024) void k_lmhead(
+    const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
+    float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    const uint8_t* __restrict__ temp, int B) {
+  using MF = Mfma<T>;
+  constexpr int EPB = 16 / sizeof(T);
+  constexpr int KS = NU * MF::KU;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
+  const int u = blockIdx.x, p0 = blockIdx.y * kTile;
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  const size_t kofs = (size_t)wave * KS + (lane >> 4) * EPB;
+
+  u32x4 bf[NU];
+  {
+    const int p = p0 + (lane & 15);
+    const T* xr = X + (size_t)(p < M ? p : 0) * H + kofs;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) bf[i] = (p < M) ? ld16(xr + i * MF::KU) : u32x4{0u, 0u, 0u, 0u};
+  }
+
+  __shared__ float red[16][kTile][20];   // [wave][position][row], rows padded to 20
+  const int epos = threadIdx.x >> 4, erow = threadIdx.x & 15;
+  const int ep = p0 + epos;
+  const bool eact = threadIdx.x < 256 && ep < M;
+  const bool esample = eact && temp != nullptr && temp[ep / B] != 0;
+  uint64_t best = kKeyMin;
+  Stat st = stat_empty();
+
+  auto load_tile = [&](int t, u32x4 (&a)[NU]) {
+    int row = t * kTile + (lane & 15);
+    row = row < V ? row : V - 1;
+    const T* wr = W + (size_t)row * H + kofs;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) a[i] = ld16_nt(wr + i * MF::KU);
+  };
+
+  u32x4 a[NU], an[NU];
+  if (tlo < thi) load_tile(tlo, a);
+  for (int t = tlo; t < thi; ++t) {
+    if (t + 1 < thi) load_tile(t + 1, an);
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NU; ++i) acc = MF::mma(a[i], bf[i], acc);
+    *reinterpret_cast<floatx4*>(&red[wave][lane & 15][4 * (lane >> 4)]) = acc;
+    __syncthreads();
+    if (threadIdx.x < 256) {
+      float v = 0.f;
+      for (int w = 0; w < NW; ++w) v += red[w][epos][erow];
+      const int row = t * kTile + erow;
+      if (eact && row < V) {
+        S[(size_t)ep * ldS + row] = v;
+        if (esample)
+          st = stat_merge(st, Stat{v, 1.f});
+        else
+          best = umax64(best, argmax_key(v, (uint32_t)row));
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NU; ++i) a[i] = an[i];
+  }
+  if (threadIdx.x < 256) {
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+      best = umax64(best, shfl_xor_u64(best, m));
+      Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
+      st = stat_merge(st, o);
+    }
+    if (erow == 0 && ep < M) {
+      keys[(size_t)u * M + ep] = best;
+      stats[(size_t)u * M + ep] = st;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
+// the full k range (r = 256 fits one chain of MFMAs); workgroups only combine
+// their waves' argmax keys.  Sampled rows write one (max, sum) per wave unit.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(1024) void k_read(
+    const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int ldS, int V,
+    int M, int ntiles, int U, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    const uint8_t* __restrict__ temp, int B, float* __restrict__ out_logits,
+    const int32_t* __restrict__ ctrl, int skip_when_done) {
+  if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
+  constexpr int NU = ReadTile<T>::NU;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
+  const int u = blockIdx.x * NW + wave, p0 = blockIdx.y * kTile;
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+
+  u32x4 bf[NU];
+  ReadTile<T>::load_z(Z, M, p0, lane, bf);
+  const int p = p0 + (lane & 15);
+  const bool act = p < M;
+  const bool sample = act && temp != nullptr && temp[p / B] != 0;
+  uint64_t best = kKeyMin;
+  Stat st = stat_empty();
+
+  // bf16 tiles are prefetched one tile ahead; fp32 tiles (twice the registers)
+  // are loaded in place so that the wave stays within its register budget.
+  constexpr bool kPrefetch = sizeof(T) == 2;
+  u32x4 a[NU], an[kPrefetch ? NU : 1];
+  if (kPrefetch && tlo < thi) ReadTile<T>::load_w(W, V, tlo, lane, a);
+  for (int t = tlo; t < thi; ++t) {
+    if constexpr (kPrefetch) {
+      if (t + 1 < thi) ReadTile<T>::load_w(W, V, t + 1, lane, an);
+    } else {
+      ReadTile<T>::load_w(W, V, t, lane, a);
+    }
+    const floatx4 acc = ReadTile<T>::chain(a, bf);
+    const int row0 = t * kTile + 4 * (lane >> 4);
+    if (act) {
+      const floatx4 sv = *reinterpret_cast<const floatx4*>(S + (size_t)p * ldS + row0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float l = acc[i] + sv[i];
+        const int row = row0 + i;
+        if (row < V) {
+          if (sample)
+            st = stat_merge(st, Stat{l, 1.f});
+          else
+            best = umax64(best, argmax_key(l, (uint32_t)row));
+          if (out_logits) out_logits[(size_t)p * V + row] = l;
+        }
+      }
+    }
+    if constexpr (kPrefetch) {
+#pragma unroll
+      for (int i = 0; i < NU; ++i) a[i] = an[i];
+    }
+  }
+#pragma unroll
+  for (int m = 16; m < 64; m <<= 1) {
+    best = umax64(best, shfl_xor_u64(best, m));
+    Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
+    st = stat_merge(st, o);
+  }
+  if (lane < 16 && sample) stats[(size_t)u * M + p] = st;
+
+  __shared__ uint64_t kred[16][kTile];
+  if (lane < 16) kred[wave][lane] = best;
+  __syncthreads();
+  if (threadIdx.x < kTile) {
+    uint64_t b = kKeyMin;
+    for (int w = 0; w < NW; ++w) b = umax64(b, kred[w][threadIdx.x]);
+    const int pp = p0 + threadIdx.x;
+    if (pp < M) keys[(size_t)blockIdx.x * M + pp] = b;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+// Waves per workgroup and load units per wave for a hidden width H: the k
+// range is split into NW slices of NU*KU values with 4 <= NW <= 16.
+static bool pick_lm_split(int H, int KU, int* NU, int* NW) {
+  for (int nu = 1; nu <= 16; nu *= 2) {
+    if (H % (nu * KU)) continue;
+    const int nw = H / (nu * KU);
+    if (nw >= 4 && nw <= 16) {
+      *NU = nu;
+      *NW = nw;
+      return true;
+    }
+  }
+  return false;
+}
+
+bool lm_split_ok(int H, int dtype) {
+  int nu, nw;
+  return pick_lm_split(H, dtype == XP_BF16 ? 32 : 16, &nu, &nw);
+}
+
+template <typename T>
+static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
+                                  hipStream_t st) {
+  int NU = 0, NW = 0;
+  if (!pick_lm_split(h->H, Mfma<T>::KU, &NU, &NW)) return hipErrorInvalidValue;
+  dim3 grid(h->lm_chunks, (M + kTile - 1) / kTile), block(NW * kWave);
+  auto args = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, block, 0, st, (const T*)h->W_lm, (const T*)hidden, h->V, h->H,
+                       M, h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
+                       h->B);
+  };
+  switch (NU) {
+    case 1: args(k_lmhead<T, 1>); break;
+    case 2: args(k_lmhead<T, 2>); break;
+    case 4: args(k_lmhead<T, 4>); break;
+    case 8: args(k_lmhead<T, 8>); break;
+    default: args(k_lmhead<T, 16>); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
+                         hipStream_t st) {
+  if (h->dtype == XP_BF16) return launch_lmhead_t<uint16_t>(h, M, hidden, temp, st);
+  return launch_lmhead_t<float>(h, M, hidden, temp, st);
+}
+
+hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
+                       float* out_logits, hipStream_t st) {
+  (void)pass;
+  const int M = batch * h->B;
+  dim3 grid(h->read_wgs, (M + kTile - 1) / kTile), block(kReadWaves * kWave);
+  const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
+  if (h->dtype == XP_BF16)
+    hipLaunchKernelGGL((k_read<uint16_t>), grid, block, 0, st, (const uint16_t*)h->W_r,
+                       (const uint16_t*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles,
+                       h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl,
+                       skip);
+  else
+    hipLaunchKernelGGL((k_read<float>), grid, block, 0, st, (const float*)h->W_r,
+                       (const float*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles, h->read_units,
+                       h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl, skip);
+  return hipGetLastError();
+}
+
+}  // namespace xp

@@ -1,0 +1,339 @@
+// Block verification (section 3.1).
+//
+// Greedy rows: n = longest prefix with y_i = t_i, next = t_{n+1}.
+// Sampled rows (temperature 1), speculative accept / reject:
+//   accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k = softmax(l_k) of the refine's
+//   last pass, p_k = softmax(target logits after the prefix y_{<k});
+//   at the first rejection next ~ max(0, p_k - q_k) (p_k if that has no mass),
+//   if all B are accepted next ~ p_{B+1}; both by inverse CDF at u_res.
+// Kernels: target log-sum-exp per row -> accept scan -> residual mass per
+// vocabulary unit (one W_r stream for all sequences) -> crossing unit + rescan.
+#include "xp_internal.h"
+#include "xp_tiles.h"
+
+namespace xp {
+
+// lseT[b][k] = log sum_v exp(T[b][k][v]) for sampled rows, k = 0..B.
+__global__ __launch_bounds__(256) void k_vtarget(const float* __restrict__ tl, int B, int V,
+                                                 const uint8_t* __restrict__ temp,
+                                                 double* __restrict__ lseT) {
+  const int k = blockIdx.x, b = blockIdx.y;
+  if (temp == nullptr || temp[b] == 0) return;
+  const float* row = tl + ((size_t)b * (B + 1) + k) * V;
+  float m = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, row[v]);
+  __shared__ float sm[256];
+  __shared__ double sd[256];
+  sm[threadIdx.x] = m;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sm[threadIdx.x] = fmaxf(sm[threadIdx.x], sm[threadIdx.x + s]);
+    __syncthreads();
+  }
+  m = sm[0];
+  double acc = 0.0;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) acc += exp((double)row[v] - (double)m);
+  sd[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sd[threadIdx.x] += sd[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) lseT[(size_t)b * (B + 1) + k] = (double)m + log(sd[0]);
+}
+
+// l = s (+ W_r z) for position p at vocabulary row v, through the Read tile of
+// the stream (all 64 lanes take part; every lane gets the value).
+template <typename T>
+__device__ float refined_logit(int with_read, const float* __restrict__ S, int ldS,
+                               const T* __restrict__ W_r, const T* __restrict__ Z, int M, int V,
+                               int p, int v) {
+  const int lane = threadIdx.x & 63;
+  float d = 0.f;
+  if (with_read) {
+    constexpr int NU = ReadTile<T>::NU;
+    u32x4 bf[NU], a[NU];
+    ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
+    ReadTile<T>::load_w(W_r, V, v / 16, lane, a);
+    const floatx4 acc = ReadTile<T>::chain(a, bf);
+    const int rr = v & 15, src = (rr >> 2) * 16 + (p & 15);
+    const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
+    const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
+    const int comp = rr & 3;
+    d = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
+  }
+  return with_read ? d + S[(size_t)p * ldS + v] : S[(size_t)p * ldS + v];
+}
+
+// One wave per sequence: accept scan.  vpos[b] = rejected position, or B.
+template <typename T>
+__global__ __launch_bounds__(64) void k_vaccept(
+    int B, int V, int M, int with_read, const int32_t* __restrict__ draft,
+    const uint8_t* __restrict__ temp, const int32_t* __restrict__ tids,
+    const float* __restrict__ tl, const float* __restrict__ racc, const float* __restrict__ S,
+    int ldS, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
+    const double* __restrict__ lseT, int32_t* __restrict__ vpos, int32_t* __restrict__ out_n,
+    int32_t* __restrict__ out_next, uint32_t* __restrict__ err) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const bool sample = temp != nullptr && temp[b] != 0;
+  int bad = 0;
+  if (!sample) {
+    if (lane == 0) {
+      int n = 0;
+      while (n < B) {
+        int t = tids[(size_t)b * (B + 1) + n];
+        if (t < 0 || t >= V) bad = 1;
+        if (draft[b * B + n] != t) break;
+        ++n;
+      }
+      int nx = tids[(size_t)b * (B + 1) + n];
+      if (nx < 0 || nx >= V) {
+        bad = 1;
+        nx = 0;
+      }
+      out_n[b] = n;
+      out_next[b] = nx;
+      vpos[b] = -1;
+      if (bad) atomicOr(err, XP_DEVERR_TOKEN);
+    }
+    return;
+  }
+  int n = B;
+  for (int k = 0; k < B; ++k) {
+    const int p = b * B + k;
+    int y = draft[p];
+    if (y < 0 || y >= V) {
+      bad = 1;
+      y = 0;
+    }
+    const float l = refined_logit<T>(with_read, S, ldS, W_r, Z, M, V, p, y);
+    const double q = exp((double)l - lse[p]);
+    const double pt =
+        exp((double)tl[((size_t)b * (B + 1) + k) * V + y] - lseT[(size_t)b * (B + 1) + k]);
+    if (!((double)racc[p] * q <= pt)) {
+      n = k;
+      break;
+    }
+  }
+  if (lane == 0) {
+    out_n[b] = n;
+    vpos[b] = n;
+    if (bad) atomicOr(err, XP_DEVERR_TOKEN);
+  }
+}
+
+// Resampling weight of vocabulary row v for sequence b: the residual
+// max(0, p - q) at the rejected position, or p_{B+1} for the bonus token.
+__device__ __forceinline__ void resample_weights(float tlv, double lseTk, bool resid, float l,
+                                                 double lsep, double* res, double* pw) {
+  const double pv = exp((double)tlv - lseTk);
+  *pw = pv;
+  if (resid) {
+    const double qv = exp((double)l - lsep);
+    *res = pv > qv ? pv - qv : 0.0;
+  } else {
+    *res = pv;
+  }
+}
+
+// Residual (and plain p) mass per vocabulary unit, one W_r stream for up to
+// 16 sequences per workgroup column; lanes of greedy sequences idle.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_vresid(
+    int batch, int B, int V, int M, int with_read, int ntiles, int U,
+    const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
+    const float* __restrict__ tl, const float* __restrict__ S, int ldS, const T* __restrict__ W_r,
+    const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
+    double* __restrict__ vmass) {
+  constexpr int NU = ReadTile<T>::NU;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
+  const int u = blockIdx.x * NW + wave;
+  const int b = blockIdx.y * 16 + (lane & 15);
+  const bool act = b < batch && temp != nullptr && temp[b] != 0;
+  const int k = act ? vpos[b] : 0;
+  const bool resid = act && k < B;
+  const int p = b * B + (k < B ? k : 0);
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  u32x4 bf[NU], a[NU];
+  ReadTile<T>::load_z_row(Z, resid ? p : -1, lane, bf);
+  const float* trow = tl + ((size_t)(act ? b : 0) * (B + 1) + k) * V;
+  const double lk = act ? lseT[(size_t)b * (B + 1) + k] : 0.0;
+  const double lp = resid ? lse[p] : 0.0;
+  double mr = 0.0, mp = 0.0;
+  for (int t = tlo; t < thi; ++t) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (with_read) {
+      ReadTile<T>::load_w(W_r, V, t, lane, a);
+      acc = ReadTile<T>::chain(a, bf);
+    }
+    if (act) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = t * kTile + 4 * (lane >> 4) + i;
+        if (row < V) {
+          const float l = resid ? acc[i] + S[(size_t)p * ldS + row] : 0.f;
+          double res, pw;
+          resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
+          mr += res;
+          mp += pw;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 16; m < 64; m <<= 1) {
+    mr += __shfl_xor(mr, m, kWave);
+    mp += __shfl_xor(mp, m, kWave);
+  }
+  if (lane < 16 && act) {
+    vmass[((size_t)u * batch + b) * 2 + 0] = mr;
+    vmass[((size_t)u * batch + b) * 2 + 1] = mp;
+  }
+}
+
+__device__ __forceinline__ double wave_scan_d(double x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const double y = __shfl_up(x, off, kWave);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+// One wave per sampled sequence: crossing unit, then an in-order rescan.
+template <typename T>
+__global__ __launch_bounds__(64) void k_vfinal(
+    int batch, int B, int V, int M, int with_read, int ntiles, int U,
+    const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
+    const float* __restrict__ tl, const float* __restrict__ S, int ldS, const T* __restrict__ W_r,
+    const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
+    const double* __restrict__ vmass, const float* __restrict__ u_res,
+    int32_t* __restrict__ out_next) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  if (temp == nullptr || temp[b] == 0) return;
+  const int k = vpos[b];
+  bool resid = k < B;
+  const int p = b * B + (k < B ? k : 0);
+  // residual with no mass falls back to p (component 1)
+  int comp = 0;
+  {
+    double c = 0.0;
+    for (int base = 0; base < U; base += 64) {
+      const int i = base + lane;
+      const double w = i < U ? vmass[((size_t)i * batch + b) * 2] : 0.0;
+      c += __shfl(wave_scan_d(w, lane), 63, kWave);
+    }
+    if (!(c > 0.0)) comp = 1;
+  }
+  const bool use_resid = resid && comp == 0;
+  double carry = 0.0;
+  for (int base = 0; base < U; base += 64) {
+    const int i = base + lane;
+    const double w = i < U ? vmass[((size_t)i * batch + b) * 2 + comp] : 0.0;
+    carry += __shfl(wave_scan_d(w, lane), 63, kWave);
+  }
+  const double target = (double)u_res[b] * carry;
+  double run = 0.0, pre = 0.0;
+  int ustar = U - 1;
+  for (int base = 0; base < U; base += 64) {
+    const int i = base + lane;
+    const double w = i < U ? vmass[((size_t)i * batch + b) * 2 + comp] : 0.0;
+    const double tot = run + wave_scan_d(w, lane);
+    const unsigned long long hit = __ballot(i < U && tot > target);
+    if (hit) {
+      const int first = __ffsll((long long)hit) - 1;
+      const double prev = __shfl_up(tot, 1, kWave);
+      const double excl = lane == 0 ? run : prev;
+      ustar = base + first;
+      pre = __shfl(excl, first, kWave);
+      break;
+    }
+    run = __shfl(tot, 63, kWave);
+    pre = run;
+  }
+  const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
+  const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
+  const float* trow = tl + ((size_t)b * (B + 1) + k) * V;
+  const double lk = lseT[(size_t)b * (B + 1) + k];
+  const double lp = resid ? lse[p] : 0.0;
+  int chosen = -1, last_pos = -1;
+  double cum = pre;
+  for (int base = rlo; base < rhi; base += 64) {
+    const int row = base + lane;
+    float mine = 0.f;
+    if (resid && with_read) {
+      constexpr int NU = ReadTile<T>::NU;
+      u32x4 bf[NU], a[NU];
+      ReadTile<T>::load_z_row(Z, p, lane, bf);
+      const int rr = lane & 15, src = (rr >> 2) * 16, cp = rr & 3;
+      for (int tt = 0; tt < 4; ++tt) {
+        const int t = (base - rlo) / kTile + tlo + tt;
+        if (t >= thi) break;
+        ReadTile<T>::load_w(W_r, V, t, lane, a);
+        const floatx4 acc = ReadTile<T>::chain(a, bf);
+        const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
+        const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
+        const float v = cp == 0 ? c0 : cp == 1 ? c1 : cp == 2 ? c2 : c3;
+        if ((lane >> 4) == tt) mine = v;
+      }
+    }
+    double w = 0.0;
+    if (row < rhi) {
+      const float l = resid ? mine + S[(size_t)p * ldS + row] : 0.f;
+      double res, pw;
+      resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
+      w = use_resid ? res : pw;
+    }
+    const double tot = cum + wave_scan_d(w, lane);
+    const unsigned long long hit = __ballot(row < rhi && tot > target);
+    const unsigned long long nz = __ballot(row < rhi && w > 0.0);
+    if (nz) last_pos = base + 63 - __clzll((long long)nz);
+    if (hit) {
+      chosen = base + __ffsll((long long)hit) - 1;
+      break;
+    }
+    cum = __shfl(tot, 63, kWave);
+  }
+  if (chosen < 0) chosen = last_pos >= 0 ? last_pos : rlo;
+  if (lane == 0) out_next[b] = chosen;
+}
+
+// ---------------------------------------------------------------------------
+template <typename T>
+static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const uint8_t* temp,
+                           const int32_t* tids, const float* tl, const float* racc,
+                           const float* ures, int32_t* out_n, int32_t* out_next, hipStream_t st) {
+  const int M = batch * h->B;
+  const int with_read = h->state_k0 ? 0 : 1;
+  if (temp)
+    hipLaunchKernelGGL(k_vtarget, dim3(h->B + 1, batch), dim3(256), 0, st, tl, h->B, h->V, temp,
+                       h->ws.vstat);
+  hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
+                     draft, temp, tids, tl, racc, h->ws.s, h->ldS, (const T*)h->W_r,
+                     (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
+                     h->ws.err);
+  if (temp) {
+    hipLaunchKernelGGL((k_vresid<T>), dim3(h->read_wgs, (batch + 15) / 16),
+                       dim3(kReadWaves * kWave), 0, st, batch, h->B, h->V, M, with_read,
+                       h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s, h->ldS,
+                       (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vmass);
+    hipLaunchKernelGGL((k_vfinal<T>), dim3(batch), dim3(64), 0, st, batch, h->B, h->V, M,
+                       with_read, h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s,
+                       h->ldS, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
+                       h->ws.vmass, ures, out_next);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_verify(xp_handle* h, int batch, const int32_t* draft_ids, const uint8_t* temp,
+                         const int32_t* target_ids, const float* target_logits,
+                         const float* r_accept, const float* u_res, int32_t* out_n,
+                         int32_t* out_next, hipStream_t st) {
+  if (h->dtype == XP_BF16)
+    return verify_t<uint16_t>(h, batch, draft_ids, temp, target_ids, target_logits, r_accept,
+                              u_res, out_n, out_next, st);
+  return verify_t<float>(h, batch, draft_ids, temp, target_ids, target_logits, r_accept, u_res,
+                         out_n, out_next, st);
+}
+
+}  // namespace xp

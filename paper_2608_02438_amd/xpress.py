@@ -1,0 +1,231 @@
+"""Python binding of libxpress.so (the C ABI in include/xpress.h).
+
+Argument marshalling only: every step of the refine + verify path runs in the
+HIP kernels of the library.  PyTorch is used for device memory and streams.
+The library must have been built (``python -m paper_2608_02438_amd.build``);
+there is no fallback implementation, and loading fails loudly without it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libxpress.so")
+
+XP_OK, XP_EINVAL, XP_EUNSUPPORTED, XP_EHIP, XP_ENOMEM = 0, -1, -2, -3, -4
+XP_F32, XP_BF16 = 0, 1
+XP_EARLY_EXIT, XP_WRITE_LOGITS = 1, 2
+XP_DEVERR_TOKEN = 1
+
+EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
+           "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
+           "xp_timing_read")
+STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
+
+
+class XpError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_status_name(status)}: {msg}")
+        self.status = status
+
+
+class _Weights(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("r", ctypes.c_int32), ("V", ctypes.c_int32),
+                ("B", ctypes.c_int32), ("dtype", ctypes.c_int32)] + [
+        (n, ctypes.c_void_p) for n in ("W_lm", "W_h", "W_g", "W_e", "W_in", "L", "W_1", "W_2", "W_r")]
+
+
+WEIGHT_NAMES = ("W_lm", "W_h", "W_g", "W_e", "W_in", "L", "W_1", "W_2", "W_r")
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libxpress.so and declare its signatures (no GPU work)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_02438_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i32, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32
+    L.xp_create.argtypes = [ctypes.POINTER(_Weights), i32, ctypes.POINTER(vp)]
+    L.xp_create.restype = i32
+    L.xp_destroy.argtypes = [vp]
+    L.xp_destroy.restype = None
+    L.xp_last_error.argtypes = [vp]
+    L.xp_last_error.restype = ctypes.c_char_p
+    L.xp_status_string.argtypes = [i32]
+    L.xp_status_string.restype = ctypes.c_char_p
+    L.xp_refine_block.argtypes = [vp, i32, vp, vp, vp, vp, vp, i32, u32, vp, vp, vp, vp, vp]
+    L.xp_refine_block.restype = i32
+    L.xp_verify_block.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.xp_verify_block.restype = i32
+    L.xp_device_errors.argtypes = [vp, ctypes.POINTER(u32), vp]
+    L.xp_device_errors.restype = i32
+    L.xp_timing_enable.argtypes = [vp, u32, i32]
+    L.xp_timing_enable.restype = i32
+    L.xp_timing_read.argtypes = [vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
+    L.xp_timing_read.restype = i32
+    _lib = L
+    return L
+
+
+def _status_name(s: int) -> str:
+    try:
+        return load_library().xp_status_string(s).decode()
+    except Exception:  # pragma: no cover
+        return str(s)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return int(t.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def bf16_tensor(bits: np.ndarray, device="cuda"):
+    """Device bf16 tensor from bf16 bit patterns (uint16)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def device_tensor(x: np.ndarray, device="cuda"):
+    """Device tensor of a stored input: uint16 -> bf16, float32 -> float32, ints as is."""
+    import torch
+    if x.dtype == np.uint16:
+        return bf16_tensor(x, device)
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device)
+
+
+@dataclass
+class RefineOut:
+    ids: object
+    iters: object
+    logits: Optional[object]
+    traj: Optional[object]
+
+
+class Refiner:
+    """One xp_handle: weights on the device plus the workspace for max_batch sequences."""
+
+    def __init__(self, weights: Dict[str, object], H: int, r: int, V: int, B: int,
+                 max_batch: int):
+        import torch
+        L = load_library()
+        w0 = weights["W_lm"]
+        self.dtype = XP_BF16 if w0.dtype == torch.bfloat16 else XP_F32
+        tdt = torch.bfloat16 if self.dtype == XP_BF16 else torch.float32
+        self.tdtype = tdt
+        self.H, self.r, self.V, self.B, self.max_batch = H, r, V, B, max_batch
+        self.device = w0.device
+        self._keep = {}
+        st = _Weights(H=H, r=r, V=V, B=B, dtype=self.dtype)
+        for n in WEIGHT_NAMES:
+            t = weights[n]
+            if t.dtype != tdt or not t.is_contiguous() or t.device != self.device:
+                raise ValueError(f"{n}: expected a contiguous {tdt} tensor on {self.device}")
+            self._keep[n] = t
+            setattr(st, n, t.data_ptr())
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            s = L.xp_create(ctypes.byref(st), max_batch, ctypes.byref(h))
+        if s != XP_OK:
+            raise XpError(s, L.xp_last_error(None).decode())
+        self._h = h
+        self._L = L
+
+    # ------------------------------------------------------------------
+    def _check(self, s: int):
+        if s != XP_OK:
+            raise XpError(s, self._L.xp_last_error(self._h).decode())
+
+    def refine_block(self, hidden, anchor, seed_ids=None, temp=None, u_draft=None, K: int = 6,
+                     early_exit: bool = False, write_logits: bool = False,
+                     want_traj: bool = False, out: Optional[RefineOut] = None,
+                     stream=None) -> RefineOut:
+        import torch
+        batch = hidden.shape[0]
+        if (tuple(hidden.shape) != (batch, self.B, self.H) or hidden.dtype != self.tdtype
+                or not hidden.is_contiguous() or hidden.device != self.device):
+            raise ValueError(f"hidden must be a contiguous [{batch}][{self.B}][{self.H}] "
+                             f"{self.tdtype} tensor on {self.device}")
+        for name, t, dt in (("anchor", anchor, torch.int32), ("seed_ids", seed_ids, torch.int32),
+                            ("temp", temp, torch.uint8), ("u_draft", u_draft, torch.float32)):
+            if t is not None and (t.dtype != dt or not t.is_contiguous() or t.device != self.device):
+                raise ValueError(f"{name}: expected a contiguous {dt} tensor on {self.device}")
+        if out is None:
+            dev = self.device
+            out = RefineOut(
+                ids=torch.empty((batch, self.B), dtype=torch.int32, device=dev),
+                iters=torch.empty((batch,), dtype=torch.int32, device=dev),
+                logits=(torch.empty((batch, self.B, self.V), dtype=torch.float32, device=dev)
+                        if write_logits else None),
+                traj=(torch.empty((K + 1, batch, self.B), dtype=torch.int32, device=dev)
+                      if want_traj else None))
+        flags = (XP_EARLY_EXIT if early_exit else 0) | (XP_WRITE_LOGITS if write_logits else 0)
+        s = self._L.xp_refine_block(
+            self._h, batch, _ptr(hidden), _ptr(anchor), _ptr(seed_ids), _ptr(temp),
+            _ptr(u_draft), K, flags, _ptr(out.ids), _ptr(out.iters),
+            _ptr(out.logits) if write_logits else None, _ptr(out.traj), _stream(stream))
+        self._check(s)
+        return out
+
+    def verify_block(self, draft_ids, target_ids, temp=None, target_logits=None, r_accept=None,
+                     u_resample=None, out=None, stream=None):
+        import torch
+        batch = draft_ids.shape[0]
+        if out is None:
+            out = (torch.empty((batch,), dtype=torch.int32, device=self.device),
+                   torch.empty((batch,), dtype=torch.int32, device=self.device))
+        s = self._L.xp_verify_block(
+            self._h, batch, _ptr(draft_ids), _ptr(temp), _ptr(target_ids), _ptr(target_logits),
+            _ptr(r_accept), _ptr(u_resample), _ptr(out[0]), _ptr(out[1]), _stream(stream))
+        self._check(s)
+        return out
+
+    def device_errors(self, stream=None) -> int:
+        v = ctypes.c_uint32(0)
+        self._check(self._L.xp_device_errors(self._h, ctypes.byref(v), _stream(stream)))
+        return int(v.value)
+
+    def timing_enable(self, stages=("lmhead",), capacity: int = 4096):
+        """Record HIP events around the named stages of every following call."""
+        mask = 0
+        for n in stages:
+            mask |= 1 << STAGES.index(n)
+        self._check(self._L.xp_timing_enable(self._h, mask, capacity))
+
+    def timing_read(self):
+        """{stage: (total ms, recorded launches)} since the last read; synchronizes."""
+        ms = (ctypes.c_float * len(STAGES))()
+        n = (ctypes.c_int32 * len(STAGES))()
+        self._check(self._L.xp_timing_read(self._h, ms, n))
+        return {s: (float(ms[i]), int(n[i])) for i, s in enumerate(STAGES)}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._L.xp_destroy(self._h)
+            self._h = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def refiner_from_arrays(weights: Dict[str, np.ndarray], H, r, V, B, max_batch, device="cuda"):
+    """Upload stored weights (bf16 bits or float32) and create a Refiner."""
+    return Refiner({n: device_tensor(weights[n], device) for n in WEIGHT_NAMES}, H, r, V, B,
+                   max_batch)

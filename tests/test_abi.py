@@ -1,0 +1,78 @@
+"""The C ABI on the host: the library loads, exports what include/xpress.h
+declares, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_02438_amd import xpress as X
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "xpress.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(xp_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(X.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = X.load_library()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def _weights(**kw):
+    w = X._Weights(H=4096, r=256, V=151936, B=16, dtype=X.XP_BF16)
+    for n in X.WEIGHT_NAMES:
+        setattr(w, n, 0x1000)          # never dereferenced: validation fails first
+    for k, v in kw.items():
+        setattr(w, k, v)
+    return w
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(r=128), X.XP_EUNSUPPORTED),
+    (dict(B=33), X.XP_EUNSUPPORTED),
+    (dict(H=4000), X.XP_EUNSUPPORTED),
+    (dict(H=16384), X.XP_EUNSUPPORTED),
+    (dict(dtype=7), X.XP_EINVAL),
+    (dict(V=0), X.XP_EINVAL),
+    (dict(W_r=None), X.XP_EINVAL),
+    (dict(W_lm=None), X.XP_EINVAL),
+])
+def test_create_rejects_bad_arguments_without_a_gpu(change, status):
+    L = X.load_library()
+    h = ctypes.c_void_p(0)
+    w = _weights(**change)
+    assert L.xp_create(ctypes.byref(w), 1, ctypes.byref(h)) == status
+    assert not h.value
+    assert L.xp_last_error(None)
+
+
+def test_create_rejects_bad_batch():
+    L = X.load_library()
+    h = ctypes.c_void_p(0)
+    assert L.xp_create(ctypes.byref(_weights()), 0, ctypes.byref(h)) == X.XP_EINVAL
+    assert L.xp_create(ctypes.byref(_weights()), 5000, ctypes.byref(h)) == X.XP_EINVAL
+    assert L.xp_create(None, 1, ctypes.byref(h)) == X.XP_EINVAL
+    assert L.xp_create(ctypes.byref(_weights()), 1, None) == X.XP_EINVAL
+
+
+def test_calls_on_a_null_handle_are_rejected():
+    L = X.load_library()
+    assert L.xp_refine_block(None, 1, 1, 1, None, None, None, 6, 0, 1, None, None, None, None) == X.XP_EINVAL
+    assert L.xp_verify_block(None, 1, 1, None, 1, None, None, None, 1, 1, None) == X.XP_EINVAL
+    assert L.xp_device_errors(None, None, None) == X.XP_EINVAL
+    L.xp_destroy(None)
+
+
+def test_status_strings():
+    L = X.load_library()
+    assert L.xp_status_string(X.XP_EHIP) == b"XP_EHIP"
+    assert L.xp_status_string(X.XP_OK) == b"XP_OK"

@@ -1,0 +1,172 @@
+"""Device path vs the fp64 oracle, through the C ABI (needs an MI355X).
+
+Small cases span several vocabulary tiles and a ragged tail (V not a multiple
+of 16) and use stress weights so that Jacobi trajectories take several passes;
+the full-size cases run the workloads' own shapes and launch configuration.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from synth.configs import TINY_F32, QWEN_B1, QWEN_B8_T1, QWEN_B32, QWEN_B64_MIXED
+
+from _parity import (E_LOGIT, check_refine, check_verify, custom_problem, make_refiner,
+                     run_device, upload, workload_problem)
+
+pytestmark = pytest.mark.gpu
+
+STRESS = dict(W_e=1.0, W_r=0.3, L=0.3, W_in=0.08, W_1=0.08, W_2=0.06)
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _verify(ref, prob, run, dev, target_ids):
+    import torch
+    from paper_2608_02438_amd.xpress import device_tensor
+    n, nx = ref.verify_block(torch.from_numpy(run.ids).cuda(), device_tensor(target_ids),
+                             temp=dev["temp"], target_logits=dev["target_logits"],
+                             r_accept=dev["r_accept"], u_resample=dev["u_res"])
+    torch.cuda.synchronize()
+    return n.cpu().numpy(), nx.cpu().numpy()
+
+
+def _full_check(prob, ref, dev, seqs=None, K=None, min_exact=1.0):
+    run = run_device(ref, prob, dev, K=K)
+    tally, finals = check_refine(prob, run, seqs=seqs)
+    _say(f"  decisions={tally.decisions} exact={tally.exact} excused={tally.excused} "
+         f"seq_exact={tally.seq_exact}/{tally.seqs} max|dl|={tally.max_logit_err:.3g}")
+    assert tally.exact >= min_exact * tally.decisions
+    seqs = list(range(prob.batch)) if seqs is None else seqs
+    target_ids = prob.inp.target_ids(run.ids)
+    n, nx = _verify(ref, prob, run, dev, target_ids)
+    exc = check_verify(prob, run, finals, n, nx, target_ids, seqs)
+    _say(f"  verify: n={n[seqs].tolist()[:8]} excused={exc}")
+    return run, tally
+
+
+# ---------------------------------------------------------------- tiny ------
+
+def test_tiny_f32_workload_matches_oracle_and_sequential_decode():
+    _say("case: tiny fp32 workload H=256 V=1024 B=8 K=8, seeded ids")
+    prob = workload_problem(TINY_F32)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    run, tally = _full_check(prob, ref, dev)
+    assert tally.seq_exact == tally.seqs
+    # Theorem 1: with K = B passes the block is the sequential decode
+    P = O.Params.from_arrays(prob.weights)
+    s = O.base_logits(P.W_lm, prob.inp.h[0])
+    ystar = O.sequential_decode(P, s, prob.inp.h[0], int(prob.inp.anchor[0]))
+    assert np.array_equal(run.ids[0], ystar)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stress_greedy_ragged_vocab(dtype):
+    _say(f"case: stress greedy {dtype} H=512 V=1000 B=16 batch=3 K=6")
+    prob = custom_problem(dtype, H=512, V=1000, B=16, batch=3, K=6, sigmas=STRESS, seed=1)
+    ref = make_refiner(prob)
+    run, tally = _full_check(prob, ref, upload(prob), min_exact=0.97)
+    assert run.iters.max() >= 3, "stress weights should need several passes"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stress_sampling_mixed_rows(dtype):
+    _say(f"case: stress mixed-temperature {dtype} H=256 V=777 B=8 batch=4 K=8")
+    prob = custom_problem(dtype, H=256, V=777, B=8, batch=4, K=8, sigmas=STRESS, temp="mixed",
+                          seed=2)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
+def test_block_of_one_and_K0():
+    _say("case: B=1 and K=0")
+    prob = custom_problem("bf16", H=256, V=300, B=1, batch=5, K=3, sigmas=STRESS, seed=3)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    _full_check(prob, ref, dev, min_exact=0.97)
+    run0 = run_device(ref, prob, dev, K=0)
+    tally, _ = check_refine(prob, run0)
+    assert np.array_equal(run0.ids, run0.traj[0]) and (run0.iters == 0).all()
+
+
+def test_seed_given_sampled_and_verify_k0():
+    _say("case: seeded ids, sampled rows, K=0 verify (q = softmax(s))")
+    prob = custom_problem("bf16", H=256, V=500, B=4, batch=6, K=0, sigmas=STRESS, temp="sample",
+                          seed=4, seed_given=True)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob))
+
+
+# ------------------------------------------------------------ invariants -----
+
+def test_early_exit_run_to_run_and_batch_invariance():
+    import torch
+    _say("case: invariants (early exit, bit-identical reruns, batch invariance)")
+    prob = custom_problem("bf16", H=512, V=2000, B=16, batch=4, K=8, sigmas=STRESS, temp="mixed",
+                          seed=5)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    a = run_device(ref, prob, dev)
+    b = run_device(ref, prob, dev)
+    assert np.array_equal(a.ids, b.ids) and np.array_equal(a.logits, b.logits)
+    c = run_device(ref, prob, dev, early_exit=True, write_logits=False)
+    assert np.array_equal(a.ids, c.ids) and np.array_equal(a.iters, c.iters)
+    # sequence 2 alone equals sequence 2 inside the batch
+    one = {k: (v[2:3].contiguous() if v is not None and v.dim() > 0 and v.shape[0] == 4 else v)
+           for k, v in dev.items()}
+    out = ref.refine_block(one["hidden"], one["anchor"], temp=one["temp"], u_draft=one["u_draft"],
+                           K=prob.K, write_logits=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.ids.cpu().numpy()[0], a.ids[2])
+    assert np.array_equal(out.logits.cpu().numpy()[0], a.logits[2])
+
+
+def test_out_of_range_token_sets_device_error():
+    import torch
+    _say("case: out-of-range anchor")
+    prob = custom_problem("f32", H=256, V=100, B=4, batch=2, K=2, seed=6)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    assert ref.device_errors() == 0
+    dev["anchor"] = torch.tensor([5, 1000], dtype=torch.int32, device="cuda")
+    run_device(ref, prob, dev)
+    assert ref.device_errors() & 1
+    assert ref.device_errors() == 0          # the read cleared it
+
+
+# ------------------------------------------------------------- full size -----
+
+@pytest.fixture(scope="module")
+def qwen_b1():
+    prob = workload_problem(QWEN_B1)
+    return prob, make_refiner(prob), upload(prob)
+
+
+def test_qwen3_shape_batch1_greedy(qwen_b1):
+    _say("case: Qwen3-8B shape, batch 1, B=16, greedy, K=6 (bench workload)")
+    prob, ref, dev = qwen_b1
+    run, tally = _full_check(prob, ref, dev, min_exact=0.99)
+
+
+def test_qwen3_shape_batch8_sampled():
+    _say("case: Qwen3-8B shape, batch 8, B=16, temperature 1, K=6")
+    prob = workload_problem(QWEN_B8_T1)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.8)
+
+
+def test_qwen3_shape_batch32_greedy_sampled_sequences():
+    _say("case: Qwen3-8B shape, batch 32, B=16, greedy (4 sequences checked)")
+    prob = workload_problem(QWEN_B32)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), seqs=[0, 9, 22, 31], min_exact=0.99)
+
+
+def test_qwen3_shape_batch64_block32_mixed_sampled_sequences():
+    _say("case: Qwen3-8B shape, batch 64, B=32, mixed rows (4 sequences checked)")
+    prob = workload_problem(QWEN_B64_MIXED)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), seqs=[0, 1, 36, 63], min_exact=0.8)
