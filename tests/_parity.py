@@ -6,19 +6,26 @@ Exactness rules
     equal the oracle's, except where a decision is a near-tie that the device's
     fp32 arithmetic may legitimately resolve the other way;
   * a near-tie is judged against the oracle's own fp64 logits computed from the
-    device's iterate (so one flipped token never excuses the rest of the block):
-    greedy: the gap l[y_oracle] - l[y_device] is at most 2E; sampled: u*Z lies
-    within 4E*Z of the device token's CDF interval; E bounds |l_device - l_exact|;
+    device's iterate (so one flipped token never excuses the rest of the block),
+    with an element-wise bound E[k][v] on |l_device - l_exact|:
+      greedy:  l[y_oracle] - l[y_device] <= E[y_oracle] + E[y_device];
+      sampled: every weight e^(l - max) moves by a factor within e^(+-2 Emax), so
+               the device token's CDF interval, widened by e^(+-4 Emax), must
+               contain u (Emax = max_v E[k][v]);
   * E is not trusted blindly: the last pass's logits are compared element by
     element and must stay within E.
 
-E for bf16 weights: the refined logits carry (i) the fp32 accumulation error of
-s = W_lm h over H = 4096 products (about 1e-6 here) and (ii) the bf16 rounding
-point of z, where an fp32 z within rounding error of a bf16 tie can round to
-the neighbouring value: one bf16 ulp of |z| <= 1 is <= 2^-8, times
-|W_r| <= 5 sigma = 0.1, gives 4e-4 per flipped element.  E = 2e-3 covers a few
-such flips and stays ten times below the 2e-2 logit tolerance.  For fp32
-weights there is no rounding point and E = 1e-5 bounds the fp32 accumulation.
+The bound E (fp32 unit roundoff u = 2^-24, probabilistic dot-product bound
+lambda sqrt(n) u sum|terms| with lambda = 6, sum|w h| <= |w|_2 |h|_2):
+    6 u sqrt(H) |W_lm[v]|_2 |h_k|_2           base readout s, H products
+  + 6 u 16 (|W_r| |z_k|)[v]                    Read, r = 256 products
+  + u |l[k][v]|                                final add and fp32 rounding
+  + bf16: (|W_r| (c_k * ulp(z_k)))[v]           z elements whose fp64 value lies
+          within 2^-16 |z| of a bf16 rounding midpoint may round the other way
+          on the device (c = 1 there); every other z element rounds identically
+    fp32: 2^-16 (|W_r| |z_k|)[v]                fp32 error of z itself
+The 2^-16 relative budget for z covers the fp32 error of the stages that make
+z (sums of up to H products); the device is far more accurate than that.
 """
 from __future__ import annotations
 
@@ -30,7 +37,8 @@ import oracle as O
 import synth
 from synth import gen
 
-E_LOGIT = {"bf16": 2e-3, "f32": 1e-5}
+U32 = 2.0 ** -24
+Z_REL = 2.0 ** -16
 
 
 @dataclass
@@ -125,6 +133,7 @@ class Tally:
     exact: int = 0
     excused: int = 0
     max_logit_err: float = 0.0
+    max_err_over_bound: float = 0.0
     seq_exact: int = 0
     seqs: int = 0
 
@@ -132,57 +141,111 @@ class Tally:
         for f in ("decisions", "exact", "excused", "seq_exact", "seqs"):
             setattr(self, f, getattr(self, f) + getattr(o, f))
         self.max_logit_err = max(self.max_logit_err, o.max_logit_err)
+        self.max_err_over_bound = max(self.max_err_over_bound, o.max_err_over_bound)
 
 
-def _decision_ok(l, y_dev, sample, u, E):
+def lm_row_norms(P):
+    """|W_lm[v]|_2 for every vocabulary row (cached on the Params object)."""
+    if getattr(P, "_lm_norm", None) is None:
+        V = P.W_lm.shape[0]
+        out = np.empty(V)
+        for v0 in range(0, V, 8192):
+            w = O.to_f64(P.W_lm[v0:v0 + 8192])
+            out[v0:v0 + 8192] = np.sqrt(np.einsum("ij,ij->i", w, w))
+        P._lm_norm = out
+        P._abs_wr = np.abs(P.W_r)
+    return P._lm_norm
+
+
+def _bf16_spacing(x):
+    _, e = np.frexp(x)
+    return np.ldexp(1.0, np.maximum(e, -125) - 8)
+
+
+def pass_logits(P, s_b, h_b, anchor, Y_prev):
+    """Oracle logits of one pass from a given iterate (Y_prev None: the base logits),
+    with the element-wise device error bound E of the module doc."""
+    lmn = lm_row_norms(P)
+    h64 = O.to_f64(h_b)
+    H = h64.shape[1]
+    if Y_prev is None:
+        l = s_b
+        Z = None
+    else:
+        st = O.fuse_static(P, h_b)
+        x_prev = np.concatenate([[anchor], np.asarray(Y_prev, dtype=np.int64)[:-1]])
+        Zraw = O.trans(P, O.mix(P.L, O.fuse(P, st, x_prev)))
+        Z = O.round_bf16(Zraw) if P.round_z else Zraw
+        l = s_b + O.read(P, Z)
+    E = 6 * U32 * np.sqrt(H) * np.linalg.norm(h64, axis=1)[:, None] * lmn[None, :] + U32 * np.abs(l)
+    if Z is not None:
+        aw = P._abs_wr
+        E += 6 * U32 * 16 * (np.abs(Z) @ aw.T)
+        if P.round_z:
+            sp = _bf16_spacing(Zraw)
+            frac = Zraw / sp - np.floor(Zraw / sp)
+            cand = np.abs(frac - 0.5) * sp <= Z_REL * np.abs(Zraw)
+            E += (cand * sp) @ aw.T
+        else:
+            E += Z_REL * (np.abs(Z) @ aw.T)
+    return l, E
+
+
+def _decision_ok(l, E, y_dev, sample, u):
     y_o, _ = O.select(l, sample, u)
     if y_o == y_dev:
         return "exact"
     if not sample:
-        ok = (l[y_o] - l[y_dev]) <= 2 * E
+        ok = (l[y_o] - l[y_dev]) <= E[y_o] + E[y_dev]
     else:
         w = O.softmax_weights(l)
         C = np.cumsum(w)
         Z = C[-1]
         lo = C[y_dev - 1] if y_dev > 0 else 0.0
-        slack = 4 * E * Z
-        ok = (lo - slack) <= u * Z <= (C[y_dev] + slack)
+        f = np.exp(4 * E.max())
+        ok = lo / f <= u * Z <= C[y_dev] * f
     return "excused" if ok else "wrong"
 
 
-def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits, E):
-    """Validate one sequence's device trajectory; returns a Tally."""
+def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits):
+    """Validate one sequence's device trajectory; returns (Tally, final logits, final E)."""
     B = s_b.shape[0]
     t = Tally(seqs=1)
     ref = O.refine_block(P, s_b, h_b, anchor, seed=seed, sample=sample, u=u, K=K,
                          early_exit=False)
     tro = ref.traj_padded(K)
     first = 0 if seed is None else 1
-    if np.array_equal(tro, traj):
+    exact_traj = np.array_equal(tro, traj)
+    l_final = E_final = None
+    for j in range(first, K + 1):
+        if exact_traj and j < K:
+            continue
+        l, E = pass_logits(P, s_b, h_b, anchor, None if j == 0 else traj[j - 1])
+        l_final, E_final = l, E
+        if exact_traj:
+            continue
+        for k in range(B):
+            r = _decision_ok(l[k], E[k], int(traj[j][k]), sample, float(u[k]))
+            assert r != "wrong", f"pass {j} position {k}: device token {traj[j][k]} is not a valid selection"
+            t.decisions += 1
+            t.exact += r == "exact"
+            t.excused += r == "excused"
+    if exact_traj:
         n = (K + 1 - first) * B
         t.decisions = t.exact = n
         t.seq_exact = 1
-        l_final = ref.logits
-    else:
-        l_final = None
-        for j in range(first, K + 1):
-            l = s_b if j == 0 else O.pass_from(P, s_b, h_b, anchor, traj[j - 1], sample, u)[2]
-            if j == K:
-                l_final = l
-            for k in range(B):
-                r = _decision_ok(l[k], int(traj[j][k]), sample, float(u[k]), E)
-                assert r != "wrong", f"pass {j} position {k}: device token {traj[j][k]} is not a valid selection"
-                t.decisions += 1
-                t.exact += r == "exact"
-                t.excused += r == "excused"
-    if K == 0:
-        l_final = s_b
+    if l_final is None:                       # K = 0 with given seed ids
+        l_final, E_final = pass_logits(P, s_b, h_b, anchor, None)
     it = next((j + 1 for j in range(K) if np.array_equal(traj[j + 1], traj[j])), K)
     assert int(iters) == it, f"iters {iters} != {it}"
     if logits is not None:
-        t.max_logit_err = float(np.max(np.abs(logits.astype(np.float64) - l_final)))
-        assert t.max_logit_err <= E, f"logit error {t.max_logit_err} > {E}"
-    return t, l_final
+        err = np.abs(logits.astype(np.float64) - l_final)
+        t.max_logit_err = float(err.max())
+        t.max_err_over_bound = float((err / E_final).max())
+        assert (err <= E_final).all(), (
+            f"logit error {t.max_logit_err} exceeds its bound at "
+            f"{np.unravel_index(np.argmax(err / E_final), err.shape)}")
+    return t, l_final, E_final
 
 
 def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None):
@@ -193,23 +256,25 @@ def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None):
     if s is None:
         s = O.base_logits(P.W_lm, i.h[seqs].reshape(len(seqs) * prob.B, prob.H)).reshape(
             len(seqs), prob.B, -1)
-    E = E_LOGIT[prob.dtype]
     tot, finals = Tally(), {}
     for n, b in enumerate(seqs):
         seed = i.seed_ids[b] if prob.seed_given else None
-        t, lf = check_sequence(P, s[n], i.h[b], int(i.anchor[b]), seed, bool(i.temp[b]),
-                               i.u_draft[b], run.traj.shape[0] - 1,
-                               run.traj[:, b], run.iters[b],
-                               None if run.logits is None else run.logits[b], E)
+        t, lf, Ef = check_sequence(P, s[n], i.h[b], int(i.anchor[b]), seed, bool(i.temp[b]),
+                                   i.u_draft[b], run.traj.shape[0] - 1, run.traj[:, b],
+                                   run.iters[b], None if run.logits is None else run.logits[b])
         tot.add(t)
-        finals[b] = lf
+        finals[b] = (lf, Ef)
     return tot, finals
 
 
 def check_verify(prob: Problem, run: DeviceRun, finals: dict, n_dev, next_dev, target_ids, seqs):
-    """Greedy rows: exact.  Sampled rows: exact or a near-tie decision (see module doc)."""
+    """Greedy rows: exact.  Sampled rows: exact or a near-tie decision.
+
+    With |l_device - l| <= E and |lse_device - lse| <= Emax the device's q moves
+    by a factor within e^(+-2 Emax); the target p (fp32 logits, fp64 sums on
+    both sides) by at most 1e-6 relative.
+    """
     i = prob.inp
-    E = E_LOGIT[prob.dtype]
     excused = 0
     for b in seqs:
         y = run.ids[b]
@@ -217,25 +282,24 @@ def check_verify(prob: Problem, run: DeviceRun, finals: dict, n_dev, next_dev, t
             n, nx = O.verify_greedy(y, target_ids[b])
             assert (int(n_dev[b]), int(next_dev[b])) == (n, nx), f"seq {b}"
             continue
+        lf, Ef = finals[b]
         pl = i.target_logits[b].astype(np.float64)
-        v = O.verify_sample(finals[b], y, pl, i.r_accept[b], float(i.u_res[b]))
+        v = O.verify_sample(lf, y, pl, i.r_accept[b], float(i.u_res[b]))
         if (int(n_dev[b]), int(next_dev[b])) == (v.n, v.next):
             continue
         k = min(int(n_dev[b]), v.n)
+        tol = np.exp(2 * Ef[min(k, prob.B - 1)].max()) - 1 + 1e-6
         if int(n_dev[b]) != v.n:
-            # the first accept decision on which they differ must be a near-tie
-            assert v.accept_margins[k] <= 4 * E, f"seq {b}: accept decision at {k} is not a near-tie"
+            assert v.accept_margins[k] <= tol, f"seq {b}: accept decision at {k} is not a near-tie"
         else:
-            q = O.softmax(finals[b][k]) if k < prob.B else None
             p = O.softmax(pl[k])
-            res = np.maximum(p - q, 0.0) if q is not None else p
+            res = np.maximum(p - O.softmax(lf[k]), 0.0) if k < prob.B else p
             if not res.sum() > 0:
                 res = p
             C = np.cumsum(res)
-            R = C[-1]
             t = int(next_dev[b])
             lo = C[t - 1] if t > 0 else 0.0
-            slack = 2 * E + 4 * E * R
-            assert lo - slack <= float(i.u_res[b]) * R <= C[t] + slack, f"seq {b}: resample"
+            uz = float(i.u_res[b]) * C[-1]
+            assert lo - tol <= uz <= C[t] + tol, f"seq {b}: resample"
         excused += 1
     return excused

@@ -11,7 +11,7 @@ import oracle as O
 import synth
 from synth.configs import TINY_F32, QWEN_B1, QWEN_B8_T1, QWEN_B32, QWEN_B64_MIXED
 
-from _parity import (E_LOGIT, check_refine, check_verify, custom_problem, make_refiner,
+from _parity import (check_refine, check_verify, custom_problem, make_refiner,
                      run_device, upload, workload_problem)
 
 pytestmark = pytest.mark.gpu
@@ -37,7 +37,8 @@ def _full_check(prob, ref, dev, seqs=None, K=None, min_exact=1.0):
     run = run_device(ref, prob, dev, K=K)
     tally, finals = check_refine(prob, run, seqs=seqs)
     _say(f"  decisions={tally.decisions} exact={tally.exact} excused={tally.excused} "
-         f"seq_exact={tally.seq_exact}/{tally.seqs} max|dl|={tally.max_logit_err:.3g}")
+         f"seq_exact={tally.seq_exact}/{tally.seqs} max|dl|={tally.max_logit_err:.3g} "
+         f"max|dl|/E={tally.max_err_over_bound:.3g}")
     assert tally.exact >= min_exact * tally.decisions
     seqs = list(range(prob.batch)) if seqs is None else seqs
     target_ids = prob.inp.target_ids(run.ids)
