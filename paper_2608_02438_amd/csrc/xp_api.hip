@@ -16,6 +16,7 @@ bool lm_split_ok(int H, int dtype);
 __global__ void k_clear_err(uint32_t* err) {
   if (threadIdx.x == 0) *err = 0u;
 }
+
 }  // namespace xp
 
 using namespace xp;
@@ -128,9 +129,7 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
       {(void**)&ws.Fh, (size_t)256 * w->H * 4},
       {(void**)&ws.Fg, (size_t)256 * w->H * 4},
       {(void**)&ws.Lp, (npairs ? npairs : 1) * 256 * es},
-      {(void**)&ws.g, (size_t)max_batch * w->H * 4},
-      {(void**)&ws.uh, Mmax * 256 * 4},
-      {(void**)&ws.ug, (size_t)max_batch * 256 * 4},
+      {(void**)&ws.ppart, (size_t)2 * prep_ksp(w->H) * Mmax * 256 * 4},
       {(void**)&ws.c, Mmax * 256 * 4},
       {(void**)&ws.h1, Mmax * 512 * 4},
       {(void**)&ws.z, Mmax * 256 * es},
@@ -288,17 +287,16 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
   XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, st));
   XP_TIMED(XP_STAGE_LMHEAD, launch_lmhead(h, batch * h->B, hidden, temp, st));
   XP_TIMED(XP_STAGE_SELECT,
-           launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj, st));
+           launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj,
+                         K == 0 ? out_ids : nullptr, K == 0 ? out_iters : nullptr, st));
   for (int j = 0; j < K; ++j) {
-    {
-      StageTimer tm_(h, XP_STAGE_RSPACE, st);
-      XP_LAUNCH(launch_fuse_mix_w1(h, batch, j, flags, anchor, st));
-      XP_LAUNCH(launch_w2(h, batch, j, flags, st));
-    }
+    XP_TIMED(XP_STAGE_RSPACE, launch_rspace(h, batch, j, flags, anchor, st));
     XP_TIMED(XP_STAGE_READ, launch_read(h, batch, j, flags, temp,
                                         (flags & XP_WRITE_LOGITS) ? out_logits : nullptr, st));
+    const bool lastp = j == K - 1;
     XP_TIMED(XP_STAGE_SELECT,
-             launch_select(h, batch, j, K, flags, nullptr, temp, u_draft, out_traj, st));
+             launch_select(h, batch, j, K, flags, nullptr, temp, u_draft, out_traj,
+                           lastp ? out_ids : nullptr, lastp ? out_iters : nullptr, st));
   }
   XP_LAUNCH(launch_finish(h, batch, K, flags, out_ids, out_iters, out_logits, st));
   h->last_batch = batch;

@@ -23,11 +23,9 @@ struct Workspace {
   float* Fh = nullptr;        // [r][H]        W_in[:, 0:r] W_h
   float* Fg = nullptr;        // [r][H]        W_in[:, r:2r] W_g
   void* Lp = nullptr;         // [npairs][r]   L[d][k][i] (i < k) at pair k(k-1)/2 + i
-  float* g = nullptr;         // [max_batch][H]
-  float* uh = nullptr;        // [Mmax][r]     Fh h_k
-  float* ug = nullptr;        // [max_batch][r] Fg g
-  float* c = nullptr;         // [Mmax][r]     Mix output
-  float* h1 = nullptr;        // [Mmax][2r]    silu(W_1 c)
+  float* ppart = nullptr;     // [2][ksp][Mmax][r] k-slice partials of Fh h_k and Fg h_k
+  float* c = nullptr;         // [Mmax][r]     Mix output of the current pass
+  float* h1 = nullptr;        // [Mmax][2r]    silu(W_1 c) of the current pass
   void* z = nullptr;          // [Mmax][r]     Trans output (dtype)
   int32_t* Y[2] = {nullptr, nullptr};   // [Mmax] iterates, ping-pong by pass parity
   uint64_t* keys = nullptr;   // [max chunks][Mmax]  greedy partials
@@ -78,10 +76,11 @@ hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t 
 hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t* temp, hipStream_t st);
 hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
                          const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
-                         int32_t* out_traj, hipStream_t st);
-hipError_t launch_fuse_mix_w1(xp_handle* h, int batch, int pass, uint32_t flags,
-                              const int32_t* anchor, hipStream_t st);
-hipError_t launch_w2(xp_handle* h, int batch, int pass, uint32_t flags, hipStream_t st);
+                         int32_t* out_traj, int32_t* out_ids, int32_t* out_iters,
+                         hipStream_t st);
+hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
+                         hipStream_t st);
+int prep_ksp(int H);
 hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
                        float* out_logits, hipStream_t st);
 hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,

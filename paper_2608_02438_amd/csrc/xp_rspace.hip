@@ -3,128 +3,424 @@
 // Fuse is linear, so its iteration-invariant part is computed once per call
 // (h and g are fixed across Jacobi passes, section 4.2):
 //     P_k = (W_in[:, 0:r] W_h) h_k + (W_in[:, r:2r] W_g) g ,   g = mean_j h_j
-// and its token part is a row of the precomputed table T = W_e W_in[:, 2r:3r]^T,
-// so a pass's Fuse is a gather:  a_k = P_k + T[x_{k-1}]  (eq. fuse).
-// Mix (eq. mix) and the first Trans product run in one kernel per
-// (sequence, slice of W_1 rows); W_2, the residual and the bf16 rounding of z
-// in a second kernel (eq. mlp).
+// by k_prep, and its token part is a row of the precomputed table
+// T = W_e W_in[:, 2r:3r]^T, so a pass's Fuse is a gather:  a_k = P_k + T[x_{k-1}].
+// A pass then runs Mix (eq. mix) and Trans (eq. mlp).  With bf16 weights the
+// r-space products run on the bf16 matrix cores with the fp32 operand split
+// into three exact bf16 terms (products exact, sums in fp32); with fp32
+// weights they use v_mfma_f32_16x16x4_f32.  z is rounded to the weight dtype.
 #include "xp_internal.h"
 
 namespace xp {
 
-// g[b][k] = (1/B) sum_j h[b][j][k]
-template <typename T>
-__global__ __launch_bounds__(256) void k_gmean(const T* __restrict__ hid, int B, int H,
-                                               float* __restrict__ g) {
-  const int b = blockIdx.x, k = blockIdx.y * 256 + threadIdx.x;
-  if (k >= H) return;
-  float acc = 0.f;
-  for (int j = 0; j < B; ++j) acc += to_f32(hid[((size_t)b * B + j) * H + k]);
-  g[(size_t)b * H + k] = acc / (float)B;
+__device__ __forceinline__ float4 load4f(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 load4f(const uint16_t* p) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u),
+                     __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u));
+}
+__device__ __forceinline__ floatx4 mma4(float4 a, float4 b, floatx4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+  return c;
 }
 
-// out[n][o] = sum_k F[o][k] x_n[k] for n < N, o < O, F fp32 [O][Kd].
-// One wave per output row, 16 input rows per workgroup column.
-template <typename TX>
-__global__ __launch_bounds__(256) void k_rowdot(const float* __restrict__ F, int O, int Kd,
-                                                const TX* __restrict__ X, int N,
-                                                float* __restrict__ out) {
+// ---------------------------------------------------------------------------
+// k_prep: part[mat][ks][m][o] = F_mat[o][slice ks] . h[m][slice ks] for
+// F_0 = W_in[:,0:r] W_h and F_1 = W_in[:,r:2r] W_g (fp32 [r][H]); the KSP
+// slice partials are added (in slice order) by their consumer.  Grid (16 row
+// tiles, KSP k-slices, 2 * position-block groups); 4 waves split a slice and
+// sum their 16x16 tiles in LDS in wave order.  F is split into three bf16
+// terms on the fly (exact), so the products run on the bf16 matrix cores.
+// Workgroup (0,0,0) also clears the per-call Jacobi state.
+// ---------------------------------------------------------------------------
+constexpr int kPrepPBG = 8;            // position blocks per workgroup
+
+// k-slices of the prep product: the most (up to 8) that leave every wave a
+// whole number of 32-element (bf16) or 16-element (fp32) MFMA steps.
+int prep_ksp(int H) {
+  for (int k = 8; k > 1; k >>= 1)
+    if (H % (k * 4 * 32) == 0) return k;
+  return 1;
+}
+
+// fp32 -> three bf16 terms with x == hi + mid + lo exactly (truncating split:
+// each term keeps the next 8 significant bits of the 24).  With bf16 weights
+// every product w * term is exact in fp32, so W x on the bf16 matrix cores
+// is W x with fp32 accumulation, as on the fp32 path.
+__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
+  const uint32_t xh = __float_as_uint(x) & 0xFFFF0000u;
+  const float r1 = x - __uint_as_float(xh);
+  const uint32_t xm = __float_as_uint(r1) & 0xFFFF0000u;
+  const float r2 = r1 - __uint_as_float(xm);
+  h = xh >> 16;
+  m = xm >> 16;
+  l = __float_as_uint(r2) >> 16;
+}
+// Three bf16x8 MFMA operands from 8 fp32 values (two float4).
+__device__ __forceinline__ void split3x8(float4 v0, float4 v1, u32x4& bh, u32x4& bm, u32x4& bl) {
+  const float x[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+  uint32_t h[8], m[8], l[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) split3(x[i], h[i], m[i], l[i]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    bh[i] = h[2 * i] | (h[2 * i + 1] << 16);
+    bm[i] = m[2 * i] | (m[2 * i + 1] << 16);
+    bl[i] = l[2 * i] | (l[2 * i + 1] << 16);
+  }
+}
+// acc += a . x over one 32-k step, x (8 fp32 per lane) split into three terms;
+// `a` is the exact bf16 operand.  The split operand may be either A or B.
+__device__ __forceinline__ floatx4 mma_split_b(u32x4 a, float4 x0, float4 x1, floatx4 acc) {
+  u32x4 bh, bm, bl;
+  split3x8(x0, x1, bh, bm, bl);
+  acc = Mfma<uint16_t>::mma(a, bh, acc);
+  acc = Mfma<uint16_t>::mma(a, bm, acc);
+  acc = Mfma<uint16_t>::mma(a, bl, acc);
+  return acc;
+}
+__device__ __forceinline__ floatx4 mma_split_a(float4 x0, float4 x1, u32x4 b, floatx4 acc) {
+  u32x4 ah, am, al;
+  split3x8(x0, x1, ah, am, al);
+  acc = Mfma<uint16_t>::mma(ah, b, acc);
+  acc = Mfma<uint16_t>::mma(am, b, acc);
+  acc = Mfma<uint16_t>::mma(al, b, acc);
+  return acc;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
+                                              const float* __restrict__ Fg,
+                                              const T* __restrict__ hid, int H, int M,
+                                              int ksp, float* __restrict__ part, int batch,
+                                              int32_t* __restrict__ iters,
+                                              int32_t* __restrict__ ctrl) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int o = blockIdx.x * 4 + wave, n0 = blockIdx.y * 16;
-  if (o >= O) return;
-  float acc[16];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) acc[j] = 0.f;
-  for (int k = lane * 4; k < Kd; k += 256) {
-    const float4 f = *reinterpret_cast<const float4*>(F + (size_t)o * Kd + k);
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int n = n0 + j;
-      if (n < N) {
-        const TX* x = X + (size_t)n * Kd + k;
-        acc[j] += f.x * to_f32(x[0]) + f.y * to_f32(x[1]) + f.z * to_f32(x[2]) + f.w * to_f32(x[3]);
+  const int rt = blockIdx.x, ks = blockIdx.y, mat = blockIdx.z & 1, pbg = blockIdx.z >> 1;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
+    for (int i = threadIdx.x; i < batch; i += blockDim.x) iters[i] = 0;
+    if (threadIdx.x < 2) ctrl[threadIdx.x] = 0;
+  }
+  const float* F = mat ? Fg : Fh;
+  const int kw = H / ksp / 4;                                 // k per wave
+  const int g = lane >> 4, li = lane & 15;
+  const int k0 = ks * (H / ksp) + wave * kw;
+  const float* arow = F + (size_t)(rt * 16 + li) * H + k0;
+  __shared__ floatx4 red[4][64];
+  const int npb = (M + 15) / 16;
+  const int pb0 = pbg * kPrepPBG, pb1 = min(npb, (pbg + 1) * kPrepPBG);
+  for (int pb = pb0; pb < pb1; ++pb) {
+    const int p = pb * 16 + li;
+    const int pc = p < M ? p : M - 1;
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (sizeof(T) == 2) {
+      const T* brow = hid + (size_t)pc * H + k0 + 8 * g;
+      for (int u = 0; u < kw / 32; ++u) {
+        const float4 a0 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g);
+        const float4 a1 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g + 4);
+        u32x4 bv = ld16(brow + u * 32);
+        if (p >= M) bv = u32x4{0u, 0u, 0u, 0u};
+        acc = mma_split_a(a0, a1, bv, acc);
+      }
+    } else {
+      const T* brow = hid + (size_t)pc * H + k0 + 4 * g;
+      for (int u = 0; u < kw / 16; ++u) {
+        const float4 a = load4f(arow + u * 16 + 4 * g);
+        float4 bv = load4f(brow + u * 16);
+        if (p >= M) bv = make_float4(0.f, 0.f, 0.f, 0.f);
+        acc = mma4(a, bv, acc);
       }
     }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+      floatx4 s = red[0][lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        const floatx4 o = red[w][lane];
+        s[0] += o[0]; s[1] += o[1]; s[2] += o[2]; s[3] += o[3];
+      }
+      if (p < M) {
+        float* dst = part + (((size_t)mat * ksp + ks) * M + p) * 256 + rt * 16 + 4 * g;
+        *reinterpret_cast<float4*>(dst) = make_float4(s[0], s[1], s[2], s[3]);
+      }
+    }
+    __syncthreads();
   }
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) acc[j] += __shfl_xor(acc[j], m, kWave);
-  }
-#pragma unroll
-  for (int j = 0; j < 16; ++j)
-    if (lane == j && n0 + j < N) out[(size_t)(n0 + j) * O + o] = acc[j];
 }
 
-// Fuse (gather form) + Mix + h1 = silu(W_1 c) for rows [j0, j0 + R1) of W_1.
-// Thread d owns channel d (r = 256 threads).  Workgroup y == 0 also stores c.
-template <typename T>
-__global__ __launch_bounds__(256) void k_fuse_mix_w1(
-    int B, int V, int R1, const float* __restrict__ uh, const float* __restrict__ ug,
-    const float* __restrict__ Ttab, const T* __restrict__ Lp, const int32_t* __restrict__ anchor,
-    const int32_t* __restrict__ Y, const T* __restrict__ W1, float* __restrict__ c_out,
-    float* __restrict__ h1, uint32_t* __restrict__ err, const int32_t* __restrict__ ctrl,
+// ---------------------------------------------------------------------------
+// One Jacobi pass in r-space runs as three short, wide kernels so that every
+// workgroup reads only a few KB (a single CU streams from L2 at well under
+// 100 GB/s, so per-workgroup bytes, not flops, set the time):
+//   k_fusemix  (batch, 16 d-tiles):  a_k = P_k + T[x_{k-1}], c = (I + L) a
+//   k_trans1   (batch, 32 row tiles): h1 = silu(W_1 c), 16 rows each
+//   k_trans2   (batch, 16 row tiles): z = c + W_2 h1, rounded to the weight dtype
+// Every load a workgroup needs is issued before its first use and none sits
+// under a branch (indices are clamped, results masked), so the loads overlap.
+// ---------------------------------------------------------------------------
+
+// Fuse (gather form) and Mix for 16 feature dims d of one sequence.  Mix is
+// independent per d (eq. mix: c^(d) = (I + L^(d)) a^(d)), so the 16 dims of a
+// workgroup need only their own 16 columns of every L^(d).
+template <typename T, int BP>
+__global__ __launch_bounds__(256) void k_fusemix(
+    int B, int V, int M, int ksp, const float* __restrict__ part, const float* __restrict__ Ttab,
+    const T* __restrict__ Lp, const int32_t* __restrict__ anchor, const int32_t* __restrict__ Y,
+    float* __restrict__ c, uint32_t* __restrict__ err, const int32_t* __restrict__ ctrl,
     int skip_when_done) {
   if (skip_when_done && ctrl[1]) return;
   constexpr int r = 256;
-  __shared__ float cs[32][r + 1];
-  const int b = blockIdx.x, d = threadIdx.x;
-  const float gpart = ug[(size_t)b * r + d];
-  for (int k = 0; k < B; ++k) {
-    int x = (k == 0) ? anchor[b] : Y[b * B + k - 1];
-    if (x < 0 || x >= V) {
-      atomicOr(err, XP_DEVERR_TOKEN);
-      x = 0;
+  constexpr int EPT = BP / 16;                       // positions per thread
+  constexpr int NPAIR = BP * (BP - 1) / 2;
+  constexpr int CPP = (int)sizeof(T);                // 16-byte chunks per pair (16 dims)
+  constexpr int LCH_T = (NPAIR * CPP + 255) / 256;   // chunks per thread
+  __shared__ float A[BP][17];
+  __shared__ float ug[16];
+  __shared__ u32x4 Ls[NPAIR * CPP > 0 ? NPAIR * CPP : 1];
+  const int b = blockIdx.x, dt = blockIdx.y, tid = threadIdx.x;
+  const int dl = tid & 15, kg = tid >> 4, d = dt * 16 + dl;
+  const int npair = B * (B - 1) / 2, nch = npair * CPP;
+
+  u32x4 lc[LCH_T];
+#pragma unroll
+  for (int j = 0; j < LCH_T; ++j) {                  // L columns [dt*16, dt*16+16) of every pair
+    int q = tid + 256 * j;
+    q = q < nch ? q : (nch > 0 ? nch - 1 : 0);
+    const int pr = q / CPP, cc = q % CPP;
+    lc[j] = *reinterpret_cast<const u32x4*>(Lp + (size_t)pr * r + dt * 16 + cc * (16 / CPP));
+  }
+  float ph[EPT], pg[EPT], tv[EPT];
+  int xv[EPT];
+  const int ya = anchor[b];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    const int kc = k < B ? k : B - 1;
+    const size_t m = (size_t)b * B + kc;
+    float sh = 0.f, sg = 0.f;
+    for (int q = 0; q < ksp; ++q) {
+      sh += part[((size_t)q * M + m) * r + d];
+      sg += part[((size_t)(ksp + q) * M + m) * r + d];
     }
-    cs[k][d] = uh[((size_t)b * B + k) * r + d] + gpart + Ttab[(size_t)x * r + d];
+    ph[j] = sh;
+    pg[j] = sg;
+    xv[j] = kc == 0 ? ya : Y[m - 1];
   }
-  // c_k = a_k + sum_{i<k} L[d][k][i] a_i, in place from the last position down
-  for (int k = B - 1; k >= 1; --k) {
-    float acc = cs[k][d];
-    const T* lk = Lp + (size_t)(k * (k - 1) / 2) * r + d;
-    for (int i = 0; i < k; ++i) acc += to_f32(lk[(size_t)i * r]) * cs[i][d];
-    cs[k][d] = acc;
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int x = xv[j];
+    const bool ok = x >= 0 && x < V;
+    bad |= !ok && kg + 16 * j < B;
+    tv[j] = Ttab[(size_t)(ok ? x : 0) * r + d];
   }
-  if (blockIdx.y == 0)
-    for (int k = 0; k < B; ++k) c_out[((size_t)b * B + k) * r + d] = cs[k][d];
+#pragma unroll
+  for (int j = 0; j < LCH_T; ++j) {
+    const int q = tid + 256 * j;
+    if (q < nch) Ls[q] = lc[j];
+  }
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    if (k < B) A[k][dl] = pg[j];
+  }
+  if (bad) atomicOr(err, XP_DEVERR_TOKEN);
   __syncthreads();
-  const int j0 = blockIdx.y * R1;
-  for (int o = threadIdx.x; o < R1 * B; o += blockDim.x) {
-    const int j = j0 + o / B, k = o % B;
-    const T* w = W1 + (size_t)j * r;
-    float acc = 0.f;
-    for (int e = 0; e < r; ++e) acc += to_f32(w[e]) * cs[k][e];
-    h1[((size_t)b * B + k) * (2 * r) + j] = acc / (1.f + expf(-acc));
+  if (tid < 16) {                                    // (W_in[:,r:2r] W_g) g, g = mean_k h_k
+    float t = 0.f;
+    for (int k = 0; k < B; ++k) t += A[k][tid];
+    ug[tid] = t / (float)B;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    if (k < B) A[k][dl] = ph[j] + ug[dl] + tv[j];   // a_k = P_k + T[x_{k-1}]
+  }
+  __syncthreads();
+  const T* ls = reinterpret_cast<const T*>(Ls);      // [pair][16 dims]
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    if (k < B) {
+      float acc = A[k][dl];
+      const int p0 = k * (k - 1) / 2;
+      for (int i = 0; i < k; ++i) acc += to_f32(ls[(p0 + i) * 16 + dl]) * A[i][dl];
+      c[((size_t)b * B + k) * r + d] = acc;
+    }
   }
 }
 
-// z = c + W_2 h1 for rows [d0, d0 + R2); rounded to bf16 for bf16 weights.
-template <typename T>
-__global__ __launch_bounds__(256) void k_w2(int B, int R2, const float* __restrict__ c,
-                                            const float* __restrict__ h1, const T* __restrict__ W2,
-                                            T* __restrict__ z, const int32_t* __restrict__ ctrl,
-                                            int skip_when_done) {
+// h1[m][16*rt .. 16*rt+16) = silu(W_1[rows] c_m) for the positions of one
+// sequence; 4 waves split the 256-long contraction and add their tiles in
+// wave order.
+template <typename T, int BP>
+__global__ __launch_bounds__(256) void k_trans1(int B, const T* __restrict__ W1,
+                                                const float* __restrict__ c,
+                                                float* __restrict__ h1,
+                                                const int32_t* __restrict__ ctrl,
+                                                int skip_when_done) {
   if (skip_when_done && ctrl[1]) return;
-  constexpr int r = 256, r2 = 512;
-  __shared__ float hs[16][r2 + 1];
-  const int b = blockIdx.x, d0 = blockIdx.y * R2;
-  for (int kg = 0; kg < B; kg += 16) {
-    const int nk = min(16, B - kg);
-    __syncthreads();
-    for (int i = threadIdx.x; i < nk * r2; i += blockDim.x)
-      hs[i / r2][i % r2] = h1[((size_t)b * B + kg + i / r2) * r2 + i % r2];
-    __syncthreads();
-    for (int o = threadIdx.x; o < R2 * nk; o += blockDim.x) {
-      const int dd = d0 + o / nk, k = o % nk;
-      const T* w = W2 + (size_t)dd * r2;
-      float acc = 0.f;
-      for (int j = 0; j < r2; ++j) acc += to_f32(w[j]) * hs[k][j];
-      const size_t m = (size_t)b * B + kg + k;
-      const float zv = c[m * r + dd] + acc;
-      if constexpr (sizeof(T) == 2)
-        z[m * r + dd] = f32_to_bf16_rne(zv);
-      else
-        z[m * r + dd] = zv;
+  constexpr int r = 256, r2 = 512, NPB = BP / 16;
+  constexpr bool kBf = sizeof(T) == 2;
+  const int b = blockIdx.x, rt = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  const int k0 = wave * (r / 4);                     // this wave's 64-long k slice
+  const T* arow = W1 + (size_t)(rt * 16 + li) * r + k0;
+  __shared__ floatx4 red[4][NPB][64];
+  floatx4 acc[NPB];
+  if constexpr (kBf) {
+    u32x4 w[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) w[u] = ld16(arow + u * 32 + 8 * g);
+    float4 x[NPB][2][2];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int k = pb * 16 + li;
+      const float* crow = c + ((size_t)b * B + (k < B ? k : B - 1)) * r + k0 + 8 * g;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        x[pb][u][0] = *reinterpret_cast<const float4*>(crow + u * 32);
+        x[pb][u][1] = *reinterpret_cast<const float4*>(crow + u * 32 + 4);
+      }
+    }
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 2; ++u) acc[pb] = mma_split_b(w[u], x[pb][u][0], x[pb][u][1], acc[pb]);
+    }
+  } else {
+    float4 w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) w[u] = load4f(arow + u * 16 + 4 * g);
+    float4 x[NPB][4];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int k = pb * 16 + li;
+      const float* crow = c + ((size_t)b * B + (k < B ? k : B - 1)) * r + k0 + 4 * g;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[pb][u] = *reinterpret_cast<const float4*>(crow + u * 16);
+    }
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[pb] = mma4(w[u], x[pb][u], acc[pb]);
+    }
+  }
+#pragma unroll
+  for (int pb = 0; pb < NPB; ++pb) red[wave][pb][lane] = acc[pb];
+  __syncthreads();
+  if (wave < NPB) {
+    const int pb = wave;
+    const floatx4 q0 = red[0][pb][lane], q1 = red[1][pb][lane];
+    const floatx4 q2 = red[2][pb][lane], q3 = red[3][pb][lane];
+    const int k = pb * 16 + li;
+    if (k < B) {
+      float o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = ((q0[i] + q1[i]) + q2[i]) + q3[i];
+        o[i] = v / (1.f + expf(-v));
+      }
+      *reinterpret_cast<float4*>(h1 + ((size_t)b * B + k) * r2 + rt * 16 + 4 * g) =
+          make_float4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
+// z[m][16*zt .. 16*zt+16) = c_m + W_2[rows] h1_m (eq. mlp), rounded to the
+// weight dtype; 4 waves split the 512-long contraction.
+template <typename T, int BP>
+__global__ __launch_bounds__(256) void k_trans2(int B, const T* __restrict__ W2,
+                                                const float* __restrict__ c,
+                                                const float* __restrict__ h1, T* __restrict__ z,
+                                                const int32_t* __restrict__ ctrl,
+                                                int skip_when_done) {
+  if (skip_when_done && ctrl[1]) return;
+  constexpr int r = 256, r2 = 512, NPB = BP / 16;
+  constexpr bool kBf = sizeof(T) == 2;
+  const int b = blockIdx.x, zt = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  const int k0 = wave * (r2 / 4);                    // this wave's 128-long k slice
+  const T* arow = W2 + (size_t)(zt * 16 + li) * r2 + k0;
+  __shared__ floatx4 red[4][NPB][64];
+  floatx4 acc[NPB];
+  float4 res[NPB];
+  if constexpr (kBf) {
+    u32x4 w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) w[u] = ld16(arow + u * 32 + 8 * g);
+    float4 x[NPB][4][2];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int k = pb * 16 + li;
+      const float* hrow = h1 + ((size_t)b * B + (k < B ? k : B - 1)) * r2 + k0 + 8 * g;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        x[pb][u][0] = *reinterpret_cast<const float4*>(hrow + u * 32);
+        x[pb][u][1] = *reinterpret_cast<const float4*>(hrow + u * 32 + 4);
+      }
+      res[pb] = *reinterpret_cast<const float4*>(c + ((size_t)b * B + (k < B ? k : B - 1)) * r +
+                                                 zt * 16 + 4 * g);
+    }
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[pb] = mma_split_b(w[u], x[pb][u][0], x[pb][u][1], acc[pb]);
+    }
+  } else {
+    float4 w[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) w[u] = load4f(arow + u * 16 + 4 * g);
+    float4 x[NPB][8];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      const int k = pb * 16 + li;
+      const float* hrow = h1 + ((size_t)b * B + (k < B ? k : B - 1)) * r2 + k0 + 4 * g;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[pb][u] = *reinterpret_cast<const float4*>(hrow + u * 16);
+      res[pb] = *reinterpret_cast<const float4*>(c + ((size_t)b * B + (k < B ? k : B - 1)) * r +
+                                                 zt * 16 + 4 * g);
+    }
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+      acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[pb] = mma4(w[u], x[pb][u], acc[pb]);
+    }
+  }
+#pragma unroll
+  for (int pb = 0; pb < NPB; ++pb) red[wave][pb][lane] = acc[pb];
+  __syncthreads();
+  if (wave < NPB) {
+    const int pb = wave;
+    const floatx4 q0 = red[0][pb][lane], q1 = red[1][pb][lane];
+    const floatx4 q2 = red[2][pb][lane], q3 = red[3][pb][lane];
+    const int k = pb * 16 + li;
+    float4 cr = res[0];                              // residual c of this block
+#pragma unroll
+    for (int q = 1; q < NPB; ++q)
+      if (pb == q) cr = res[q];
+    if (k < B) {
+      const float cv[4] = {cr.x, cr.y, cr.z, cr.w};
+      const size_t m = (size_t)b * B + k;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float zv = cv[i] + (((q0[i] + q1[i]) + q2[i]) + q3[i]);
+        if constexpr (kBf)
+          z[m * r + zt * 16 + 4 * g + i] = f32_to_bf16_rne(zv);
+        else
+          z[m * r + zt * 16 + 4 * g + i] = zv;
+      }
     }
   }
 }
@@ -132,52 +428,47 @@ __global__ __launch_bounds__(256) void k_w2(int B, int R2, const float* __restri
 // ---------------------------------------------------------------------------
 hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t st) {
   const int M = batch * h->B;
-  dim3 gg(batch, (h->H + 255) / 256);
+  const int npb = (M + 15) / 16;
+  const int ksp = prep_ksp(h->H);
+  dim3 grid(h->r / 16, ksp, 2 * ((npb + kPrepPBG - 1) / kPrepPBG));
+  if (h->dtype == XP_BF16)
+    hipLaunchKernelGGL((k_prep<uint16_t>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
+                       (const uint16_t*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
+                       h->ws.ctrl);
+  else
+    hipLaunchKernelGGL((k_prep<float>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
+                       (const float*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
+                       h->ws.ctrl);
+  return hipGetLastError();
+}
+
+template <typename T, int BP>
+static void rspace_t(xp_handle* h, int batch, int pass, int skip, const int32_t* anchor,
+                     hipStream_t st) {
+  const int M = batch * h->B;
+  hipLaunchKernelGGL((k_fusemix<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B, h->V, M,
+                     prep_ksp(h->H), h->ws.ppart, h->ws.T, (const T*)h->ws.Lp, anchor,
+                     h->ws.Y[pass % 2], h->ws.c, h->ws.err, h->ws.ctrl, skip);
+  hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
+                     (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.ctrl, skip);
+  hipLaunchKernelGGL((k_trans2<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B,
+                     (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.ctrl, skip);
+}
+
+hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
+                         hipStream_t st) {
+  const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16) {
-    hipLaunchKernelGGL((k_gmean<uint16_t>), gg, dim3(256), 0, st, (const uint16_t*)hidden, h->B,
-                       h->H, h->ws.g);
-    hipLaunchKernelGGL((k_rowdot<uint16_t>), dim3(h->r / 4, (M + 15) / 16), dim3(256), 0, st,
-                       h->ws.Fh, h->r, h->H, (const uint16_t*)hidden, M, h->ws.uh);
+    if (h->B <= 16)
+      rspace_t<uint16_t, 16>(h, batch, pass, skip, anchor, st);
+    else
+      rspace_t<uint16_t, 32>(h, batch, pass, skip, anchor, st);
   } else {
-    hipLaunchKernelGGL((k_gmean<float>), gg, dim3(256), 0, st, (const float*)hidden, h->B, h->H,
-                       h->ws.g);
-    hipLaunchKernelGGL((k_rowdot<float>), dim3(h->r / 4, (M + 15) / 16), dim3(256), 0, st,
-                       h->ws.Fh, h->r, h->H, (const float*)hidden, M, h->ws.uh);
+    if (h->B <= 16)
+      rspace_t<float, 16>(h, batch, pass, skip, anchor, st);
+    else
+      rspace_t<float, 32>(h, batch, pass, skip, anchor, st);
   }
-  hipLaunchKernelGGL((k_rowdot<float>), dim3(h->r / 4, (batch + 15) / 16), dim3(256), 0, st,
-                     h->ws.Fg, h->r, h->H, (const float*)h->ws.g, batch, h->ws.ug);
-  return hipGetLastError();
-}
-
-static constexpr int kR1 = 16;   // W_1 rows per workgroup
-static constexpr int kR2 = 16;   // W_2 rows per workgroup
-
-hipError_t launch_fuse_mix_w1(xp_handle* h, int batch, int pass, uint32_t flags,
-                              const int32_t* anchor, hipStream_t st) {
-  const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
-  dim3 grid(batch, 2 * h->r / kR1);
-  if (h->dtype == XP_BF16)
-    hipLaunchKernelGGL((k_fuse_mix_w1<uint16_t>), grid, dim3(256), 0, st, h->B, h->V, kR1,
-                       h->ws.uh, h->ws.ug, h->ws.T, (const uint16_t*)h->ws.Lp, anchor,
-                       h->ws.Y[pass % 2], (const uint16_t*)h->W_1, h->ws.c, h->ws.h1, h->ws.err,
-                       h->ws.ctrl, skip);
-  else
-    hipLaunchKernelGGL((k_fuse_mix_w1<float>), grid, dim3(256), 0, st, h->B, h->V, kR1, h->ws.uh,
-                       h->ws.ug, h->ws.T, (const float*)h->ws.Lp, anchor, h->ws.Y[pass % 2],
-                       (const float*)h->W_1, h->ws.c, h->ws.h1, h->ws.err, h->ws.ctrl, skip);
-  return hipGetLastError();
-}
-
-hipError_t launch_w2(xp_handle* h, int batch, int pass, uint32_t flags, hipStream_t st) {
-  (void)pass;
-  const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
-  dim3 grid(batch, h->r / kR2);
-  if (h->dtype == XP_BF16)
-    hipLaunchKernelGGL((k_w2<uint16_t>), grid, dim3(256), 0, st, h->B, kR2, h->ws.c, h->ws.h1,
-                       (const uint16_t*)h->W_2, (uint16_t*)h->ws.z, h->ws.ctrl, skip);
-  else
-    hipLaunchKernelGGL((k_w2<float>), grid, dim3(256), 0, st, h->B, kR2, h->ws.c, h->ws.h1,
-                       (const float*)h->W_2, (float*)h->ws.z, h->ws.ctrl, skip);
   return hipGetLastError();
 }
 

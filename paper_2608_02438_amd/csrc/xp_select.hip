@@ -99,17 +99,18 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
       ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
       float mine = 0.f;
       const int rr = lane & 15, src = (rr >> 2) * 16 + (p & 15), comp = rr & 3;
+      const int pl = (p & ~15) + (lane & 15);
       for (int tt = 0; tt < 4; ++tt) {
         const int t = (base - rlo) / kTile + tlo + tt;
         if (t >= thi) break;                         // wave-uniform
         ReadTile<T>::load_w(W_r, V, t, lane, a);
-        const floatx4 acc = ReadTile<T>::chain(a, bf);
+        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, pl, pl < M, t, lane));
         const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
         const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
         const float v = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
         if ((lane >> 4) == tt) mine = v;
       }
-      if (row < rhi) l = mine + S[(size_t)p * ldS + row];
+      if (row < rhi) l = mine;
     }
     const double w = (row < rhi) ? exp((double)l - (double)m) : 0.0;
     const double tot = cum + wave_incl_scan(w, lane);
@@ -129,22 +130,23 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
 // One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
 // caller's seed ids); mode 1: the selection of Jacobi pass `pass`.
 template <typename T>
-__global__ __launch_bounds__(256) void k_select(
+__global__ __launch_bounds__(512) void k_select(
     int mode, int pass, int batch, int B, int V, int M, const float* __restrict__ S, int ldS,
     const T* __restrict__ W_r, const T* __restrict__ Z, const uint64_t* __restrict__ keys,
     int nkeys, const Stat* __restrict__ stats, int ntiles, int U,
     const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
     const float* __restrict__ u_draft, const int32_t* __restrict__ Yprev, int32_t* __restrict__ Ynew,
     int32_t* __restrict__ traj, double* __restrict__ lse, int32_t* __restrict__ iters,
-    int32_t* __restrict__ ctrl, uint32_t* __restrict__ err, int early_exit) {
+    int32_t* __restrict__ ctrl, uint32_t* __restrict__ err, int early_exit,
+    int32_t* __restrict__ out_ids, int32_t* __restrict__ out_iters, int K) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
   __shared__ int changed;
   if (threadIdx.x == 0) changed = 0;
   __syncthreads();
   const bool sample = temp != nullptr && temp[b] != 0;
   const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
-  for (int k = wave; k < B; k += 4) {
+  for (int k = wave; k < B; k += NW) {
     const int p = b * B + k;
     int y = 0;
     if (skip) {
@@ -170,28 +172,18 @@ __global__ __launch_bounds__(256) void k_select(
     if (lane == 0) {
       Ynew[p] = y;
       if (traj) traj[p] = y;
+      if (out_ids) out_ids[p] = y;
       if (mode == 1 && y != Yprev[p]) atomicOr(&changed, 1);
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0 && mode == 1 && !skip && changed == 0 && iters[b] == 0) {
-    iters[b] = pass + 1;
-    if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
+  if (threadIdx.x == 0) {
+    if (mode == 1 && !skip && changed == 0 && iters[b] == 0) {
+      iters[b] = pass + 1;
+      if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
+    }
+    if (out_iters) out_iters[b] = mode == 0 ? 0 : (iters[b] ? iters[b] : K);
   }
-}
-
-__global__ void k_reset(int batch, int32_t* __restrict__ iters, int32_t* __restrict__ ctrl) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < batch) iters[i] = 0;
-  if (i < 2) ctrl[i] = 0;
-}
-
-__global__ void k_finish(int M, int batch, int K, const int32_t* __restrict__ Yfin,
-                         const int32_t* __restrict__ iters, int32_t* __restrict__ out_ids,
-                         int32_t* __restrict__ out_iters) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < M) out_ids[i] = Yfin[i];
-  if (out_iters && i < batch) out_iters[i] = iters[i] ? iters[i] : K;
 }
 
 __global__ void k_copy_logits(int M, int V, const float* __restrict__ S, int ldS,
@@ -207,41 +199,38 @@ __global__ void k_copy_logits(int M, int V, const float* __restrict__ S, int ldS
 // ---------------------------------------------------------------------------
 hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
                          const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
-                         int32_t* out_traj, hipStream_t st) {
-  (void)K;
+                         int32_t* out_traj, int32_t* out_ids, int32_t* out_iters,
+                         hipStream_t st) {
   const int M = batch * h->B;
   const int mode = pass < 0 ? 0 : 1;
   int32_t* Yprev = h->ws.Y[(pass + 2) % 2];      // pass j reads Y[j % 2]
   int32_t* Ynew = h->ws.Y[(pass + 1) % 2];       // and writes Y[(j+1) % 2]
   int32_t* traj = out_traj ? out_traj + (size_t)(pass + 1) * M : nullptr;
-  if (mode == 0) {
-    hipLaunchKernelGGL(k_reset, dim3((batch + 255) / 256), dim3(256), 0, st, batch, h->ws.iters,
-                       h->ws.ctrl);
-  }
   const int nkeys = mode == 0 ? h->lm_chunks : h->read_wgs;
   const int U = mode == 0 ? h->lm_chunks : h->read_units;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16)
-    hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(256), 0, st, mode, pass, batch,
+    hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(512), 0, st, mode, pass, batch,
                        h->B, h->V, M, h->ws.s, h->ldS, (const uint16_t*)h->W_r,
                        (const uint16_t*)h->ws.z, h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
-                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early);
+                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early, out_ids, out_iters,
+                       K);
   else
-    hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(256), 0, st, mode, pass, batch, h->B,
+    hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(512), 0, st, mode, pass, batch, h->B,
                        h->V, M, h->ws.s, h->ldS, (const float*)h->W_r, (const float*)h->ws.z,
                        h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
-                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early);
+                       h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early, out_ids, out_iters,
+                       K);
   return hipGetLastError();
 }
 
 hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,
                          int32_t* out_iters, float* out_logits, hipStream_t st) {
+  (void)out_ids;
+  (void)out_iters;
   const int M = batch * h->B;
-  const int n = M > batch ? M : batch;
-  hipLaunchKernelGGL(k_finish, dim3((n + 255) / 256), dim3(256), 0, st, M, batch, K,
-                     h->ws.Y[K % 2], h->ws.iters, out_ids, out_iters);
   if (K == 0 && (flags & XP_WRITE_LOGITS) && out_logits)
     hipLaunchKernelGGL(k_copy_logits, dim3(1024), dim3(256), 0, st, M, h->V, h->ws.s, h->ldS,
                        out_logits);

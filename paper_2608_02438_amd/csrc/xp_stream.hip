@@ -98,10 +98,133 @@ __global__ __launch_bounds__(1024) void k_lmhead(
 }
 
 // ---------------------------------------------------------------------------
-// A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
-// the full k range (r = 256 fits one chain of MFMAs); workgroups only combine
-// their waves' argmax keys.  Sampled rows write one (max, sum) per wave unit.
+// A1, LDS variant (16 * H * sizeof(T) <= 128 KB): the 16 positions' h live in
+// LDS (16-byte chunks XOR-swizzled by position so that the B-operand reads of a
+// wave hit distinct banks), which frees registers for a three-deep ring of
+// W_lm tiles in flight per wave.  Partial tiles go through a double-buffered
+// LDS area, so one barrier per tile suffices.
 // ---------------------------------------------------------------------------
+constexpr int kHChunks = 512;          // 16-byte chunks of h per position (8 KB)
+
+template <typename T, int NU>
+__global__ __launch_bounds__(1024) void k_lmhead_lds(
+    const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
+    float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    const uint8_t* __restrict__ temp, int B) {
+  using MF = Mfma<T>;
+  constexpr int EPB = 16 / sizeof(T);
+  constexpr int KS = NU * MF::KU;
+  constexpr int CPU_ = MF::KU / EPB;                  // chunks per load unit (4)
+  __shared__ u32x4 hl[16 * kHChunks];                 // 128 KB
+  __shared__ floatx4 red[2][16][64];                  // 32 KB
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
+  const int u = blockIdx.x, p0 = blockIdx.y * kTile;
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  const int nch = H / EPB;                            // chunks per position row
+
+  for (int e = threadIdx.x; e < 16 * nch; e += blockDim.x) {
+    const int p = e / nch, c = e % nch;
+    const int cs = (c & ~15) | ((c & 15) ^ p);
+    hl[p * kHChunks + cs] =
+        (p0 + p < M) ? ld16(X + (size_t)(p0 + p) * H + (size_t)c * EPB) : u32x4{0u, 0u, 0u, 0u};
+  }
+  __syncthreads();
+
+  const int li = lane & 15, g = lane >> 4;
+  const int cbase = wave * (KS / EPB) + g;            // chunk of this lane's first unit
+  const size_t kofs = (size_t)wave * KS + g * EPB;
+  const int epos = threadIdx.x >> 4, erow = threadIdx.x & 15;
+  const int ep = p0 + epos;
+  const bool eact = threadIdx.x < 256 && ep < M;
+  const bool esample = eact && temp != nullptr && temp[ep / B] != 0;
+  uint64_t best = kKeyMin;
+  Stat st = stat_empty();
+  int buf = 0;
+
+  auto load_tile = [&](int t, u32x4 (&a)[NU]) {
+    int row = t * kTile + li;
+    row = row < V ? row : V - 1;
+    const T* wr = W + (size_t)row * H + kofs;
+#pragma unroll
+    for (int i = 0; i < NU; ++i) a[i] = ld16_nt(wr + i * MF::KU);
+  };
+  auto step = [&](const u32x4 (&a)[NU], int t) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NU; ++i) {
+      const int c = cbase + i * CPU_;
+      const u32x4 bfr = hl[li * kHChunks + ((c & ~15) | ((c & 15) ^ li))];
+      acc = MF::mma(a[i], bfr, acc);
+    }
+    red[buf][wave][lane] = acc;
+    __syncthreads();
+    if (threadIdx.x < 256) {
+      // red[.][w][lane'] holds rows 4*(lane'/16)+i of position lane'%16
+      const int src = (erow >> 2) * 16 + epos, comp = erow & 3;
+      float v = 0.f;
+      for (int w = 0; w < NW; ++w) v += red[buf][w][src][comp];
+      const int row = t * kTile + erow;
+      if (eact && row < V) {
+        S[(size_t)ep * ldS + row] = v;
+        if (esample)
+          st = stat_merge(st, Stat{v, 1.f});
+        else
+          best = umax64(best, argmax_key(v, (uint32_t)row));
+      }
+    }
+    buf ^= 1;
+  };
+
+  // Three register tiles in flight.  The steady-state loop has no conditional
+  // loads, so the compiler's wait counts stay exact and never drain the ring;
+  // the at most four remaining tiles are handled after it.
+  u32x4 a0[NU], a1[NU], a2[NU];
+  if (tlo < thi) load_tile(tlo, a0);
+  if (tlo + 1 < thi) load_tile(tlo + 1, a1);
+  int t = tlo;
+  for (; t + 4 < thi; t += 3) {
+    load_tile(t + 2, a2);
+    step(a0, t);
+    load_tile(t + 3, a0);
+    step(a1, t + 1);
+    load_tile(t + 4, a1);
+    step(a2, t + 2);
+  }
+  if (t < thi) {
+    if (t + 2 < thi) load_tile(t + 2, a2);
+    step(a0, t);
+  }
+  if (t + 1 < thi) {
+    if (t + 3 < thi) load_tile(t + 3, a0);
+    step(a1, t + 1);
+  }
+  if (t + 2 < thi) step(a2, t + 2);
+  if (t + 3 < thi) step(a0, t + 3);
+  if (threadIdx.x < 256) {
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+      best = umax64(best, shfl_xor_u64(best, m));
+      Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
+      st = stat_merge(st, o);
+    }
+    if (erow == 0 && ep < M) {
+      keys[(size_t)u * M + ep] = best;
+      stats[(size_t)u * M + ep] = st;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
+// the full k range (one chain of MFMAs per tile); the position block's z
+// fragments sit in LDS, shared by the waves.  A unit of at most kReadMaxT
+// tiles (the common case) issues all its W_r and s loads before the first
+// MFMA; the loads are unconditional (a short unit re-reads its last tile,
+// which hits in L2), so the wait counts stay exact.  Workgroups merge their
+// waves' argmax keys; sampled rows write one (max, sum) per wave unit.
+// ---------------------------------------------------------------------------
+constexpr int kReadMaxT = 3;
+
 template <typename T>
 __global__ __launch_bounds__(1024) void k_read(
     const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int ldS, int V,
@@ -113,33 +236,22 @@ __global__ __launch_bounds__(1024) void k_read(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
   const int u = blockIdx.x * NW + wave, p0 = blockIdx.y * kTile;
   const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  const int n = thi - tlo;
+  __shared__ u32x4 zl[NU][64];
+  __shared__ uint64_t kred[16][kTile];
 
-  u32x4 bf[NU];
-  ReadTile<T>::load_z(Z, M, p0, lane, bf);
   const int p = p0 + (lane & 15);
   const bool act = p < M;
   const bool sample = act && temp != nullptr && temp[p / B] != 0;
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
 
-  // bf16 tiles are prefetched one tile ahead; fp32 tiles (twice the registers)
-  // are loaded in place so that the wave stays within its register budget.
-  constexpr bool kPrefetch = sizeof(T) == 2;
-  u32x4 a[NU], an[kPrefetch ? NU : 1];
-  if (kPrefetch && tlo < thi) ReadTile<T>::load_w(W, V, tlo, lane, a);
-  for (int t = tlo; t < thi; ++t) {
-    if constexpr (kPrefetch) {
-      if (t + 1 < thi) ReadTile<T>::load_w(W, V, t + 1, lane, an);
-    } else {
-      ReadTile<T>::load_w(W, V, t, lane, a);
-    }
-    const floatx4 acc = ReadTile<T>::chain(a, bf);
+  auto epilogue = [&](const floatx4& acc, int t) {
     const int row0 = t * kTile + 4 * (lane >> 4);
     if (act) {
-      const floatx4 sv = *reinterpret_cast<const floatx4*>(S + (size_t)p * ldS + row0);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float l = acc[i] + sv[i];
+        const float l = acc[i];
         const int row = row0 + i;
         if (row < V) {
           if (sample)
@@ -150,9 +262,48 @@ __global__ __launch_bounds__(1024) void k_read(
         }
       }
     }
-    if constexpr (kPrefetch) {
+  };
+  auto chain_lds = [&](const u32x4 (&a)[NU], floatx4 acc) {
 #pragma unroll
-      for (int i = 0; i < NU; ++i) a[i] = an[i];
+    for (int i = 0; i < NU; ++i) acc = Mfma<T>::mma(a[i], zl[i][lane], acc);
+    return acc;
+  };
+
+  if (n >= 1 && n <= kReadMaxT) {
+    // tiles t0, t1 resident; t2 reuses t0's registers once t0's chain is issued
+    const int t0 = tlo, t1 = tlo + (n > 1 ? 1 : 0), t2 = tlo + (n > 2 ? 2 : n - 1);
+    u32x4 a0[NU], a1[NU];
+    ReadTile<T>::load_w(W, V, t0, lane, a0);
+    floatx4 c0 = ReadTile<T>::load_s(S, ldS, p, act, t0, lane);
+    ReadTile<T>::load_w(W, V, t1, lane, a1);
+    floatx4 c1 = ReadTile<T>::load_s(S, ldS, p, act, t1, lane);
+    if (wave == 0) {
+      u32x4 bf[NU];
+      ReadTile<T>::load_z(Z, M, p0, lane, bf);
+#pragma unroll
+      for (int i = 0; i < NU; ++i) zl[i][lane] = bf[i];
+    }
+    __syncthreads();
+    const floatx4 r0 = chain_lds(a0, c0);
+    ReadTile<T>::load_w(W, V, t2, lane, a0);
+    c0 = ReadTile<T>::load_s(S, ldS, p, act, t2, lane);
+    epilogue(r0, t0);
+    const floatx4 r1 = chain_lds(a1, c1);
+    if (n > 1) epilogue(r1, t1);
+    const floatx4 r2 = chain_lds(a0, c0);
+    if (n > 2) epilogue(r2, t2);
+  } else {
+    if (wave == 0) {
+      u32x4 bf[NU];
+      ReadTile<T>::load_z(Z, M, p0, lane, bf);
+#pragma unroll
+      for (int i = 0; i < NU; ++i) zl[i][lane] = bf[i];
+    }
+    __syncthreads();
+    u32x4 a[NU];
+    for (int t = tlo; t < thi; ++t) {
+      ReadTile<T>::load_w(W, V, t, lane, a);
+      epilogue(chain_lds(a, ReadTile<T>::load_s(S, ldS, p, act, t, lane)), t);
     }
   }
 #pragma unroll
@@ -163,7 +314,6 @@ __global__ __launch_bounds__(1024) void k_read(
   }
   if (lane < 16 && sample) stats[(size_t)u * M + p] = st;
 
-  __shared__ uint64_t kred[16][kTile];
   if (lane < 16) kred[wave][lane] = best;
   __syncthreads();
   if (threadIdx.x < kTile) {
@@ -203,17 +353,28 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
   int NU = 0, NW = 0;
   if (!pick_lm_split(h->H, Mfma<T>::KU, &NU, &NW)) return hipErrorInvalidValue;
   dim3 grid(h->lm_chunks, (M + kTile - 1) / kTile), block(NW * kWave);
+  const bool lds = (size_t)h->H * sizeof(T) <= 16u * kHChunks;
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, 0, st, (const T*)h->W_lm, (const T*)hidden, h->V, h->H,
                        M, h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
                        h->B);
   };
-  switch (NU) {
-    case 1: args(k_lmhead<T, 1>); break;
-    case 2: args(k_lmhead<T, 2>); break;
-    case 4: args(k_lmhead<T, 4>); break;
-    case 8: args(k_lmhead<T, 8>); break;
-    default: args(k_lmhead<T, 16>); break;
+  if (lds) {
+    switch (NU) {
+      case 1: args(k_lmhead_lds<T, 1>); break;
+      case 2: args(k_lmhead_lds<T, 2>); break;
+      case 4: args(k_lmhead_lds<T, 4>); break;
+      case 8: args(k_lmhead_lds<T, 8>); break;
+      default: args(k_lmhead_lds<T, 16>); break;
+    }
+  } else {
+    switch (NU) {
+      case 1: args(k_lmhead<T, 1>); break;
+      case 2: args(k_lmhead<T, 2>); break;
+      case 4: args(k_lmhead<T, 4>); break;
+      case 8: args(k_lmhead<T, 8>); break;
+      default: args(k_lmhead<T, 16>); break;
+    }
   }
   return hipGetLastError();
 }

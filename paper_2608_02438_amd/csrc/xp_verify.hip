@@ -53,16 +53,18 @@ __device__ float refined_logit(int with_read, const float* __restrict__ S, int l
   if (with_read) {
     constexpr int NU = ReadTile<T>::NU;
     u32x4 bf[NU], a[NU];
+    const int pl = (p & ~15) + (lane & 15);
     ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
     ReadTile<T>::load_w(W_r, V, v / 16, lane, a);
-    const floatx4 acc = ReadTile<T>::chain(a, bf);
+    const floatx4 acc =
+        ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, pl, pl < M, v / 16, lane));
     const int rr = v & 15, src = (rr >> 2) * 16 + (p & 15);
     const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
     const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
     const int comp = rr & 3;
     d = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
   }
-  return with_read ? d + S[(size_t)p * ldS + v] : S[(size_t)p * ldS + v];
+  return with_read ? d : S[(size_t)p * ldS + v];
 }
 
 // One wave per sequence: accept scan.  vpos[b] = rejected position, or B.
@@ -161,17 +163,17 @@ __global__ __launch_bounds__(1024) void k_vresid(
   const double lp = resid ? lse[p] : 0.0;
   double mr = 0.0, mp = 0.0;
   for (int t = tlo; t < thi; ++t) {
-    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    floatx4 acc = ReadTile<T>::load_s(S, ldS, p, resid, t, lane);
     if (with_read) {
       ReadTile<T>::load_w(W_r, V, t, lane, a);
-      acc = ReadTile<T>::chain(a, bf);
+      acc = ReadTile<T>::chain(a, bf, acc);
     }
     if (act) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = t * kTile + 4 * (lane >> 4) + i;
         if (row < V) {
-          const float l = resid ? acc[i] + S[(size_t)p * ldS + row] : 0.f;
+          const float l = resid ? acc[i] : 0.f;
           double res, pw;
           resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
           mr += res;
@@ -270,16 +272,17 @@ __global__ __launch_bounds__(64) void k_vfinal(
         const int t = (base - rlo) / kTile + tlo + tt;
         if (t >= thi) break;
         ReadTile<T>::load_w(W_r, V, t, lane, a);
-        const floatx4 acc = ReadTile<T>::chain(a, bf);
+        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, p, true, t, lane));
         const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
         const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
         const float v = cp == 0 ? c0 : cp == 1 ? c1 : cp == 2 ? c2 : c3;
         if ((lane >> 4) == tt) mine = v;
       }
     }
+    if (resid && !with_read && row < rhi) mine = S[(size_t)p * ldS + row];   // K = 0: l = s
     double w = 0.0;
     if (row < rhi) {
-      const float l = resid ? mine + S[(size_t)p * ldS + row] : 0.f;
+      const float l = resid ? mine : 0.f;
       double res, pw;
       resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
       w = use_resid ? res : pw;
