@@ -215,6 +215,213 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
 }
 
 // ---------------------------------------------------------------------------
+// A1, stream-K variant (bf16, 16 * H * 2 <= 128 KB).  W_lm is read with
+// line-complete loads: an item is 16 rows x 64 k (2 KB), fetched by two
+// instructions that each cover 8 rows x 128 B, then transposed through a
+// per-wave 2 KB LDS tile into MFMA operand order; h (16 positions) lives in
+// LDS for the whole kernel.  Every wave runs the full k range on its own
+// contiguous share of the workgroup's (tile, k-group) items, so the main loop
+// has no barrier.  A tile whose items straddle a wave boundary is finished
+// once at the end: its partial tiles are added in wave order (= k order), so
+// results do not depend on timing, batch or position block.
+// ---------------------------------------------------------------------------
+constexpr int kSkWaves = 16;
+constexpr int kSkPF = 7;               // items in flight per wave
+
+// XOR swizzle of the 8 16-byte chunks of a transpose-tile row: conflict-free
+// for 8 consecutive lanes writing one row and for 16 lanes reading one chunk
+// of 16 rows.
+__device__ __forceinline__ int sk_slot(int row, int c) { return row * 8 + (c ^ ((row & 7) ^ (row >> 3))); }
+
+template <int PF>
+__global__ __launch_bounds__(1024) void k_lmhead_sk(
+    const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M, int ntiles,
+    int U, float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    const uint8_t* __restrict__ temp, int B) {
+  using MF = Mfma<uint16_t>;
+  __shared__ u32x4 lds[16 * kHChunks + kSkWaves * 128];   // h (128 KB) + transpose tiles (32 KB)
+  u32x4* hl = lds;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  u32x4* tb = lds + 16 * kHChunks + wave * 128;
+  const int u = blockIdx.x, p0 = blockIdx.y * kTile;
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  const int nch = H / 8;                                  // 16-byte chunks per row
+  const int G = H / 64;                                   // items per tile
+  const int N = (thi - tlo) * G;
+  auto wlo = [&](int w) { return (int)(((long)w * N) / kSkWaves); };
+  const int i0 = wlo(wave), i1 = wlo(wave + 1);
+
+  // h: every thread issues its (at most 8) chunk loads at once; rows past M
+  // are loaded from row M-1 and zeroed
+  constexpr int kHPer = 16 * kHChunks / (kSkWaves * kWave);
+  u32x4 hv[kHPer];
+#pragma unroll
+  for (int j = 0; j < kHPer; ++j) {
+    int e = threadIdx.x + kSkWaves * kWave * j;
+    e = e < 16 * nch ? e : 0;
+    const int pr = p0 + e / nch;
+    hv[j] = ld16(X + (size_t)(pr < M ? pr : M - 1) * H + (size_t)(e % nch) * 8);
+  }
+
+  // load role: 8 lanes per row, lane -> (row ri of 8, chunk lc of 8)
+  const int ri = lane >> 3, lc = lane & 7;
+  // MFMA role: row / position li, k-group g
+  const int li = lane & 15, g = lane >> 4;
+  const int p = p0 + li;
+  const bool pact = p < M;
+  const bool psample = pact && temp != nullptr && temp[p / B] != 0;
+  uint64_t best = kKeyMin;
+  Stat st = stat_empty();
+
+  // item counters of the next load: tile (relative) and k-group; frozen at the
+  // wave's last item, so the loads past the end re-read it (no extra bytes)
+  int lt = G > 0 ? i0 / G : 0, lq = i0 - lt * G, ln = i0;
+  auto load_item = [&](u32x4 (&r)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      int row = (tlo + lt) * kTile + 8 * j + ri;
+      row = row < V ? row : V - 1;
+      r[j] = ld16_nt(W + (size_t)row * H + (size_t)(8 * lq + lc) * 8);
+    }
+    if (ln + 1 < i1) {
+      ++ln;
+      if (++lq == G) {
+        lq = 0;
+        ++lt;
+      }
+    }
+  };
+  auto finalize = [&](floatx4 acc, int t) {
+    if (!pact) return;
+    const int row0 = t * kTile + 4 * g;
+    *reinterpret_cast<float4*>(S + (size_t)p * ldS + row0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (row0 + i < V) {
+        if (psample)
+          st = stat_merge(st, Stat{acc[i], 1.f});
+        else
+          best = umax64(best, argmax_key(acc[i], (uint32_t)(row0 + i)));
+      }
+    }
+  };
+
+  const int tf = G > 0 ? i0 / G : 0;                      // first (relative) tile of the wave
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f}, part0 = acc, part1 = acc;
+  int ct = tf, cq = i0 - tf * G;                          // item being computed
+  auto step = [&](const u32x4 (&r)[2], int i) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) tb[sk_slot(8 * j + ri, lc)] = r[j];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int uu = 0; uu < 2; ++uu) {
+      const int c = 4 * uu + g;
+      const u32x4 a = tb[sk_slot(li, c)];
+      const int cc = 8 * cq + c;
+      const u32x4 b = hl[li * kHChunks + ((cc & ~15) | ((cc & 15) ^ li))];
+      acc = MF::mma(a, b, acc);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (cq == G - 1 || i == i1 - 1) {                     // end of a tile segment
+      if (cq == G - 1 && ct * G >= i0)
+        finalize(acc, tlo + ct);
+      else if (ct == tf)
+        part0 = acc;
+      else
+        part1 = acc;
+      acc = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (++cq == G) {
+      cq = 0;
+      ++ct;
+    }
+  };
+
+  u32x4 ring[PF][2];
+  if (i0 < i1) {
+#pragma unroll
+    for (int q = 0; q < PF; ++q) load_item(ring[q]);
+  }
+#pragma unroll
+  for (int j = 0; j < kHPer; ++j) {
+    const int e = threadIdx.x + kSkWaves * kWave * j;
+    if (e < 16 * nch) {
+      const int pp = e / nch, c = e % nch;
+      hl[pp * kHChunks + ((c & ~15) | ((c & 15) ^ pp))] =
+          p0 + pp < M ? hv[j] : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+  __syncthreads();                                        // h is in LDS
+  if (i0 < i1) {
+    int i = i0;
+    for (; i + PF <= i1; i += PF) {
+#pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        step(ring[q], i + q);
+        load_item(ring[q]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < PF; ++q)
+      if (i + q < i1) step(ring[q], i + q);
+  }
+
+  // tiles split between waves: partial tiles through LDS (the h area is free)
+  __syncthreads();
+  floatx4* fx = reinterpret_cast<floatx4*>(lds);          // [wave][2][64]
+  fx[(wave * 2 + 0) * 64 + lane] = part0;
+  fx[(wave * 2 + 1) * 64 + lane] = part1;
+  __syncthreads();
+  if (i0 < i1) {
+    const int tl = (i1 - 1) / G;
+    int tfin = -1;
+    floatx4 a = part0;
+    if (i0 % G == 0 && i1 < (tf + 1) * G) {               // starts a tile it does not finish
+      tfin = tf;
+    } else if (tl > tf && i1 % G != 0) {                  // last tile started here, unfinished
+      tfin = tl;
+      a = part1;
+    }
+    if (tfin >= 0) {
+      for (int w = wave + 1; w < kSkWaves && wlo(w) < (tfin + 1) * G; ++w) {
+        if (wlo(w + 1) > wlo(w)) {
+          const floatx4 o = fx[(w * 2 + 0) * 64 + lane];
+          a[0] += o[0]; a[1] += o[1]; a[2] += o[2]; a[3] += o[3];
+        }
+      }
+      finalize(a, tlo + tfin);
+    }
+  }
+  // per-position selection partials: lanes of one position, then waves in order
+#pragma unroll
+  for (int m = 16; m < 64; m <<= 1) {
+    best = umax64(best, shfl_xor_u64(best, m));
+    Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
+    st = stat_merge(st, o);
+  }
+  uint64_t* kr = reinterpret_cast<uint64_t*>(lds + 2 * kSkWaves * 64);   // past fx
+  Stat* sr = reinterpret_cast<Stat*>(kr + kSkWaves * 16);
+  if (lane < 16) {
+    kr[wave * 16 + lane] = best;
+    sr[wave * 16 + lane] = st;
+  }
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    uint64_t bb = kKeyMin;
+    Stat ss = stat_empty();
+    for (int w = 0; w < kSkWaves; ++w) {
+      bb = umax64(bb, kr[w * 16 + threadIdx.x]);
+      ss = stat_merge(ss, sr[w * 16 + threadIdx.x]);
+    }
+    const int pp = p0 + threadIdx.x;
+    if (pp < M) {
+      keys[(size_t)u * M + pp] = bb;
+      stats[(size_t)u * M + pp] = ss;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
 // the full k range (one chain of MFMAs per tile); the position block's z
 // fragments sit in LDS, shared by the waves.  A unit of at most kReadMaxT
@@ -354,6 +561,15 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
   if (!pick_lm_split(h->H, Mfma<T>::KU, &NU, &NW)) return hipErrorInvalidValue;
   dim3 grid(h->lm_chunks, (M + kTile - 1) / kTile), block(NW * kWave);
   const bool lds = (size_t)h->H * sizeof(T) <= 16u * kHChunks;
+  if constexpr (sizeof(T) == 2) {
+    if (lds) {
+      hipLaunchKernelGGL((k_lmhead_sk<kSkPF>), grid, dim3(kSkWaves * kWave), 0, st,
+                         (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
+                         h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
+                         h->B);
+      return hipGetLastError();
+    }
+  }
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, 0, st, (const T*)h->W_lm, (const T*)hidden, h->V, h->H,
                        M, h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
