@@ -130,6 +130,7 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
       {(void**)&ws.Fg, (size_t)256 * w->H * 4},
       {(void**)&ws.Lp, (npairs ? npairs : 1) * 256 * es},
       {(void**)&ws.ppart, (size_t)2 * prep_ksp(w->H) * Mmax * 256 * 4},
+      {(void**)&ws.Pa, Mmax * 256 * 4},
       {(void**)&ws.c, Mmax * 256 * 4},
       {(void**)&ws.h1, Mmax * 512 * 4},
       {(void**)&ws.z, Mmax * 256 * es},
@@ -284,19 +285,25 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
     return fail(h, XP_EINVAL, "out_logits given without XP_WRITE_LOGITS");
   hipStream_t st = (hipStream_t)stream;
   h->state_valid = false;
+  // All-greedy batches run the selection of pass j-1, Fuse, Mix and the first
+  // Trans product of pass j as one kernel; the others use separate kernels.
+  const bool fused = K > 0 && pass_fused_ok(h, temp);
   XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, st));
   XP_TIMED(XP_STAGE_LMHEAD, launch_lmhead(h, batch * h->B, hidden, temp, st));
-  XP_TIMED(XP_STAGE_SELECT,
-           launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj,
-                         K == 0 ? out_ids : nullptr, K == 0 ? out_iters : nullptr, st));
+  if (!fused)
+    XP_TIMED(XP_STAGE_SELECT,
+             launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj,
+                           K == 0 ? out_ids : nullptr, K == 0 ? out_iters : nullptr, st));
   for (int j = 0; j < K; ++j) {
-    XP_TIMED(XP_STAGE_RSPACE, launch_rspace(h, batch, j, flags, anchor, st));
+    if (fused) XP_TIMED(XP_STAGE_RSPACE, launch_pass(h, batch, j, flags, seed_ids, anchor, out_traj, st));
+    XP_TIMED(XP_STAGE_RSPACE, launch_rspace(h, batch, j, flags, anchor, !fused, st));
     XP_TIMED(XP_STAGE_READ, launch_read(h, batch, j, flags, temp,
                                         (flags & XP_WRITE_LOGITS) ? out_logits : nullptr, st));
     const bool lastp = j == K - 1;
-    XP_TIMED(XP_STAGE_SELECT,
-             launch_select(h, batch, j, K, flags, nullptr, temp, u_draft, out_traj,
-                           lastp ? out_ids : nullptr, lastp ? out_iters : nullptr, st));
+    if (!fused || lastp)
+      XP_TIMED(XP_STAGE_SELECT,
+               launch_select(h, batch, j, K, flags, nullptr, temp, u_draft, out_traj,
+                             lastp ? out_ids : nullptr, lastp ? out_iters : nullptr, st));
   }
   XP_LAUNCH(launch_finish(h, batch, K, flags, out_ids, out_iters, out_logits, st));
   h->last_batch = batch;

@@ -14,7 +14,7 @@ namespace xp {
 
 // Launch shapes of the two vocabulary streams (tuned for 256 CUs).
 constexpr int kLmWaves = 16;    // A1: waves per workgroup, each owning H/16 of the k range
-constexpr int kReadWaves = 16;  // A7: waves per workgroup, each streaming its own tiles
+constexpr int kReadWaves = 8;   // A7: waves per workgroup, each streaming its own tiles
 constexpr int kMaxK = 64;
 
 struct Workspace {
@@ -24,6 +24,7 @@ struct Workspace {
   float* Fg = nullptr;        // [r][H]        W_in[:, r:2r] W_g
   void* Lp = nullptr;         // [npairs][r]   L[d][k][i] (i < k) at pair k(k-1)/2 + i
   float* ppart = nullptr;     // [2][ksp][Mmax][r] k-slice partials of Fh h_k and Fg h_k
+  float* Pa = nullptr;        // [Mmax][r]     Fh h_k + Fg g (pass-invariant part of Fuse)
   float* c = nullptr;         // [Mmax][r]     Mix output of the current pass
   float* h1 = nullptr;        // [Mmax][2r]    silu(W_1 c) of the current pass
   void* z = nullptr;          // [Mmax][r]     Trans output (dtype)
@@ -79,7 +80,10 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
                          int32_t* out_traj, int32_t* out_ids, int32_t* out_iters,
                          hipStream_t st);
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
-                         hipStream_t st);
+                         bool front, hipStream_t st);
+bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
+hipError_t launch_pass(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* seed_ids,
+                       const int32_t* anchor, int32_t* out_traj, hipStream_t st);
 int prep_ksp(int H);
 hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
                        float* out_logits, hipStream_t st);

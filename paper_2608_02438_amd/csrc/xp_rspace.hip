@@ -10,6 +10,7 @@
 // into three exact bf16 terms (products exact, sums in fp32); with fp32
 // weights they use v_mfma_f32_16x16x4_f32.  z is rounded to the weight dtype.
 #include "xp_internal.h"
+#include "xp_split.h"
 
 namespace xp {
 
@@ -37,6 +38,8 @@ __device__ __forceinline__ floatx4 mma4(float4 a, float4 b, floatx4 c) {
 // Workgroup (0,0,0) also clears the per-call Jacobi state.
 // ---------------------------------------------------------------------------
 constexpr int kPrepPBG = 8;            // position blocks per workgroup
+constexpr int kMaxKsp = 8;             // most k-slices of the prep product
+constexpr int kPrepSteps = 4;          // 32-wide steps per wave loaded at once
 
 // k-slices of the prep product: the most (up to 8) that leave every wave a
 // whole number of 32-element (bf16) or 16-element (fp32) MFMA steps.
@@ -44,51 +47,6 @@ int prep_ksp(int H) {
   for (int k = 8; k > 1; k >>= 1)
     if (H % (k * 4 * 32) == 0) return k;
   return 1;
-}
-
-// fp32 -> three bf16 terms with x == hi + mid + lo exactly (truncating split:
-// each term keeps the next 8 significant bits of the 24).  With bf16 weights
-// every product w * term is exact in fp32, so W x on the bf16 matrix cores
-// is W x with fp32 accumulation, as on the fp32 path.
-__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
-  const uint32_t xh = __float_as_uint(x) & 0xFFFF0000u;
-  const float r1 = x - __uint_as_float(xh);
-  const uint32_t xm = __float_as_uint(r1) & 0xFFFF0000u;
-  const float r2 = r1 - __uint_as_float(xm);
-  h = xh >> 16;
-  m = xm >> 16;
-  l = __float_as_uint(r2) >> 16;
-}
-// Three bf16x8 MFMA operands from 8 fp32 values (two float4).
-__device__ __forceinline__ void split3x8(float4 v0, float4 v1, u32x4& bh, u32x4& bm, u32x4& bl) {
-  const float x[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-  uint32_t h[8], m[8], l[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) split3(x[i], h[i], m[i], l[i]);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    bh[i] = h[2 * i] | (h[2 * i + 1] << 16);
-    bm[i] = m[2 * i] | (m[2 * i + 1] << 16);
-    bl[i] = l[2 * i] | (l[2 * i + 1] << 16);
-  }
-}
-// acc += a . x over one 32-k step, x (8 fp32 per lane) split into three terms;
-// `a` is the exact bf16 operand.  The split operand may be either A or B.
-__device__ __forceinline__ floatx4 mma_split_b(u32x4 a, float4 x0, float4 x1, floatx4 acc) {
-  u32x4 bh, bm, bl;
-  split3x8(x0, x1, bh, bm, bl);
-  acc = Mfma<uint16_t>::mma(a, bh, acc);
-  acc = Mfma<uint16_t>::mma(a, bm, acc);
-  acc = Mfma<uint16_t>::mma(a, bl, acc);
-  return acc;
-}
-__device__ __forceinline__ floatx4 mma_split_a(float4 x0, float4 x1, u32x4 b, floatx4 acc) {
-  u32x4 ah, am, al;
-  split3x8(x0, x1, ah, am, al);
-  acc = Mfma<uint16_t>::mma(ah, b, acc);
-  acc = Mfma<uint16_t>::mma(am, b, acc);
-  acc = Mfma<uint16_t>::mma(al, b, acc);
-  return acc;
 }
 
 template <typename T>
@@ -117,13 +75,28 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
     const int pc = p < M ? p : M - 1;
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
     if constexpr (sizeof(T) == 2) {
+      // all (at most kPrepSteps) steps of the wave's slice are loaded at once
       const T* brow = hid + (size_t)pc * H + k0 + 8 * g;
-      for (int u = 0; u < kw / 32; ++u) {
-        const float4 a0 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g);
-        const float4 a1 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g + 4);
-        u32x4 bv = ld16(brow + u * 32);
-        if (p >= M) bv = u32x4{0u, 0u, 0u, 0u};
-        acc = mma_split_a(a0, a1, bv, acc);
+      const int ns = kw / 32;
+      float4 a0[kPrepSteps], a1[kPrepSteps];
+      u32x4 bv[kPrepSteps];
+#pragma unroll
+      for (int u = 0; u < kPrepSteps; ++u) {
+        const int uc = u < ns ? u : ns - 1;
+        a0[u] = *reinterpret_cast<const float4*>(arow + uc * 32 + 8 * g);
+        a1[u] = *reinterpret_cast<const float4*>(arow + uc * 32 + 8 * g + 4);
+        bv[u] = ld16(brow + uc * 32);
+      }
+#pragma unroll
+      for (int u = 0; u < kPrepSteps; ++u) {
+        if (u < ns) acc = mma_split_a(a0[u], a1[u], p < M ? bv[u] : u32x4{0u, 0u, 0u, 0u}, acc);
+      }
+      for (int u = kPrepSteps; u < ns; ++u) {       // slices longer than kPrepSteps steps
+        const float4 c0 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g);
+        const float4 c1 = *reinterpret_cast<const float4*>(arow + u * 32 + 8 * g + 4);
+        u32x4 b1 = ld16(brow + u * 32);
+        if (p >= M) b1 = u32x4{0u, 0u, 0u, 0u};
+        acc = mma_split_a(c0, c1, b1, acc);
       }
     } else {
       const T* brow = hid + (size_t)pc * H + k0 + 4 * g;
@@ -163,12 +136,62 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
 // under a branch (indices are clamped, results masked), so the loads overlap.
 // ---------------------------------------------------------------------------
 
+// Pa_k = F_h h_k + (1/B) sum_j F_g h_j: the pass-invariant part of Fuse,
+// from the prep k-slice partials (added in slice order), once per call.
+template <int BP>
+__global__ __launch_bounds__(256) void k_prep_sum(int B, int M, int ksp,
+                                                  const float* __restrict__ part,
+                                                  float* __restrict__ Pa) {
+  constexpr int r = 256, EPT = BP / 16;
+  __shared__ float G[BP][17];
+  __shared__ float ug[16];
+  const int b = blockIdx.x, dt = blockIdx.y, tid = threadIdx.x;
+  const int dl = tid & 15, kg = tid >> 4, d = dt * 16 + dl;
+  float phv[EPT][kMaxKsp], pgv[EPT][kMaxKsp];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    const size_t m = (size_t)b * B + (k < B ? k : B - 1);
+#pragma unroll
+    for (int q = 0; q < kMaxKsp; ++q) {
+      const int qc = q < ksp ? q : ksp - 1;
+      phv[j][q] = part[((size_t)qc * M + m) * r + d];
+      pgv[j][q] = part[((size_t)(ksp + qc) * M + m) * r + d];
+    }
+  }
+  float ph[EPT];
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    float sh = 0.f, sg = 0.f;
+#pragma unroll
+    for (int q = 0; q < kMaxKsp; ++q) {
+      sh += q < ksp ? phv[j][q] : 0.f;
+      sg += q < ksp ? pgv[j][q] : 0.f;
+    }
+    ph[j] = sh;
+    const int k = kg + 16 * j;
+    if (k < B) G[k][dl] = sg;
+  }
+  __syncthreads();
+  if (tid < 16) {                                    // (W_in[:,r:2r] W_g) g, g = mean_k h_k
+    float t = 0.f;
+    for (int k = 0; k < B; ++k) t += G[k][tid];
+    ug[tid] = t / (float)B;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < EPT; ++j) {
+    const int k = kg + 16 * j;
+    if (k < B) Pa[((size_t)b * B + k) * r + d] = ph[j] + ug[dl];
+  }
+}
+
 // Fuse (gather form) and Mix for 16 feature dims d of one sequence.  Mix is
 // independent per d (eq. mix: c^(d) = (I + L^(d)) a^(d)), so the 16 dims of a
 // workgroup need only their own 16 columns of every L^(d).
 template <typename T, int BP>
 __global__ __launch_bounds__(256) void k_fusemix(
-    int B, int V, int M, int ksp, const float* __restrict__ part, const float* __restrict__ Ttab,
+    int B, int V, int M, const float* __restrict__ Pa, const float* __restrict__ Ttab,
     const T* __restrict__ Lp, const int32_t* __restrict__ anchor, const int32_t* __restrict__ Y,
     float* __restrict__ c, uint32_t* __restrict__ err, const int32_t* __restrict__ ctrl,
     int skip_when_done) {
@@ -179,7 +202,6 @@ __global__ __launch_bounds__(256) void k_fusemix(
   constexpr int CPP = (int)sizeof(T);                // 16-byte chunks per pair (16 dims)
   constexpr int LCH_T = (NPAIR * CPP + 255) / 256;   // chunks per thread
   __shared__ float A[BP][17];
-  __shared__ float ug[16];
   __shared__ u32x4 Ls[NPAIR * CPP > 0 ? NPAIR * CPP : 1];
   const int b = blockIdx.x, dt = blockIdx.y, tid = threadIdx.x;
   const int dl = tid & 15, kg = tid >> 4, d = dt * 16 + dl;
@@ -193,7 +215,8 @@ __global__ __launch_bounds__(256) void k_fusemix(
     const int pr = q / CPP, cc = q % CPP;
     lc[j] = *reinterpret_cast<const u32x4*>(Lp + (size_t)pr * r + dt * 16 + cc * (16 / CPP));
   }
-  float ph[EPT], pg[EPT], tv[EPT];
+  // the Fuse constant Pa_k and the previous tokens, issued together
+  float pa[EPT], tv[EPT];
   int xv[EPT];
   const int ya = anchor[b];
 #pragma unroll
@@ -201,14 +224,9 @@ __global__ __launch_bounds__(256) void k_fusemix(
     const int k = kg + 16 * j;
     const int kc = k < B ? k : B - 1;
     const size_t m = (size_t)b * B + kc;
-    float sh = 0.f, sg = 0.f;
-    for (int q = 0; q < ksp; ++q) {
-      sh += part[((size_t)q * M + m) * r + d];
-      sg += part[((size_t)(ksp + q) * M + m) * r + d];
-    }
-    ph[j] = sh;
-    pg[j] = sg;
-    xv[j] = kc == 0 ? ya : Y[m - 1];
+    pa[j] = Pa[m * r + d];
+    xv[j] = Y[kc == 0 ? m : m - 1];
+    if (kc == 0) xv[j] = ya;
   }
   bool bad = false;
 #pragma unroll
@@ -224,23 +242,11 @@ __global__ __launch_bounds__(256) void k_fusemix(
     if (q < nch) Ls[q] = lc[j];
   }
 #pragma unroll
-  for (int j = 0; j < EPT; ++j) {
-    const int k = kg + 16 * j;
-    if (k < B) A[k][dl] = pg[j];
+  for (int j = 0; j < EPT; ++j) {                    // a_k = Pa_k + T[x_{k-1}]; rows >= B
+    const int k = kg + 16 * j;                       // are zeroed without a branch
+    A[k][dl] = (pa[j] + tv[j]) * (k < B ? 1.f : 0.f);
   }
   if (bad) atomicOr(err, XP_DEVERR_TOKEN);
-  __syncthreads();
-  if (tid < 16) {                                    // (W_in[:,r:2r] W_g) g, g = mean_k h_k
-    float t = 0.f;
-    for (int k = 0; k < B; ++k) t += A[k][tid];
-    ug[tid] = t / (float)B;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < EPT; ++j) {
-    const int k = kg + 16 * j;
-    if (k < B) A[k][dl] = ph[j] + ug[dl] + tv[j];   // a_k = P_k + T[x_{k-1}]
-  }
   __syncthreads();
   const T* ls = reinterpret_cast<const T*>(Ls);      // [pair][16 dims]
 #pragma unroll
@@ -439,35 +445,45 @@ hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t 
     hipLaunchKernelGGL((k_prep<float>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
                        (const float*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
                        h->ws.ctrl);
+  if (h->B <= 16)
+    hipLaunchKernelGGL((k_prep_sum<16>), dim3(batch, 16), dim3(256), 0, st, h->B, M, ksp,
+                       h->ws.ppart, h->ws.Pa);
+  else
+    hipLaunchKernelGGL((k_prep_sum<32>), dim3(batch, 16), dim3(256), 0, st, h->B, M, ksp,
+                       h->ws.ppart, h->ws.Pa);
   return hipGetLastError();
 }
 
+// front = false launches only the second Trans product (the fused pass kernel
+// has already produced c and h1).
 template <typename T, int BP>
 static void rspace_t(xp_handle* h, int batch, int pass, int skip, const int32_t* anchor,
-                     hipStream_t st) {
+                     bool front, hipStream_t st) {
   const int M = batch * h->B;
-  hipLaunchKernelGGL((k_fusemix<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B, h->V, M,
-                     prep_ksp(h->H), h->ws.ppart, h->ws.T, (const T*)h->ws.Lp, anchor,
-                     h->ws.Y[pass % 2], h->ws.c, h->ws.err, h->ws.ctrl, skip);
-  hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
-                     (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.ctrl, skip);
+  if (front) {
+    hipLaunchKernelGGL((k_fusemix<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B, h->V, M,
+                       h->ws.Pa, h->ws.T, (const T*)h->ws.Lp, anchor, h->ws.Y[pass % 2], h->ws.c,
+                       h->ws.err, h->ws.ctrl, skip);
+    hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
+                       (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.ctrl, skip);
+  }
   hipLaunchKernelGGL((k_trans2<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B,
                      (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.ctrl, skip);
 }
 
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
-                         hipStream_t st) {
+                         bool front, hipStream_t st) {
   const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16) {
     if (h->B <= 16)
-      rspace_t<uint16_t, 16>(h, batch, pass, skip, anchor, st);
+      rspace_t<uint16_t, 16>(h, batch, pass, skip, anchor, front, st);
     else
-      rspace_t<uint16_t, 32>(h, batch, pass, skip, anchor, st);
+      rspace_t<uint16_t, 32>(h, batch, pass, skip, anchor, front, st);
   } else {
     if (h->B <= 16)
-      rspace_t<float, 16>(h, batch, pass, skip, anchor, st);
+      rspace_t<float, 16>(h, batch, pass, skip, anchor, front, st);
     else
-      rspace_t<float, 32>(h, batch, pass, skip, anchor, st);
+      rspace_t<float, 32>(h, batch, pass, skip, anchor, front, st);
   }
   return hipGetLastError();
 }

@@ -128,9 +128,16 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
 }
 
 // One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
-// caller's seed ids); mode 1: the selection of Jacobi pass `pass`.
+// caller's seed ids); mode 1: the selection of Jacobi pass `pass`.  Greedy
+// rows issue every key load of the wave's positions (and the previous
+// iterate and iteration count) before the first use, so a greedy selection
+// costs one memory round trip.
+constexpr int kSelWaves = 8;
+constexpr int kSelKPL = 4;                      // keys per lane and position (256 units)
+constexpr int kSelPPW = 32 / kSelWaves;         // positions per wave (B <= 32)
+
 template <typename T>
-__global__ __launch_bounds__(512) void k_select(
+__global__ __launch_bounds__(kSelWaves * kWave) void k_select(
     int mode, int pass, int batch, int B, int V, int M, const float* __restrict__ S, int ldS,
     const T* __restrict__ W_r, const T* __restrict__ Z, const uint64_t* __restrict__ keys,
     int nkeys, const Stat* __restrict__ stats, int ntiles, int U,
@@ -140,17 +147,35 @@ __global__ __launch_bounds__(512) void k_select(
     int32_t* __restrict__ ctrl, uint32_t* __restrict__ err, int early_exit,
     int32_t* __restrict__ out_ids, int32_t* __restrict__ out_iters, int K) {
   const int b = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ int changed;
+  const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
+  // independent loads first (keys unconditionally: unused ones are harmless)
+  uint64_t kv[kSelPPW][kSelKPL];
+  int yprev[kSelPPW];
+#pragma unroll
+  for (int m = 0; m < kSelPPW; ++m) {
+    const int k = wave + kSelWaves * m;
+    const int p = b * B + (k < B ? k : B - 1);
+#pragma unroll
+    for (int r = 0; r < kSelKPL; ++r) {
+      const int i = lane + kWave * r;
+      kv[m][r] = keys[(size_t)(i < nkeys ? i : nkeys - 1) * M + p];
+    }
+    yprev[m] = mode == 1 ? Yprev[p] : 0;
+  }
+  const int it0 = iters[b];
+  const bool sample = temp != nullptr && temp[b] != 0;
   if (threadIdx.x == 0) changed = 0;
   __syncthreads();
-  const bool sample = temp != nullptr && temp[b] != 0;
-  const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
-  for (int k = wave; k < B; k += NW) {
+#pragma unroll
+  for (int m = 0; m < kSelPPW; ++m) {
+    const int k = wave + kSelWaves * m;
+    if (k >= B) continue;                         // wave-uniform
     const int p = b * B + k;
     int y = 0;
     if (skip) {
-      y = Yprev[p];
+      y = yprev[m];
     } else if (mode == 0 && seed_ids != nullptr) {
       y = seed_ids[p];
       if (y < 0 || y >= V) {
@@ -160,10 +185,13 @@ __global__ __launch_bounds__(512) void k_select(
       if (sample)
         sample_position<T>(0, p, 0.f, S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p, false);
     } else if (!sample) {
-      uint64_t best = kKeyMin;
-      for (int i = lane; i < nkeys; i += 64) best = umax64(best, keys[(size_t)i * M + p]);
+      uint64_t best = kv[m][0];
 #pragma unroll
-      for (int m = 1; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
+      for (int r = 1; r < kSelKPL; ++r) best = umax64(best, kv[m][r]);
+      for (int i = lane + kWave * kSelKPL; i < nkeys; i += kWave)   // more than 256 units
+        best = umax64(best, keys[(size_t)i * M + p]);
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) best = umax64(best, shfl_xor_u64(best, o));
       y = (int)key_index(best);
     } else {
       y = sample_position<T>(mode, p, u_draft[p], S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p,
@@ -173,16 +201,18 @@ __global__ __launch_bounds__(512) void k_select(
       Ynew[p] = y;
       if (traj) traj[p] = y;
       if (out_ids) out_ids[p] = y;
-      if (mode == 1 && y != Yprev[p]) atomicOr(&changed, 1);
+      if (mode == 1 && y != yprev[m]) atomicOr(&changed, 1);
     }
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    if (mode == 1 && !skip && changed == 0 && iters[b] == 0) {
-      iters[b] = pass + 1;
+    int it = it0;
+    if (mode == 1 && !skip && changed == 0 && it == 0) {
+      it = pass + 1;
+      iters[b] = it;
       if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
     }
-    if (out_iters) out_iters[b] = mode == 0 ? 0 : (iters[b] ? iters[b] : K);
+    if (out_iters) out_iters[b] = mode == 0 ? 0 : (it ? it : K);
   }
 }
 
@@ -210,14 +240,14 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
   const int U = mode == 0 ? h->lm_chunks : h->read_units;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16)
-    hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(512), 0, st, mode, pass, batch,
+    hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,
                        h->B, h->V, M, h->ws.s, h->ldS, (const uint16_t*)h->W_r,
                        (const uint16_t*)h->ws.z, h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
                        h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early, out_ids, out_iters,
                        K);
   else
-    hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(512), 0, st, mode, pass, batch, h->B,
+    hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch, h->B,
                        h->V, M, h->ws.s, h->ldS, (const float*)h->W_r, (const float*)h->ws.z,
                        h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,

@@ -269,7 +269,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   const int li = lane & 15, g = lane >> 4;
   const int p = p0 + li;
   const bool pact = p < M;
-  const bool psample = pact && temp != nullptr && temp[p / B] != 0;
+  bool psample = false;                                   // set once the loads are in flight
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
 
@@ -341,6 +341,11 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   if (i0 < i1) {
 #pragma unroll
     for (int q = 0; q < PF; ++q) load_item(ring[q]);
+  }
+  {
+    int tv = 0;
+    if (temp != nullptr) tv = temp[(pact ? p : M - 1) / B];
+    psample = pact && tv != 0;
   }
 #pragma unroll
   for (int j = 0; j < kHPer; ++j) {
@@ -423,35 +428,36 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
 
 // ---------------------------------------------------------------------------
 // A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
-// the full k range (one chain of MFMAs per tile); the position block's z
-// fragments sit in LDS, shared by the waves.  A unit of at most kReadMaxT
-// tiles (the common case) issues all its W_r and s loads before the first
-// MFMA; the loads are unconditional (a short unit re-reads its last tile,
-// which hits in L2), so the wait counts stay exact.  Workgroups merge their
-// waves' argmax keys; sampled rows write one (max, sum) per wave unit.
+// the full k range (one chain of MFMAs per tile, seeded with s); the position
+// block's z fragments sit in LDS, shared by the waves.  A unit of at most
+// kReadRes tiles (the common case) keeps all of them in registers: every W_r,
+// s and z load of the wave is issued, unconditionally, before the first
+// MFMA, so the whole unit is in flight at once (a short unit re-reads its
+// last tile, which hits in L2).  Workgroups merge their waves' argmax keys;
+// sampled rows write one (max, sum) per wave unit.
 // ---------------------------------------------------------------------------
-constexpr int kReadMaxT = 3;
-
 template <typename T>
-__global__ __launch_bounds__(1024) void k_read(
+__global__ __launch_bounds__(kReadWaves * kWave) void k_read(
     const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int ldS, int V,
     int M, int ntiles, int U, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B, float* __restrict__ out_logits,
     const int32_t* __restrict__ ctrl, int skip_when_done) {
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   constexpr int NU = ReadTile<T>::NU;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
-  const int u = blockIdx.x * NW + wave, p0 = blockIdx.y * kTile;
+  constexpr int NR = sizeof(T) == 2 ? 5 : 2;      // resident tiles per wave (32 / 64 VGPRs each)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int u = blockIdx.x * kReadWaves + wave, p0 = blockIdx.y * kTile;
   const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
   const int n = thi - tlo;
   __shared__ u32x4 zl[NU][64];
-  __shared__ uint64_t kred[16][kTile];
+  __shared__ uint64_t kred[kReadWaves][kTile];
 
   const int p = p0 + (lane & 15);
   const bool act = p < M;
-  const bool sample = act && temp != nullptr && temp[p / B] != 0;
+  const int pc = act ? p : M - 1;
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
+  bool sample = false;
 
   auto epilogue = [&](const floatx4& acc, int t) {
     const int row0 = t * kTile + 4 * (lane >> 4);
@@ -475,42 +481,59 @@ __global__ __launch_bounds__(1024) void k_read(
     for (int i = 0; i < NU; ++i) acc = Mfma<T>::mma(a[i], zl[i][lane], acc);
     return acc;
   };
+  auto load_s = [&](int t) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(S + (size_t)pc * ldS + t * kTile + 4 * (lane >> 4));
+    return act ? v : floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+  // z fragments of the position block, one 16-byte chunk per thread
+  constexpr int kZPer = (NU * 64 + kReadWaves * kWave - 1) / (kReadWaves * kWave);
+  u32x4 zv[kZPer];
+  auto load_z = [&]() {
+#pragma unroll
+    for (int j = 0; j < kZPer; ++j) {
+      const int c = threadIdx.x + kReadWaves * kWave * j;
+      const int zi = (c / 64) % NU, zlane = c % 64;
+      const int zp = p0 + (zlane & 15);
+      zv[j] = ld16(Z + (size_t)(zp < M ? zp : M - 1) * 256 + (zlane >> 4) * ReadTile<T>::EPB +
+                   zi * ReadTile<T>::KU);
+      if (zp >= M) zv[j] = u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto put_z = [&]() {
+#pragma unroll
+    for (int j = 0; j < kZPer; ++j) {
+      const int c = threadIdx.x + kReadWaves * kWave * j;
+      if (c < NU * 64) zl[c / 64][c % 64] = zv[j];
+    }
+  };
 
-  if (n >= 1 && n <= kReadMaxT) {
-    // tiles t0, t1 resident; t2 reuses t0's registers once t0's chain is issued
-    const int t0 = tlo, t1 = tlo + (n > 1 ? 1 : 0), t2 = tlo + (n > 2 ? 2 : n - 1);
-    u32x4 a0[NU], a1[NU];
-    ReadTile<T>::load_w(W, V, t0, lane, a0);
-    floatx4 c0 = ReadTile<T>::load_s(S, ldS, p, act, t0, lane);
-    ReadTile<T>::load_w(W, V, t1, lane, a1);
-    floatx4 c1 = ReadTile<T>::load_s(S, ldS, p, act, t1, lane);
-    if (wave == 0) {
-      u32x4 bf[NU];
-      ReadTile<T>::load_z(Z, M, p0, lane, bf);
+  if (n >= 1 && n <= NR) {
+    u32x4 a[NR][NU];
+    floatx4 c[NR];
 #pragma unroll
-      for (int i = 0; i < NU; ++i) zl[i][lane] = bf[i];
-    }
+    for (int j = 0; j < NR; ++j) ReadTile<T>::load_w(W, V, tlo + (j < n ? j : n - 1), lane, a[j]);
+#pragma unroll
+    for (int j = 0; j < NR; ++j) c[j] = load_s(tlo + (j < n ? j : n - 1));
+    load_z();
+    int tv = 0;
+    if (temp != nullptr) tv = temp[pc / B];
+    sample = act && tv != 0;
+    put_z();
     __syncthreads();
-    const floatx4 r0 = chain_lds(a0, c0);
-    ReadTile<T>::load_w(W, V, t2, lane, a0);
-    c0 = ReadTile<T>::load_s(S, ldS, p, act, t2, lane);
-    epilogue(r0, t0);
-    const floatx4 r1 = chain_lds(a1, c1);
-    if (n > 1) epilogue(r1, t1);
-    const floatx4 r2 = chain_lds(a0, c0);
-    if (n > 2) epilogue(r2, t2);
-  } else {
-    if (wave == 0) {
-      u32x4 bf[NU];
-      ReadTile<T>::load_z(Z, M, p0, lane, bf);
 #pragma unroll
-      for (int i = 0; i < NU; ++i) zl[i][lane] = bf[i];
-    }
+    for (int j = 0; j < NR; ++j)
+      if (j < n) epilogue(chain_lds(a[j], c[j]), tlo + j);
+  } else {
+    load_z();
+    int tv = 0;
+    if (temp != nullptr) tv = temp[pc / B];
+    sample = act && tv != 0;
+    put_z();
     __syncthreads();
     u32x4 a[NU];
     for (int t = tlo; t < thi; ++t) {
       ReadTile<T>::load_w(W, V, t, lane, a);
-      epilogue(chain_lds(a, ReadTile<T>::load_s(S, ldS, p, act, t, lane)), t);
+      epilogue(chain_lds(a, load_s(t)), t);
     }
   }
 #pragma unroll
@@ -525,7 +548,7 @@ __global__ __launch_bounds__(1024) void k_read(
   __syncthreads();
   if (threadIdx.x < kTile) {
     uint64_t b = kKeyMin;
-    for (int w = 0; w < NW; ++w) b = umax64(b, kred[w][threadIdx.x]);
+    for (int w = 0; w < kReadWaves; ++w) b = umax64(b, kred[w][threadIdx.x]);
     const int pp = p0 + threadIdx.x;
     if (pp < M) keys[(size_t)blockIdx.x * M + pp] = b;
   }

@@ -125,6 +125,37 @@ def test_early_exit_run_to_run_and_batch_invariance():
     assert np.array_equal(out.logits.cpu().numpy()[0], a.logits[2])
 
 
+@pytest.mark.parametrize("B,batch", [(16, 4), (8, 3)])
+def test_fused_greedy_pass_matches_separate_kernels(B, batch):
+    """All-greedy batches run selection + Fuse + Mix + W_1 as one kernel; an
+    all-zero temperature vector sends the same rows through the separate
+    select / fusemix / trans1 kernels.  Both compute the same fp32 values in
+    the same order, so every output must agree bit for bit (also with early
+    exit, which must not change ids or pass counts)."""
+    import torch
+    _say(f"case: fused vs separate greedy pass kernels, bf16 B={B} batch={batch}")
+    prob = custom_problem("bf16", H=512, V=2000, B=B, batch=batch, K=8, sigmas=STRESS, seed=7)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    assert dev["temp"] is None
+    fused = run_device(ref, prob, dev)
+    sep = dict(dev)
+    sep["temp"] = torch.zeros(batch, dtype=torch.uint8, device="cuda")
+    sep["u_draft"] = torch.zeros((batch, B), dtype=torch.float32, device="cuda")
+    split = run_device(ref, prob, sep)
+    assert fused.iters.max() >= 3
+    assert np.array_equal(fused.ids, split.ids)
+    assert np.array_equal(fused.iters, split.iters)
+    assert np.array_equal(fused.traj, split.traj)
+    assert np.array_equal(fused.logits, split.logits)
+    fe = run_device(ref, prob, dev, early_exit=True, write_logits=False)
+    se = run_device(ref, prob, sep, early_exit=True, write_logits=False)
+    assert np.array_equal(fe.ids, fused.ids) and np.array_equal(fe.iters, fused.iters)
+    assert np.array_equal(se.ids, fused.ids) and np.array_equal(se.iters, fused.iters)
+    tally, _ = check_refine(prob, fused)
+    assert tally.exact >= 0.97 * tally.decisions
+
+
 def test_out_of_range_token_sets_device_error():
     import torch
     _say("case: out-of-range anchor")
