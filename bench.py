@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "refined draft blocks/sec (refine+LM-head+verify), Qwen3-8B shape; % HBM/MFMA peak"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md")
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc", "xp_stream.hip")
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc", "xp_lmhead.hip")
 
 
 def log(*a):

@@ -1,16 +1,12 @@
-// Vocabulary streams: the base readout s = W_lm h (the target LM head read out
-// on the drafter states, section 4.1 / Fig. 2a) and Read + Correct
-// l = s + W_r z (eqs. read, correct), each fused with the first stage of token
-// selection so that no logit row is ever written on the fast path.
+// A1: the base readout s = W_lm h (the target LM head read out on the drafter
+// states, section 4.1 / Fig. 2a), fused with the first stage of token
+// selection so that no logit row is ever re-read for it: per vocabulary unit
+// the kernel leaves 64-bit argmax keys (greedy rows) or (max, sum exp(l - max))
+// (sampled rows) next to the fp32 rows of s that the Jacobi passes add onto.
 //
-// Both kernels stream their weight matrix exactly once per 16-position block,
-// row tile by row tile (16 vocabulary rows), straight from HBM into MFMA
-// operand registers; the 16 positions' activations stay in registers for the
-// whole kernel.  Selection partials leave the kernel per vocabulary unit:
-//   greedy rows   -> 64-bit argmax keys per workgroup (ties to the lowest index)
-//   sampled rows  -> (max, sum exp(l - max)) per unit, for the inverse-CDF pass.
+// W_lm is streamed exactly once per 16-position block; the 16 positions'
+// activations stay on chip (LDS or registers) for the whole kernel.
 #include "xp_internal.h"
-#include "xp_tiles.h"
 
 namespace xp {
 
@@ -427,134 +423,6 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
 }
 
 // ---------------------------------------------------------------------------
-// A7: l = s + W_r z, r = 256.  Every wave streams its own unit of tiles with
-// the full k range (one chain of MFMAs per tile, seeded with s); the position
-// block's z fragments sit in LDS, shared by the waves.  A unit of at most
-// kReadRes tiles (the common case) keeps all of them in registers: every W_r,
-// s and z load of the wave is issued, unconditionally, before the first
-// MFMA, so the whole unit is in flight at once (a short unit re-reads its
-// last tile, which hits in L2).  Workgroups merge their waves' argmax keys;
-// sampled rows write one (max, sum) per wave unit.
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(kReadWaves * kWave) void k_read(
-    const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int ldS, int V,
-    int M, int ntiles, int U, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
-    const uint8_t* __restrict__ temp, int B, float* __restrict__ out_logits,
-    const int32_t* __restrict__ ctrl, int skip_when_done) {
-  if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
-  constexpr int NU = ReadTile<T>::NU;
-  constexpr int NR = sizeof(T) == 2 ? 5 : 2;      // resident tiles per wave (32 / 64 VGPRs each)
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int u = blockIdx.x * kReadWaves + wave, p0 = blockIdx.y * kTile;
-  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
-  const int n = thi - tlo;
-  __shared__ u32x4 zl[NU][64];
-  __shared__ uint64_t kred[kReadWaves][kTile];
-
-  const int p = p0 + (lane & 15);
-  const bool act = p < M;
-  const int pc = act ? p : M - 1;
-  uint64_t best = kKeyMin;
-  Stat st = stat_empty();
-  bool sample = false;
-
-  auto epilogue = [&](const floatx4& acc, int t) {
-    const int row0 = t * kTile + 4 * (lane >> 4);
-    if (act) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float l = acc[i];
-        const int row = row0 + i;
-        if (row < V) {
-          if (sample)
-            st = stat_merge(st, Stat{l, 1.f});
-          else
-            best = umax64(best, argmax_key(l, (uint32_t)row));
-          if (out_logits) out_logits[(size_t)p * V + row] = l;
-        }
-      }
-    }
-  };
-  auto chain_lds = [&](const u32x4 (&a)[NU], floatx4 acc) {
-#pragma unroll
-    for (int i = 0; i < NU; ++i) acc = Mfma<T>::mma(a[i], zl[i][lane], acc);
-    return acc;
-  };
-  auto load_s = [&](int t) {
-    const floatx4 v = *reinterpret_cast<const floatx4*>(S + (size_t)pc * ldS + t * kTile + 4 * (lane >> 4));
-    return act ? v : floatx4{0.f, 0.f, 0.f, 0.f};
-  };
-  // z fragments of the position block, one 16-byte chunk per thread
-  constexpr int kZPer = (NU * 64 + kReadWaves * kWave - 1) / (kReadWaves * kWave);
-  u32x4 zv[kZPer];
-  auto load_z = [&]() {
-#pragma unroll
-    for (int j = 0; j < kZPer; ++j) {
-      const int c = threadIdx.x + kReadWaves * kWave * j;
-      const int zi = (c / 64) % NU, zlane = c % 64;
-      const int zp = p0 + (zlane & 15);
-      zv[j] = ld16(Z + (size_t)(zp < M ? zp : M - 1) * 256 + (zlane >> 4) * ReadTile<T>::EPB +
-                   zi * ReadTile<T>::KU);
-      if (zp >= M) zv[j] = u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-  auto put_z = [&]() {
-#pragma unroll
-    for (int j = 0; j < kZPer; ++j) {
-      const int c = threadIdx.x + kReadWaves * kWave * j;
-      if (c < NU * 64) zl[c / 64][c % 64] = zv[j];
-    }
-  };
-
-  if (n >= 1 && n <= NR) {
-    u32x4 a[NR][NU];
-    floatx4 c[NR];
-#pragma unroll
-    for (int j = 0; j < NR; ++j) ReadTile<T>::load_w(W, V, tlo + (j < n ? j : n - 1), lane, a[j]);
-#pragma unroll
-    for (int j = 0; j < NR; ++j) c[j] = load_s(tlo + (j < n ? j : n - 1));
-    load_z();
-    int tv = 0;
-    if (temp != nullptr) tv = temp[pc / B];
-    sample = act && tv != 0;
-    put_z();
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NR; ++j)
-      if (j < n) epilogue(chain_lds(a[j], c[j]), tlo + j);
-  } else {
-    load_z();
-    int tv = 0;
-    if (temp != nullptr) tv = temp[pc / B];
-    sample = act && tv != 0;
-    put_z();
-    __syncthreads();
-    u32x4 a[NU];
-    for (int t = tlo; t < thi; ++t) {
-      ReadTile<T>::load_w(W, V, t, lane, a);
-      epilogue(chain_lds(a, load_s(t)), t);
-    }
-  }
-#pragma unroll
-  for (int m = 16; m < 64; m <<= 1) {
-    best = umax64(best, shfl_xor_u64(best, m));
-    Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
-    st = stat_merge(st, o);
-  }
-  if (lane < 16 && sample) stats[(size_t)u * M + p] = st;
-
-  if (lane < 16) kred[wave][lane] = best;
-  __syncthreads();
-  if (threadIdx.x < kTile) {
-    uint64_t b = kKeyMin;
-    for (int w = 0; w < kReadWaves; ++w) b = umax64(b, kred[w][threadIdx.x]);
-    const int pp = p0 + threadIdx.x;
-    if (pp < M) keys[(size_t)blockIdx.x * M + pp] = b;
-  }
-}
-
-// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 // Waves per workgroup and load units per wave for a hidden width H: the k
@@ -622,24 +490,6 @@ hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t*
                          hipStream_t st) {
   if (h->dtype == XP_BF16) return launch_lmhead_t<uint16_t>(h, M, hidden, temp, st);
   return launch_lmhead_t<float>(h, M, hidden, temp, st);
-}
-
-hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
-                       float* out_logits, hipStream_t st) {
-  (void)pass;
-  const int M = batch * h->B;
-  dim3 grid(h->read_wgs, (M + kTile - 1) / kTile), block(kReadWaves * kWave);
-  const int skip = (flags & XP_EARLY_EXIT) ? 1 : 0;
-  if (h->dtype == XP_BF16)
-    hipLaunchKernelGGL((k_read<uint16_t>), grid, block, 0, st, (const uint16_t*)h->W_r,
-                       (const uint16_t*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles,
-                       h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl,
-                       skip);
-  else
-    hipLaunchKernelGGL((k_read<float>), grid, block, 0, st, (const float*)h->W_r,
-                       (const float*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles, h->read_units,
-                       h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl, skip);
-  return hipGetLastError();
 }
 
 }  // namespace xp
