@@ -58,6 +58,36 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
 // ---------------------------------------------------------------------------
+// Order a wave's LDS writes before its later LDS reads of other lanes' data.
+// A wave's LDS instructions execute in program order, so only the compiler
+// must be kept from moving the accesses across this point.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_wave_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Workgroup barrier that publishes LDS writes only.  __syncthreads() also
+// waits for every outstanding global load of the wave (the fence drains the
+// whole vector-memory counter); this one waits for the wave's LDS (and
+// scalar) operations, so loads issued earlier stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0); vmcnt, expcnt left at their maxima
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A per-sequence temperature flag, loaded unconditionally (from `dummy`, any
+// valid device address, when there are no flags): a load under a branch makes
+// the compiler wait for every load issued before it at the join.
+__device__ __forceinline__ int load_flag(const uint8_t* flags, int idx, const void* dummy) {
+  const uint8_t* p = flags != nullptr ? flags + idx : reinterpret_cast<const uint8_t*>(dummy);
+  const int v = *p;
+  return flags != nullptr ? v : 0;
+}
+
+// ---------------------------------------------------------------------------
 // Online softmax statistics (max, sum of exp(x - max)) in fp32.
 // ---------------------------------------------------------------------------
 struct Stat {

@@ -222,7 +222,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
 // results do not depend on timing, batch or position block.
 // ---------------------------------------------------------------------------
 constexpr int kSkWaves = 16;
-constexpr int kSkPF = 7;               // items in flight per wave
+constexpr int kSkPF = 5;               // items in flight per wave
 
 // XOR swizzle of the 8 16-byte chunks of a transpose-tile row: conflict-free
 // for 8 consecutive lanes writing one row and for 16 lanes reading one chunk
@@ -237,7 +237,9 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   using MF = Mfma<uint16_t>;
   __shared__ u32x4 lds[16 * kHChunks + kSkWaves * 128];   // h (128 KB) + transpose tiles (32 KB)
   u32x4* hl = lds;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the wave index is wave-uniform: make it a scalar, so that the item
+  // bookkeeping below is scalar and never masks lanes
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   u32x4* tb = lds + 16 * kHChunks + wave * 128;
   const int u = blockIdx.x, p0 = blockIdx.y * kTile;
   const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
@@ -247,6 +249,11 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   auto wlo = [&](int w) { return (int)(((long)w * N) / kSkWaves); };
   const int i0 = wlo(wave), i1 = wlo(wave + 1);
 
+  // the sampling flag of the lane's position first (its wait then covers no
+  // other load), then h, then the first items of W_lm
+  const int p_flag = p0 + (lane & 15);
+  const int tvf = load_flag(temp, (p_flag < M ? p_flag : M - 1) / B, X);
+  asm volatile("" ::: "memory");
   // h: every thread issues its (at most 8) chunk loads at once; rows past M
   // are loaded from row M-1 and zeroed
   constexpr int kHPer = 16 * kHChunks / (kSkWaves * kWave);
@@ -265,7 +272,8 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   const int li = lane & 15, g = lane >> 4;
   const int p = p0 + li;
   const bool pact = p < M;
-  bool psample = false;                                   // set once the loads are in flight
+  const bool psample = pact && tvf != 0;
+  const bool any_sample = __ballot(psample) != 0;        // wave-uniform
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
 
@@ -279,25 +287,32 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
       row = row < V ? row : V - 1;
       r[j] = ld16_nt(W + (size_t)row * H + (size_t)(8 * lq + lc) * 8);
     }
-    if (ln + 1 < i1) {
-      ++ln;
-      if (++lq == G) {
-        lq = 0;
-        ++lt;
-      }
-    }
+    const int adv = ln + 1 < i1 ? 1 : 0;                  // scalar, branch-free
+    ln += adv;
+    lq += adv;
+    const int wrap = lq == G ? 1 : 0;
+    lq = wrap ? 0 : lq;
+    lt += wrap;
   };
+  // s of one finished tile, and its selection partials without branches on
+  // the greedy path (every key is formed and kept or dropped by a select)
   auto finalize = [&](floatx4 acc, int t) {
-    if (!pact) return;
     const int row0 = t * kTile + 4 * g;
-    *reinterpret_cast<float4*>(S + (size_t)p * ldS + row0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    if (pact)
+      *reinterpret_cast<float4*>(S + (size_t)p * ldS + row0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      if (row0 + i < V) {
-        if (psample)
-          st = stat_merge(st, Stat{acc[i], 1.f});
-        else
-          best = umax64(best, argmax_key(acc[i], (uint32_t)(row0 + i)));
+      const bool v = pact && row0 + i < V && !psample;
+      const uint64_t key = umax64(best, argmax_key(acc[i], (uint32_t)(row0 + i)));
+      best = v ? key : best;
+    }
+    if (any_sample) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool v = pact && row0 + i < V && psample;
+        const Stat nx = stat_merge(st, Stat{acc[i], 1.f});
+        st.m = v ? nx.m : st.m;
+        st.s = v ? nx.s : st.s;
       }
     }
   };
@@ -308,7 +323,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   auto step = [&](const u32x4 (&r)[2], int i) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) tb[sk_slot(8 * j + ri, lc)] = r[j];
-    __builtin_amdgcn_wave_barrier();
+    wave_lds_order();
 #pragma unroll
     for (int uu = 0; uu < 2; ++uu) {
       const int c = 4 * uu + g;
@@ -317,7 +332,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
       const u32x4 b = hl[li * kHChunks + ((cc & ~15) | ((cc & 15) ^ li))];
       acc = MF::mma(a, b, acc);
     }
-    __builtin_amdgcn_wave_barrier();
+    wave_lds_order();
     if (cq == G - 1 || i == i1 - 1) {                     // end of a tile segment
       if (cq == G - 1 && ct * G >= i0)
         finalize(acc, tlo + ct);
@@ -333,26 +348,24 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
     }
   };
 
+  asm volatile("" ::: "memory");
   u32x4 ring[PF][2];
   if (i0 < i1) {
 #pragma unroll
     for (int q = 0; q < PF; ++q) load_item(ring[q]);
   }
-  {
-    int tv = 0;
-    if (temp != nullptr) tv = temp[(pact ? p : M - 1) / B];
-    psample = pact && tv != 0;
-  }
+  asm volatile("" ::: "memory");
+  // no guard on the stores (a guarded store would sink its load): chunks past
+  // 16 * nch were loaded from chunk 0 and rewrite chunk 0's slot with its value
 #pragma unroll
   for (int j = 0; j < kHPer; ++j) {
-    const int e = threadIdx.x + kSkWaves * kWave * j;
-    if (e < 16 * nch) {
-      const int pp = e / nch, c = e % nch;
-      hl[pp * kHChunks + ((c & ~15) | ((c & 15) ^ pp))] =
-          p0 + pp < M ? hv[j] : u32x4{0u, 0u, 0u, 0u};
-    }
+    int e = threadIdx.x + kSkWaves * kWave * j;
+    e = e < 16 * nch ? e : 0;
+    const int pp = e / nch, c = e % nch;
+    hl[pp * kHChunks + ((c & ~15) | ((c & 15) ^ pp))] =
+        p0 + pp < M ? hv[j] : u32x4{0u, 0u, 0u, 0u};
   }
-  __syncthreads();                                        // h is in LDS
+  lds_barrier();                                          // h is in LDS; items stay in flight
   if (i0 < i1) {
     int i = i0;
     for (; i + PF <= i1; i += PF) {

@@ -29,12 +29,15 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   constexpr int NU = ReadTile<T>::NU;
   constexpr int NR = sizeof(T) == 2 ? 5 : 2;      // resident tiles per wave (32 / 64 VGPRs each)
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int u = blockIdx.x * kReadWaves + wave, p0 = blockIdx.y * kTile;
   const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
   const int n = thi - tlo;
   __shared__ u32x4 zl[NU][64];
   __shared__ uint64_t kred[kReadWaves][kTile];
+  // per-wave transpose tile (16 rows x 32 chunks, chunk XOR-swizzled by row:
+  // conflict-free for the row-contiguous writes and the MFMA-order reads)
+  __shared__ u32x4 tbuf[sizeof(T) == 2 ? kReadWaves : 1][16 * 32];
 
   const int p = p0 + (lane & 15);
   const bool act = p < M;
@@ -43,26 +46,41 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
   Stat st = stat_empty();
   bool sample = false;
 
+  bool any_sample = false;                      // wave-uniform: some lane of the wave samples
+  // Selection partials of one tile, without branches on the greedy path: the
+  // key of every element is formed and kept or dropped by a select.
   auto epilogue = [&](const floatx4& acc, int t) {
     const int row0 = t * kTile + 4 * (lane >> 4);
-    if (act) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool v = act && row0 + i < V && !sample;
+      const uint64_t key = umax64(best, argmax_key(acc[i], (uint32_t)(row0 + i)));
+      best = v ? key : best;
+    }
+    if (any_sample) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float l = acc[i];
-        const int row = row0 + i;
-        if (row < V) {
-          if (sample)
-            st = stat_merge(st, Stat{l, 1.f});
-          else
-            best = umax64(best, argmax_key(l, (uint32_t)row));
-          if (out_logits) out_logits[(size_t)p * V + row] = l;
-        }
+        const bool v = act && row0 + i < V && sample;
+        const Stat nx = stat_merge(st, Stat{acc[i], 1.f});
+        st.m = v ? nx.m : st.m;
+        st.s = v ? nx.s : st.s;
       }
     }
+    if (out_logits) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (act && row0 + i < V) out_logits[(size_t)p * V + row0 + i] = acc[i];
+    }
+  };
+  // z fragments, read once from LDS into registers after the barrier
+  u32x4 zr[NU];
+  auto fetch_z = [&]() {
+#pragma unroll
+    for (int i = 0; i < NU; ++i) zr[i] = zl[i][lane];
   };
   auto chain_lds = [&](const u32x4 (&a)[NU], floatx4 acc) {
 #pragma unroll
-    for (int i = 0; i < NU; ++i) acc = Mfma<T>::mma(a[i], zl[i][lane], acc);
+    for (int i = 0; i < NU; ++i) acc = Mfma<T>::mma(a[i], zr[i], acc);
     return acc;
   };
   auto load_s = [&](int t) {
@@ -83,15 +101,80 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
       if (zp >= M) zv[j] = u32x4{0u, 0u, 0u, 0u};
     }
   };
-  auto put_z = [&]() {
+  static_assert(NU * 64 == kZPer * kReadWaves * kWave, "z chunks fill the workgroup exactly");
+  auto put_z = [&]() {                          // no guard: a guarded store would sink its load
 #pragma unroll
     for (int j = 0; j < kZPer; ++j) {
       const int c = threadIdx.x + kReadWaves * kWave * j;
-      if (c < NU * 64) zl[c / 64][c % 64] = zv[j];
+      zl[c / 64][c % 64] = zv[j];
     }
   };
 
-  if (n >= 1 && n <= NR) {
+  if constexpr (sizeof(T) == 2) {
+    if (n >= 1 && n <= NR) {
+      // Line-complete loads: instruction i of a tile reads its rows 2i, 2i+1
+      // (1 KB contiguous, non-temporal); each tile is then transposed through
+      // the wave's LDS tile into the MFMA operand order of ReadTile::load_w,
+      // so the chain sees exactly the operands of the rescans.
+      // Issue order = use order (z, s, then the tiles): the vector-memory
+      // counter drains in order, so tile j waits only for the loads before it.
+      u32x4 a[NR][8];
+      floatx4 c[NR];
+      const int lrow = lane >> 5, lch = lane & 31;
+      const int tv = load_flag(temp, pc / B, S);
+      load_z();
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int j = 0; j < NR; ++j) c[j] = load_s(tlo + (j < n ? j : n - 1));
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+        const int t = tlo + (j < n ? j : n - 1);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          int row = t * kTile + 2 * i + lrow;
+          row = row < V ? row : V - 1;
+          a[j][i] = ld16_nt(W + (size_t)row * 256 + lch * 8);
+        }
+      }
+      sample = act && tv != 0;
+      any_sample = __ballot(sample) != 0;
+      put_z();
+      lds_barrier();
+      fetch_z();
+      u32x4* tb = tbuf[wave];
+      const int li = lane & 15, g = lane >> 4;
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+        if (j < n) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int row = 2 * i + lrow;
+            tb[row * 32 + (lch ^ row)] = a[j][i];
+          }
+          wave_lds_order();
+          u32x4 m[NU];
+#pragma unroll
+          for (int i = 0; i < NU; ++i) m[i] = tb[li * 32 + ((4 * i + g) ^ li)];
+          wave_lds_order();
+          epilogue(chain_lds(m, c[j]), tlo + j);
+        }
+      }
+    } else {
+      load_z();
+      const int tv = load_flag(temp, pc / B, S);
+      sample = act && tv != 0;
+      any_sample = __ballot(sample) != 0;
+      put_z();
+      __syncthreads();
+      fetch_z();
+      u32x4 a[NU];
+      for (int t = tlo; t < thi; ++t) {
+        ReadTile<T>::load_w(W, V, t, lane, a);
+        epilogue(chain_lds(a, load_s(t)), t);
+      }
+    }
+  } else if (n >= 1 && n <= NR) {
     u32x4 a[NR][NU];
     floatx4 c[NR];
 #pragma unroll
@@ -99,21 +182,23 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
 #pragma unroll
     for (int j = 0; j < NR; ++j) c[j] = load_s(tlo + (j < n ? j : n - 1));
     load_z();
-    int tv = 0;
-    if (temp != nullptr) tv = temp[pc / B];
+    const int tv = load_flag(temp, pc / B, S);
     sample = act && tv != 0;
+    any_sample = __ballot(sample) != 0;
     put_z();
     __syncthreads();
+    fetch_z();
 #pragma unroll
     for (int j = 0; j < NR; ++j)
       if (j < n) epilogue(chain_lds(a[j], c[j]), tlo + j);
   } else {
     load_z();
-    int tv = 0;
-    if (temp != nullptr) tv = temp[pc / B];
+    const int tv = load_flag(temp, pc / B, S);
     sample = act && tv != 0;
+    any_sample = __ballot(sample) != 0;
     put_z();
     __syncthreads();
+    fetch_z();
     u32x4 a[NU];
     for (int t = tlo; t < thi; ++t) {
       ReadTile<T>::load_w(W, V, t, lane, a);
