@@ -116,8 +116,11 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
   const size_t es = w->dtype == XP_BF16 ? 2 : 4;
   const size_t Mmax = (size_t)max_batch * w->B;
   const size_t npairs = (size_t)w->B * (w->B - 1) / 2;
-  const size_t nk = (size_t)(h->lm_chunks > h->read_wgs ? h->lm_chunks : h->read_wgs);
-  const size_t nu = (size_t)(h->lm_chunks > h->read_units ? h->lm_chunks : h->read_units);
+  size_t nk = (size_t)(h->lm_chunks > h->read_wgs ? h->lm_chunks : h->read_wgs);
+  size_t nu = (size_t)(h->lm_chunks > h->read_units ? h->lm_chunks : h->read_units);
+  const size_t ng = (size_t)gemm_units(h, 1 << 30);     // the larger (8-tile) partition
+  nk = nk > ng ? nk : ng;
+  nu = nu > ng ? nu : ng;
   struct Slice {
     void** dst;
     size_t bytes;
@@ -287,9 +290,9 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
   h->state_valid = false;
   // All-greedy batches run the selection of pass j-1, Fuse, Mix and the first
   // Trans product of pass j as one kernel; the others use separate kernels.
-  const bool fused = K > 0 && pass_fused_ok(h, temp);
   XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, st));
   XP_TIMED(XP_STAGE_LMHEAD, launch_lmhead(h, batch * h->B, hidden, temp, st));
+  const bool fused = K > 0 && pass_fused_ok(h, temp);
   if (!fused)
     XP_TIMED(XP_STAGE_SELECT,
              launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj,

@@ -57,7 +57,8 @@ struct xp_handle {
              *L = nullptr, *W_1 = nullptr, *W_2 = nullptr, *W_r = nullptr;
   int ldS = 0, ntiles = 0;
   int cus = 0;
-  int lm_chunks = 0;           // A1 workgroups along the vocabulary (= units)
+  int lm_chunks = 0;           // A1 stream workgroups along the vocabulary (= units)
+  int lm_units_cur = 0;        // selection units of the last A1 launch (stream or GEMM)
   int read_wgs = 0;            // A7 workgroups along the vocabulary
   int read_units = 0;          // read_wgs * kReadWaves
   xp::Workspace ws;
@@ -82,6 +83,10 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
+int gemm_units(const xp_handle* h, int M);
+bool lmhead_gemm_ok(const xp_handle* h, int M);
+hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
+                              hipStream_t st);
 hipError_t launch_pass(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* seed_ids,
                        const int32_t* anchor, int32_t* out_traj, hipStream_t st);
 int prep_ksp(int H);

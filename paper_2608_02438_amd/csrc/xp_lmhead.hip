@@ -501,6 +501,11 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
 
 hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
                          hipStream_t st) {
+  if (lmhead_gemm_ok(h, M)) {                 // many positions: one GEMM instead of M/16 streams
+    h->lm_units_cur = gemm_units(h, M);
+    return launch_lmhead_gemm(h, M, hidden, temp, st);
+  }
+  h->lm_units_cur = h->lm_chunks;
   if (h->dtype == XP_BF16) return launch_lmhead_t<uint16_t>(h, M, hidden, temp, st);
   return launch_lmhead_t<float>(h, M, hidden, temp, st);
 }

@@ -188,8 +188,9 @@ __global__ __launch_bounds__(256) void k_pass(
 }
 
 // ---------------------------------------------------------------------------
+// Call after the A1 launch of the same refine (it sets the unit count).
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp) {
-  return temp == nullptr && h->dtype == XP_BF16 && h->B <= 16 && h->lm_chunks <= kPassUnits &&
+  return temp == nullptr && h->dtype == XP_BF16 && h->B <= 16 && h->lm_units_cur <= kPassUnits &&
          h->read_wgs <= kPassUnits;
 }
 
@@ -200,7 +201,7 @@ hipError_t launch_pass(xp_handle* h, int batch, int pass, uint32_t flags, const 
   int32_t* Ynew = h->ws.Y[pass % 2];
   const int32_t* Yprev = h->ws.Y[(pass + 1) % 2];
   int32_t* traj = out_traj ? out_traj + (size_t)pass * M : nullptr;
-  const int nkeys = mode == 0 ? h->lm_chunks : h->read_wgs;
+  const int nkeys = mode == 0 ? h->lm_units_cur : h->read_wgs;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   hipLaunchKernelGGL(k_pass, dim3(batch, 32), dim3(256), 0, st, mode, pass, batch, h->B, h->V, M,
                      h->ws.keys, nkeys, mode == 0 ? seed_ids : nullptr, h->ws.Pa, h->ws.T,

@@ -236,8 +236,8 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
   int32_t* Yprev = h->ws.Y[(pass + 2) % 2];      // pass j reads Y[j % 2]
   int32_t* Ynew = h->ws.Y[(pass + 1) % 2];       // and writes Y[(j+1) % 2]
   int32_t* traj = out_traj ? out_traj + (size_t)(pass + 1) * M : nullptr;
-  const int nkeys = mode == 0 ? h->lm_chunks : h->read_wgs;
-  const int U = mode == 0 ? h->lm_chunks : h->read_units;
+  const int nkeys = mode == 0 ? h->lm_units_cur : h->read_wgs;
+  const int U = mode == 0 ? h->lm_units_cur : h->read_units;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,
