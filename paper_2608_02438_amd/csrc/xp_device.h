@@ -67,6 +67,15 @@ __device__ __forceinline__ void wave_lds_order() {
   asm volatile("" ::: "memory");
 }
 
+// 16 bytes per lane from global memory straight into LDS
+// (global_load_lds_dwordx4): lane l's data lands at lds + 16 l, lds must be the
+// same for the whole wave.  The loads count in the vector-memory counter and
+// the compiler does not wait for them: the caller waits explicitly before the
+// data is read.
+__device__ __forceinline__ void lds_dma16(const void* g, u32x4* lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+
 // Workgroup barrier that publishes LDS writes only.  __syncthreads() also
 // waits for every outstanding global load of the wave (the fence drains the
 // whole vector-memory counter); this one waits for the wave's LDS (and

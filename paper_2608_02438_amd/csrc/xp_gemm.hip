@@ -29,12 +29,6 @@ __device__ __forceinline__ floatx16 mma32(u32x4 a, u32x4 b, floatx16 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane l's data lands
-// at lds + 16 l (lds must be the same for the whole wave).
-__device__ __forceinline__ void lds_dma16(const uint16_t* g, u32x4* lds) {
-  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
-}
-
 // A stage row holds 32 k (64 B = four 16-byte chunks); chunk c of row r sits in
 // slot 4 r + (c ^ swz(r)).  The swizzle makes the operand reads (32 rows, one
 // chunk) conflict-free for both 32- and 64-bank LDS grouping.
