@@ -57,6 +57,14 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 }
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
+// The base logits s are stored tile-major: the 16 rows of vocabulary tile t
+// for position p are 64 contiguous bytes at float offset 16 (t Ms + p), so a
+// tile's rows for consecutive positions are contiguous.  Ms is the position
+// count of the refine call that wrote them.
+__host__ __device__ __forceinline__ size_t s_index(int p, int row, int Ms) {
+  return ((size_t)(row >> 4) * Ms + p) * 16 + (row & 15);
+}
+
 // ---------------------------------------------------------------------------
 // Order a wave's LDS writes before its later LDS reads of other lanes' data.
 // A wave's LDS instructions execute in program order, so only the compiler

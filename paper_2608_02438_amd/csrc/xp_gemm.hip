@@ -49,7 +49,7 @@ __device__ __forceinline__ int gslot(int r, int c) { return 4 * r + (c ^ (((r >>
 template <int BN, int BM>
 __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M,
-    int ntiles, int U, int nMb, float* __restrict__ S, int ldS, uint64_t* __restrict__ keys,
+    int ntiles, int U, int nMb, float* __restrict__ S, int Ms, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B) {
   constexpr int WS = BN * kGK * 2 / 16, HS = BM * kGK * 2 / 16;  // slots per operand stage
   constexpr int NS = kGLds / (WS + HS);                          // stages (5 or 4)
@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
         const int rl = wv * 128 + a * 32 + 8 * q + 4 * lk;       // local row of acc[a][c][4q]
         const bool rv = pact && rl < nrows;                      // nrows is a multiple of 16
         if (rv)
-          *reinterpret_cast<float4*>(S + (size_t)p * ldS + r0 + rl) =
+          *reinterpret_cast<float4*>(S + s_index(p, r0 + rl, Ms)) =
               make_float4(acc[a][c][4 * q], acc[a][c][4 * q + 1], acc[a][c][4 * q + 2],
                           acc[a][c][4 * q + 3]);
         // rows past V (the last unit's padding, computed from the clamped
@@ -245,13 +245,13 @@ hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uin
     hipLaunchKernelGGL((k_lmhead_gemm<256, 256>), dim3(8 * nMb * ((U + 7) / 8)),
                        dim3(kGWaves * kWave), 0, st, (const uint16_t*)h->W_lm,
                        (const uint16_t*)hidden, h->V, h->H, M, h->ntiles, U, nMb, h->ws.s,
-                       h->ldS, h->ws.keys, h->ws.stats, temp, h->B);
+                       M, h->ws.keys, h->ws.stats, temp, h->B);
   } else {
     const int nMb = (M + 511) / 512;
     hipLaunchKernelGGL((k_lmhead_gemm<128, 512>), dim3(8 * nMb * ((U + 7) / 8)),
                        dim3(kGWaves * kWave), 0, st, (const uint16_t*)h->W_lm,
                        (const uint16_t*)hidden, h->V, h->H, M, h->ntiles, U, nMb, h->ws.s,
-                       h->ldS, h->ws.keys, h->ws.stats, temp, h->B);
+                       M, h->ws.keys, h->ws.stats, temp, h->B);
   }
   return hipGetLastError();
 }

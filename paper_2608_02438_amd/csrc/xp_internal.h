@@ -18,7 +18,7 @@ constexpr int kReadWaves = 8;   // A7: waves per workgroup, each streaming its o
 constexpr int kMaxK = 64;
 
 struct Workspace {
-  float* s = nullptr;         // [Mmax][ldS]   base logits s_k
+  float* s = nullptr;         // base logits s_k, tile-major (s_index), Mmax x ldS floats
   float* T = nullptr;         // [V][r]        token table W_e W_in[:, 2r:3r]^T
   float* Fh = nullptr;        // [r][H]        W_in[:, 0:r] W_h
   float* Fg = nullptr;        // [r][H]        W_in[:, r:2r] W_g

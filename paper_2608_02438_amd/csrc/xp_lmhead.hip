@@ -20,7 +20,7 @@ namespace xp {
 template <typename T, int NU>
 __global__ __launch_bounds__(1024) void k_lmhead(
     const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
-    float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B) {
   using MF = Mfma<T>;
   constexpr int EPB = 16 / sizeof(T);
@@ -68,7 +68,7 @@ __global__ __launch_bounds__(1024) void k_lmhead(
       for (int w = 0; w < NW; ++w) v += red[w][epos][erow];
       const int row = t * kTile + erow;
       if (eact && row < V) {
-        S[(size_t)ep * ldS + row] = v;
+        S[s_index(ep, row, Ms)] = v;
         if (esample)
           st = stat_merge(st, Stat{v, 1.f});
         else
@@ -105,7 +105,7 @@ constexpr int kHChunks = 512;          // 16-byte chunks of h per position (8 KB
 template <typename T, int NU>
 __global__ __launch_bounds__(1024) void k_lmhead_lds(
     const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
-    float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B) {
   using MF = Mfma<T>;
   constexpr int EPB = 16 / sizeof(T);
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
       for (int w = 0; w < NW; ++w) v += red[buf][w][src][comp];
       const int row = t * kTile + erow;
       if (eact && row < V) {
-        S[(size_t)ep * ldS + row] = v;
+        S[s_index(ep, row, Ms)] = v;
         if (esample)
           st = stat_merge(st, Stat{v, 1.f});
         else
@@ -232,7 +232,7 @@ __device__ __forceinline__ int sk_slot(int row, int c) { return row * 8 + (c ^ (
 template <int PF>
 __global__ __launch_bounds__(1024) void k_lmhead_sk(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M, int ntiles,
-    int U, float* __restrict__ S, int ldS, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
+    int U, float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B) {
   using MF = Mfma<uint16_t>;
   __shared__ u32x4 lds[16 * kHChunks + kSkWaves * 128];   // h (128 KB) + transpose tiles (32 KB)
@@ -299,7 +299,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   auto finalize = [&](floatx4 acc, int t) {
     const int row0 = t * kTile + 4 * g;
     if (pact)
-      *reinterpret_cast<float4*>(S + (size_t)p * ldS + row0) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      *reinterpret_cast<float4*>(S + s_index(p, row0, Ms)) = make_float4(acc[0], acc[1], acc[2], acc[3]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const bool v = pact && row0 + i < V && !psample;
@@ -469,14 +469,14 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
     if (lds) {
       hipLaunchKernelGGL((k_lmhead_sk<kSkPF>), grid, dim3(kSkWaves * kWave), 0, st,
                          (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
-                         h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
+                         h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
                          h->B);
       return hipGetLastError();
     }
   }
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, 0, st, (const T*)h->W_lm, (const T*)hidden, h->V, h->H,
-                       M, h->ntiles, h->lm_chunks, h->ws.s, h->ldS, h->ws.keys, h->ws.stats, temp,
+                       M, h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
                        h->B);
   };
   if (lds) {

@@ -22,7 +22,7 @@ namespace xp {
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
-    const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int ldS, int V,
+    const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int Ms, int V,
     int M, int ntiles, int U, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B, float* __restrict__ out_logits,
     const int32_t* __restrict__ ctrl, int skip_when_done) {
@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
     return acc;
   };
   auto load_s = [&](int t) {
-    const floatx4 v = *reinterpret_cast<const floatx4*>(S + (size_t)pc * ldS + t * kTile + 4 * (lane >> 4));
+    const floatx4 v = *reinterpret_cast<const floatx4*>(S + s_index(pc, t * kTile + 4 * (lane >> 4), Ms));
     return act ? v : floatx4{0.f, 0.f, 0.f, 0.f};
   };
   // z fragments of the position block, one 16-byte chunk per thread
@@ -229,75 +229,86 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
 // (8 wave units) for 128 P positions: each wave keeps the z fragments of its
 // 16 P positions in registers and runs through all the workgroup's tiles, so
 // W_r is read once per 128 P positions and the pass is bound by reading s.
-// W_r tiles pass through a ring of LDS slots (one 1 KB global-to-LDS load per
-// wave and tile, shared by the 8 waves); the s operands of a tile are loaded
-// into registers two tiles ahead.  Each (tile, 16 positions) product is the
-// chain of matrix operations seeded with s used by the stream kernel and the
-// sampling rescan (ReadTile), so all of them produce the same fp32 logits.
-// Outputs have the stream kernel's layout: one key row per workgroup, one
-// (max, sum) per wave unit and position.
-constexpr int kRmSlots = 3;
+// The W_r tile and the s operands of every tile go through a ring of LDS
+// stages filled by global-to-LDS loads three tiles ahead (each wave loads one
+// 1 KB part of the W_r tile and the s of its own positions), so up to 100 KB
+// per CU is in flight without staging registers.  Each (tile, 16 positions)
+// product is the chain of matrix operations seeded with s used by the stream
+// kernel and the sampling rescan (ReadTile), so all of them produce the same
+// fp32 logits.  Outputs have the stream kernel's layout: one key row per
+// workgroup, one (max, sum) per wave unit and position.
+constexpr int kRmStages = 4;
 
-// A W_r tile in LDS: 16 rows x 32 chunks of 16 bytes, chunk c of row r at
-// slot 32 r + (c ^ r): the fragment reads (16 rows, one chunk) hit 16
-// different bank groups.
-__device__ __forceinline__ int rm_slot(int r, int c) { return 32 * r + (c ^ r); }
+// W_r tile in LDS: 16 rows x 32 chunks of 16 bytes, chunk c of row r at slot
+// 32 r + (c ^ r); s of 16 positions x 16 rows: chunk c (4 rows) of position q
+// at slot 4 q + (c ^ (q / 4)).  The fragment reads (16 rows or positions, one
+// chunk) then hit 16 different bank groups.
+__device__ __forceinline__ int rm_wslot(int r, int c) { return 32 * r + (c ^ r); }
+__device__ __forceinline__ int rm_sslot(int q, int c) { return 4 * q + ((c ^ (q >> 2)) & 3); }
 
 template <int P>
 __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ Z, const float* __restrict__ S,
-    int ldS, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
+    int Ms, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B,
     float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done) {
   static_assert(kReadWaves == 8, "one 1 KB load per wave fills a 16-row tile");
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   using RT = ReadTile<uint16_t>;
   constexpr int NU = RT::NU;
+  constexpr int WSL = 512, SSL = kReadWaves * P * 64;          // 16-byte slots per stage
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = blockIdx.x, u_lo = g * kReadWaves, u_hi = u_lo + kReadWaves;
   const int t0 = unit_tile_lo(u_lo, ntiles, U), n = unit_tile_lo(u_hi, ntiles, U) - t0;
   const int pw = blockIdx.y * (kReadWaves * kTile * P) + wave * (kTile * P);
-  __shared__ u32x4 wt[kRmSlots][512];
+  __shared__ u32x4 lds[kRmStages * (WSL + SSL)];                // [stage][W tile | s]
 
   u32x4 zf[P][NU];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) RT::load_z(Z, M, pw + kTile * pb, lane, zf[pb]);
-  int pc[P];
   bool act[P], sample[P];
   bool any = false;
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
     const int p = pw + kTile * pb + (lane & 15);
     act[pb] = p < M;
-    pc[pb] = act[pb] ? p : M - 1;
-    sample[pb] = act[pb] && load_flag(temp, pc[pb] / B, S) != 0;
+    sample[pb] = act[pb] && load_flag(temp, (act[pb] ? p : M - 1) / B, S) != 0;
     any = any || sample[pb];
   }
   const bool any_sample = __ballot(any) != 0;    // wave-uniform
-  uint64_t best[P];
+  // greedy rows: running maximum and its row (rows arrive in increasing order
+  // in every lane, so a strict comparison keeps the lowest index of a tie;
+  // -0 == +0 as in the key order)
+  float bv[P];
+  uint32_t bi[P];
   Stat st[P];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
-    best[pb] = kKeyMin;
+    bv[pb] = -INFINITY;
+    bi[pb] = 0xFFFFFFFFu;
     st[pb] = stat_empty();
   }
 
-  // loads of the workgroup's tile j (clamped into the range, so that every
-  // wave issues the same number of loads per tile): this wave's 1 KB of the
-  // W_r tile into slot j % kRmSlots, and the s operands of its positions
-  const int srow = (kWave * wave + lane) >> 5;
-  const int schunk = ((kWave * wave + lane) & 31) ^ srow;
-  auto issue = [&](int j, floatx4 (&c)[P]) {
-    const int t = t0 + (j < n ? j : n - 1);
-    int row = t * kTile + srow;
-    row = row < V ? row : V - 1;
-    lds_dma16(W + (size_t)row * 256 + 8 * schunk, &wt[j % kRmSlots][kWave * wave]);
+  // loads of tile j (clamped into the range, so that every wave issues the
+  // same number of loads per tile) into stage j % kRmStages
+  const int wrow = (kWave * wave + lane) >> 5;
+  const int wchunk = ((kWave * wave + lane) & 31) ^ wrow;
+  const int sq = lane >> 2, sc = (lane & 3) ^ ((sq >> 2) & 3);
+  const float* sbase[P];
 #pragma unroll
-    for (int pb = 0; pb < P; ++pb) {
-      const floatx4 v = *reinterpret_cast<const floatx4*>(S + (size_t)pc[pb] * ldS + t * kTile +
-                                                          4 * (lane >> 4));
-      c[pb] = act[pb] ? v : floatx4{0.f, 0.f, 0.f, 0.f};
-    }
+  for (int pb = 0; pb < P; ++pb) {
+    const int p = pw + kTile * pb + sq;
+    sbase[pb] = S + s_index(p < M ? p : M - 1, 4 * sc, Ms);
+  }
+  auto issue = [&](int j) {
+    const int t = t0 + (j < n ? j : n - 1);
+    int row = t * kTile + wrow;
+    row = row < V ? row : V - 1;
+    u32x4* stage = lds + (j % kRmStages) * (WSL + SSL);
+    lds_dma16(W + (size_t)row * 256 + 8 * wchunk, stage + kWave * wave);
+#pragma unroll
+    for (int pb = 0; pb < P; ++pb)
+      lds_dma16(sbase[pb] + (size_t)t * Ms * kTile, stage + WSL + kWave * (P * wave + pb));
   };
   // (max, sum) of every unit that ends at or before tile boundary tend
   int uc = u_lo, ue = unit_tile_lo(u_lo + 1, ntiles, U);
@@ -312,7 +323,8 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
             const Stat o{__shfl_xor(q.m, m, kWave), __shfl_xor(q.s, m, kWave)};
             q = stat_merge(q, o);
           }
-          if (lane < 16 && sample[pb]) stats[(size_t)uc * M + pc[pb]] = q;
+          const int p = pw + kTile * pb + (lane & 15);
+          if (lane < 16 && sample[pb]) stats[(size_t)uc * M + p] = q;
           st[pb] = stat_empty();
         }
       }
@@ -320,30 +332,42 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
       ue = unit_tile_lo(uc + 1, ntiles, U);
     }
   };
-  constexpr int kPend = 1 + P;                    // loads of one tile
+
+  flush_until(t0);                                // units without tiles
+#pragma unroll
+  for (int j = 0; j < kRmStages - 1; ++j) issue(j);
+  constexpr int kPend = (kRmStages - 2) * (1 + P); // loads of the two later tiles
   static_assert(kPend < 16, "vmcnt field");
-  auto step = [&](int j, floatx4 (&c)[P]) {
-    // tile j's loads are done once only the next tile's are outstanding; the
-    // barrier then covers every wave's part of the W_r tile, and every wave's
-    // reads of the slot that the next issue overwrites
+  for (int j = 0; j < n; ++j) {
+    // tile j's loads are done once only the two later tiles' are outstanding;
+    // the barrier then covers every wave's part of stage j, and every wave's
+    // reads of the stage that the next issue overwrites (tile j - 1)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0x0070 | kPend);
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    const int t = t0 + j;
+    issue(j + kRmStages - 1);
+    const u32x4* stage = lds + (j % kRmStages) * (WSL + SSL);
     u32x4 a[NU];
-    const u32x4* slot = wt[j % kRmSlots];
 #pragma unroll
-    for (int i = 0; i < NU; ++i) a[i] = slot[rm_slot(lane & 15, (lane >> 4) + 4 * i)];
+    for (int i = 0; i < NU; ++i) a[i] = stage[rm_wslot(lane & 15, (lane >> 4) + 4 * i)];
+    floatx4 c[P];
+#pragma unroll
+    for (int pb = 0; pb < P; ++pb)
+      c[pb] = __builtin_bit_cast(floatx4, stage[WSL + kWave * (P * wave + pb) +
+                                               rm_sslot(lane & 15, lane >> 4)]);
+    const int t = t0 + j;
     const int row0 = t * kTile + 4 * (lane >> 4);
+    const bool last = (t + 1) * kTile > V;         // wave-uniform: rows past V in this tile
 #pragma unroll
     for (int pb = 0; pb < P; ++pb) {
       const floatx4 acc = RT::chain(a, zf[pb], c[pb]);
+      const bool gv = act[pb] && !sample[pb];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bool v = act[pb] && row0 + i < V && !sample[pb];
-        const uint64_t key = umax64(best[pb], argmax_key(acc[i], (uint32_t)(row0 + i)));
-        best[pb] = v ? key : best[pb];
+        const bool take = gv && (!last || row0 + i < V) && acc[i] > bv[pb];
+        bv[pb] = take ? acc[i] : bv[pb];
+        bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
       }
       if (any_sample) {
 #pragma unroll
@@ -355,29 +379,22 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
         }
       }
       if (out_logits) {
+        const int p = pw + kTile * pb + (lane & 15);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (act[pb] && row0 + i < V) out_logits[(size_t)pc[pb] * V + row0 + i] = acc[i];
+          if (act[pb] && row0 + i < V) out_logits[(size_t)p * V + row0 + i] = acc[i];
       }
     }
     flush_until(t + 1);
-    issue(j + 2, c);
-  };
-
-  flush_until(t0);                                // units without tiles
-  floatx4 cA[P], cB[P];
-  issue(0, cA);
-  issue(1, cB);
-  for (int j = 0; j < n; j += 2) {                // n is the same for every wave
-    step(j, cA);
-    if (j + 1 < n) step(j + 1, cB);
   }
   __builtin_amdgcn_s_waitcnt(0x0070);             // the clamped loads past the end
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
+    uint64_t best = bi[pb] == 0xFFFFFFFFu ? kKeyMin : argmax_key(bv[pb], bi[pb]);
 #pragma unroll
-    for (int m = 16; m < 64; m <<= 1) best[pb] = umax64(best[pb], shfl_xor_u64(best[pb], m));
-    if (lane < 16 && act[pb]) keys[(size_t)g * M + pc[pb]] = best[pb];
+    for (int m = 16; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
+    const int p = pw + kTile * pb + (lane & 15);
+    if (lane < 16 && act[pb]) keys[(size_t)g * M + p] = best;
   }
 }
 
@@ -397,22 +414,22 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     const uint16_t* Zb = (const uint16_t*)h->ws.z;
     switch (P) {
       case 1:
-        hipLaunchKernelGGL((k_read_multi<1>), grid, block, 0, st, Wr, Zb, h->ws.s, h->ldS, h->V,
+        hipLaunchKernelGGL((k_read_multi<1>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
                            out_logits, h->ws.ctrl, skip);
         break;
       case 2:
-        hipLaunchKernelGGL((k_read_multi<2>), grid, block, 0, st, Wr, Zb, h->ws.s, h->ldS, h->V,
+        hipLaunchKernelGGL((k_read_multi<2>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
                            out_logits, h->ws.ctrl, skip);
         break;
       case 3:
-        hipLaunchKernelGGL((k_read_multi<3>), grid, block, 0, st, Wr, Zb, h->ws.s, h->ldS, h->V,
+        hipLaunchKernelGGL((k_read_multi<3>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
                            out_logits, h->ws.ctrl, skip);
         break;
       default:
-        hipLaunchKernelGGL((k_read_multi<4>), grid, block, 0, st, Wr, Zb, h->ws.s, h->ldS, h->V,
+        hipLaunchKernelGGL((k_read_multi<4>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
                            out_logits, h->ws.ctrl, skip);
     }
@@ -420,12 +437,12 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
   }
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_read<uint16_t>), grid, block, 0, st, (const uint16_t*)h->W_r,
-                       (const uint16_t*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles,
+                       (const uint16_t*)h->ws.z, h->ws.s, M, h->V, M, h->ntiles,
                        h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl,
                        skip);
   else
     hipLaunchKernelGGL((k_read<float>), grid, block, 0, st, (const float*)h->W_r,
-                       (const float*)h->ws.z, h->ws.s, h->ldS, h->V, M, h->ntiles, h->read_units,
+                       (const float*)h->ws.z, h->ws.s, M, h->V, M, h->ntiles, h->read_units,
                        h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl, skip);
   return hipGetLastError();
 }

@@ -41,7 +41,7 @@ __device__ __forceinline__ double unit_mass(const Stat* __restrict__ stats, int 
 // Inverse-CDF selection for position p (one wave).  mode 0 reads l = s from
 // memory, mode 1 recomputes l = s + W_r z for the crossing unit.
 template <typename T>
-__device__ int sample_position(int mode, int p, float u, const float* __restrict__ S, int ldS,
+__device__ int sample_position(int mode, int p, float u, const float* __restrict__ S, int Ms,
                                const T* __restrict__ W_r, const T* __restrict__ Z, int M, int V,
                                const Stat* __restrict__ stats, int ntiles, int U, double* lse_out,
                                bool pick) {
@@ -91,7 +91,7 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
     const int row = base + lane;
     float l = 0.f;
     if (mode == 0) {
-      if (row < rhi) l = S[(size_t)p * ldS + row];
+      if (row < rhi) l = S[s_index(p, row, Ms)];
     } else {
       // four 16-row tiles cover these 64 rows; lane (r/4)*16 + p%16 holds row r
       constexpr int NU = ReadTile<T>::NU;
@@ -104,7 +104,7 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
         const int t = (base - rlo) / kTile + tlo + tt;
         if (t >= thi) break;                         // wave-uniform
         ReadTile<T>::load_w(W_r, V, t, lane, a);
-        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, pl, pl < M, t, lane));
+        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, pl, pl < M, t, lane));
         const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
         const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
         const float v = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
@@ -138,7 +138,7 @@ constexpr int kSelPPW = 32 / kSelWaves;         // positions per wave (B <= 32)
 
 template <typename T>
 __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
-    int mode, int pass, int batch, int B, int V, int M, const float* __restrict__ S, int ldS,
+    int mode, int pass, int batch, int B, int V, int M, const float* __restrict__ S, int Ms,
     const T* __restrict__ W_r, const T* __restrict__ Z, const uint64_t* __restrict__ keys,
     int nkeys, const Stat* __restrict__ stats, int ntiles, int U,
     const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
         y = 0;
       }
       if (sample)
-        sample_position<T>(0, p, 0.f, S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p, false);
+        sample_position<T>(0, p, 0.f, S, Ms, W_r, Z, M, V, stats, ntiles, U, lse + p, false);
     } else if (!sample) {
       uint64_t best = kv[m][0];
 #pragma unroll
@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
       for (int o = 1; o < 64; o <<= 1) best = umax64(best, shfl_xor_u64(best, o));
       y = (int)key_index(best);
     } else {
-      y = sample_position<T>(mode, p, u_draft[p], S, ldS, W_r, Z, M, V, stats, ntiles, U, lse + p,
+      y = sample_position<T>(mode, p, u_draft[p], S, Ms, W_r, Z, M, V, stats, ntiles, U, lse + p,
                              true);
     }
     if (lane == 0) {
@@ -216,13 +216,13 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
   }
 }
 
-__global__ void k_copy_logits(int M, int V, const float* __restrict__ S, int ldS,
+__global__ void k_copy_logits(int M, int V, const float* __restrict__ S,
                               float* __restrict__ out) {
   const size_t n = (size_t)M * V;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x) {
     const size_t p = i / V, v = i % V;
-    out[i] = S[p * ldS + v];
+    out[i] = S[s_index((int)p, (int)v, M)];
   }
 }
 
@@ -241,14 +241,14 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,
-                       h->B, h->V, M, h->ws.s, h->ldS, (const uint16_t*)h->W_r,
+                       h->B, h->V, M, h->ws.s, M, (const uint16_t*)h->W_r,
                        (const uint16_t*)h->ws.z, h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
                        h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early, out_ids, out_iters,
                        K);
   else
     hipLaunchKernelGGL((k_select<float>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch, h->B,
-                       h->V, M, h->ws.s, h->ldS, (const float*)h->W_r, (const float*)h->ws.z,
+                       h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
                        h->ws.keys, nkeys, h->ws.stats, h->ntiles, U,
                        mode == 0 ? seed_ids : nullptr, temp, u_draft, Yprev, Ynew, traj,
                        h->ws.lse, h->ws.iters, h->ws.ctrl, h->ws.err, early, out_ids, out_iters,
@@ -262,7 +262,7 @@ hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t
   (void)out_iters;
   const int M = batch * h->B;
   if (K == 0 && (flags & XP_WRITE_LOGITS) && out_logits)
-    hipLaunchKernelGGL(k_copy_logits, dim3(1024), dim3(256), 0, st, M, h->V, h->ws.s, h->ldS,
+    hipLaunchKernelGGL(k_copy_logits, dim3(1024), dim3(256), 0, st, M, h->V, h->ws.s,
                        out_logits);
   return hipGetLastError();
 }

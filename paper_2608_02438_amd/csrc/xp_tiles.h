@@ -43,10 +43,10 @@ struct ReadTile {
   }
   // s operand: the base logits of the lane's four output rows (the MFMA
   // accumulator starts from them, so the chain yields l = s + W_r z directly).
-  __device__ static __forceinline__ floatx4 load_s(const float* __restrict__ S, int ldS, int p,
+  __device__ static __forceinline__ floatx4 load_s(const float* __restrict__ S, int Ms, int p,
                                                    bool valid, int tile, int lane) {
     if (!valid) return floatx4{0.f, 0.f, 0.f, 0.f};
-    return *reinterpret_cast<const floatx4*>(S + (size_t)p * ldS + tile * 16 + 4 * (lane >> 4));
+    return *reinterpret_cast<const floatx4*>(S + s_index(p, tile * 16 + 4 * (lane >> 4), Ms));
   }
   // acc[i] of lane l = init[i] + sum_k W_r[16*tile + 4*(l/16) + i][k] * z[position l%16][k]
   __device__ static __forceinline__ floatx4 chain(const u32x4 (&a)[NU], const u32x4 (&bf)[NU],

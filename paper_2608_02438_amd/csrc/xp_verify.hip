@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) void k_vtarget(const float* __restrict__ tl, i
 // l = s (+ W_r z) for position p at vocabulary row v, through the Read tile of
 // the stream (all 64 lanes take part; every lane gets the value).
 template <typename T>
-__device__ float refined_logit(int with_read, const float* __restrict__ S, int ldS,
+__device__ float refined_logit(int with_read, const float* __restrict__ S, int Ms,
                                const T* __restrict__ W_r, const T* __restrict__ Z, int M, int V,
                                int p, int v) {
   const int lane = threadIdx.x & 63;
@@ -57,14 +57,14 @@ __device__ float refined_logit(int with_read, const float* __restrict__ S, int l
     ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
     ReadTile<T>::load_w(W_r, V, v / 16, lane, a);
     const floatx4 acc =
-        ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, pl, pl < M, v / 16, lane));
+        ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, pl, pl < M, v / 16, lane));
     const int rr = v & 15, src = (rr >> 2) * 16 + (p & 15);
     const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
     const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
     const int comp = rr & 3;
     d = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
   }
-  return with_read ? d : S[(size_t)p * ldS + v];
+  return with_read ? d : S[s_index(p, v, Ms)];
 }
 
 // One wave per sequence: accept scan.  vpos[b] = rejected position, or B.
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(64) void k_vaccept(
     int B, int V, int M, int with_read, const int32_t* __restrict__ draft,
     const uint8_t* __restrict__ temp, const int32_t* __restrict__ tids,
     const float* __restrict__ tl, const float* __restrict__ racc, const float* __restrict__ S,
-    int ldS, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
+    int Ms, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
     const double* __restrict__ lseT, int32_t* __restrict__ vpos, int32_t* __restrict__ out_n,
     int32_t* __restrict__ out_next, uint32_t* __restrict__ err) {
   const int b = blockIdx.x, lane = threadIdx.x;
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(64) void k_vaccept(
       bad = 1;
       y = 0;
     }
-    const float l = refined_logit<T>(with_read, S, ldS, W_r, Z, M, V, p, y);
+    const float l = refined_logit<T>(with_read, S, Ms, W_r, Z, M, V, p, y);
     const double q = exp((double)l - lse[p]);
     const double pt =
         exp((double)tl[((size_t)b * (B + 1) + k) * V + y] - lseT[(size_t)b * (B + 1) + k]);
@@ -144,7 +144,7 @@ template <typename T>
 __global__ __launch_bounds__(1024) void k_vresid(
     int batch, int B, int V, int M, int with_read, int ntiles, int U,
     const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
-    const float* __restrict__ tl, const float* __restrict__ S, int ldS, const T* __restrict__ W_r,
+    const float* __restrict__ tl, const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
     const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
     double* __restrict__ vmass) {
   constexpr int NU = ReadTile<T>::NU;
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(1024) void k_vresid(
   const double lp = resid ? lse[p] : 0.0;
   double mr = 0.0, mp = 0.0;
   for (int t = tlo; t < thi; ++t) {
-    floatx4 acc = ReadTile<T>::load_s(S, ldS, p, resid, t, lane);
+    floatx4 acc = ReadTile<T>::load_s(S, Ms, p, resid, t, lane);
     if (with_read) {
       ReadTile<T>::load_w(W_r, V, t, lane, a);
       acc = ReadTile<T>::chain(a, bf, acc);
@@ -207,7 +207,7 @@ template <typename T>
 __global__ __launch_bounds__(64) void k_vfinal(
     int batch, int B, int V, int M, int with_read, int ntiles, int U,
     const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
-    const float* __restrict__ tl, const float* __restrict__ S, int ldS, const T* __restrict__ W_r,
+    const float* __restrict__ tl, const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
     const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
     const double* __restrict__ vmass, const float* __restrict__ u_res,
     int32_t* __restrict__ out_next) {
@@ -272,14 +272,14 @@ __global__ __launch_bounds__(64) void k_vfinal(
         const int t = (base - rlo) / kTile + tlo + tt;
         if (t >= thi) break;
         ReadTile<T>::load_w(W_r, V, t, lane, a);
-        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, ldS, p, true, t, lane));
+        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, p, true, t, lane));
         const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
         const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
         const float v = cp == 0 ? c0 : cp == 1 ? c1 : cp == 2 ? c2 : c3;
         if ((lane >> 4) == tt) mine = v;
       }
     }
-    if (resid && !with_read && row < rhi) mine = S[(size_t)p * ldS + row];   // K = 0: l = s
+    if (resid && !with_read && row < rhi) mine = S[s_index(p, row, Ms)];   // K = 0: l = s
     double w = 0.0;
     if (row < rhi) {
       const float l = resid ? mine : 0.f;
@@ -312,17 +312,17 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
     hipLaunchKernelGGL(k_vtarget, dim3(h->B + 1, batch), dim3(256), 0, st, tl, h->B, h->V, temp,
                        h->ws.vstat);
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
-                     draft, temp, tids, tl, racc, h->ws.s, h->ldS, (const T*)h->W_r,
+                     draft, temp, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
                      (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
                      h->ws.err);
   if (temp) {
     hipLaunchKernelGGL((k_vresid<T>), dim3(h->read_wgs, (batch + 15) / 16),
                        dim3(kReadWaves * kWave), 0, st, batch, h->B, h->V, M, with_read,
-                       h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s, h->ldS,
+                       h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s, M,
                        (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vmass);
     hipLaunchKernelGGL((k_vfinal<T>), dim3(batch), dim3(64), 0, st, batch, h->B, h->V, M,
                        with_read, h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s,
-                       h->ldS, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
+                       M, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
                        h->ws.vmass, ures, out_next);
   }
   return hipGetLastError();
