@@ -148,6 +148,8 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
       {(void**)&ws.vstat, (size_t)max_batch * (w->B + 1) * 8},
       {(void**)&ws.vpos, (size_t)max_batch * 4},
       {(void**)&ws.vmass, (size_t)h->read_units * max_batch * 16},
+      {(void**)&ws.vpart,
+       (size_t)max_batch * (w->B + 1) * ((w->V + kVChunk - 1) / kVChunk) * 16},
   };
   size_t total = 0;
   for (auto& s : sl) total += align_up(s.bytes, 256);

@@ -39,7 +39,11 @@ struct Workspace {
   double* vstat = nullptr;    // [max_batch][B+1][2] target (max, log-sum-exp) per row
   int32_t* vpos = nullptr;    // [max_batch][2] rejected position (or B), state
   double* vmass = nullptr;    // [max units][max_batch] residual / bonus mass per unit
+  double* vpart = nullptr;    // [max_batch][B+1][vchunks][2] target row (max, sum) per chunk
 };
+
+// Target rows are reduced in chunks of kVChunk entries (16 per thread).
+constexpr int kVChunk = 4096;
 
 }  // namespace xp
 

@@ -3,10 +3,13 @@
 //
 // Greedy rows: the maximum 64-bit key over the stream's workgroups gives
 // argmax_v l_v with ties to the lowest index.
-// Sampled rows (temperature 1): y = min{v : sum_{w<=v} e^{l_w - m} > u Z}.
-//   1. m = max over units, Z = in-order fp64 scan of the unit masses
-//      sum_u e^{max_u - m};
-//   2. the same scan again finds the unit whose inclusive prefix exceeds u Z;
+// Sampled rows (temperature 1): y = min{v : sum_{w<=v} e^{l_w - m} > u Z},
+// one workgroup per position (k_sample):
+//   1. m = max over units; the unit masses sum_u e^{max_u - m} are summed in
+//      fp64, each wave over a contiguous range of units (in-order wave
+//      scans), then the wave totals in wave order: Z;
+//   2. the first wave whose running total exceeds u Z redoes its scans (same
+//      arithmetic) to find the crossing unit;
 //   3. that unit's rows are recomputed with the stream's own MFMA tile code
 //      (same fp32 logits) and scanned in vocabulary order in fp64.
 // The log-sum-exp m + log Z of the chosen pass is kept for verification.
@@ -38,51 +41,15 @@ __device__ __forceinline__ double unit_mass(const Stat* __restrict__ stats, int 
   return s.s > 0.f ? (double)s.s * exp((double)s.m - (double)m) : 0.0;
 }
 
-// Inverse-CDF selection for position p (one wave).  mode 0 reads l = s from
-// memory, mode 1 recomputes l = s + W_r z for the crossing unit.
+// Rows of unit ustar for position p, scanned in vocabulary order from the
+// cumulative mass `pre` of the units before it, until the cumulative mass
+// exceeds `target` (one wave; every lane returns the row).  mode 0 reads
+// l = s, mode 1 recomputes l = s + W_r z with the stream's tile code.
 template <typename T>
-__device__ int sample_position(int mode, int p, float u, const float* __restrict__ S, int Ms,
-                               const T* __restrict__ W_r, const T* __restrict__ Z, int M, int V,
-                               const Stat* __restrict__ stats, int ntiles, int U, double* lse_out,
-                               bool pick) {
+__device__ int rescan_unit(int mode, int p, int ustar, double pre, double target, float m,
+                           const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
+                           const T* __restrict__ Z, int M, int V, int ntiles, int U) {
   const int lane = threadIdx.x & 63;
-  float m = -INFINITY;
-  for (int i = lane; i < U; i += 64) {
-    const Stat s = stats[(size_t)i * M + p];
-    if (s.s > 0.f) m = fmaxf(m, s.m);
-  }
-  m = wave_max(m);
-  double carry = 0.0;
-  for (int base = 0; base < U; base += 64) {
-    const double incl = wave_incl_scan(unit_mass(stats, base + lane, U, M, p, m), lane);
-    carry += __shfl(incl, 63, kWave);
-  }
-  const double Zs = carry;
-  if (lane == 0 && lse_out) *lse_out = (double)m + log(Zs);
-  if (!pick) return 0;
-  const double target = (double)u * Zs;
-
-  // crossing unit: first i with (carry + incl_i) > target, same arithmetic as Zs
-  carry = 0.0;
-  int ustar = U - 1;
-  double pre = 0.0;                       // mass of units before ustar
-  for (int base = 0; base < U; base += 64) {
-    const double incl = wave_incl_scan(unit_mass(stats, base + lane, U, M, p, m), lane);
-    const double tot = carry + incl;
-    const unsigned long long hit = __ballot(base + lane < U && tot > target);
-    if (hit) {
-      const int first = __ffsll((long long)hit) - 1;
-      const double prev = __shfl_up(tot, 1, kWave);
-      const double excl = (lane == 0) ? carry : prev;
-      ustar = base + first;
-      pre = __shfl(excl, first, kWave);
-      break;
-    }
-    carry += __shfl(incl, 63, kWave);
-    pre = carry;
-  }
-
-  // rescan the unit's rows in vocabulary order
   const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
   const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
   int chosen = -1, last_pos = -1;
@@ -125,6 +92,100 @@ __device__ int sample_position(int mode, int p, float u, const float* __restrict
   }
   if (chosen < 0) chosen = last_pos >= 0 ? last_pos : rlo;   // rounding left no crossing
   return chosen;
+}
+
+// Inverse-CDF selection at temperature 1, one workgroup per position (rows at
+// temperature 0, and every row of a batch that is at its fixed point, return
+// at once).  mode 0: the seed Y^(0) from the base logits (with caller seeds
+// only the log-sum-exp is kept); mode 1: the selection of a Jacobi pass.  The
+// chosen row goes to Ynew, where the selection kernel that follows picks it up.
+constexpr int kSmpWaves = 8;
+
+template <typename T>
+__global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
+    int mode, int B, int V, int M, const float* __restrict__ S, int Ms,
+    const T* __restrict__ W_r, const T* __restrict__ Z, const Stat* __restrict__ stats,
+    int ntiles, int U, const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
+    const float* __restrict__ u_draft, int32_t* __restrict__ Ynew, double* __restrict__ lse,
+    const int32_t* __restrict__ ctrl, int early_exit) {
+  const int p = blockIdx.x;
+  if (temp[p / B] == 0) return;
+  if (mode == 1 && early_exit && ctrl[1] != 0) return;     // the selection keeps Y^(j)
+  const bool pick = !(mode == 0 && seed_ids != nullptr);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ float wmax[kSmpWaves];
+  __shared__ double wtot[kSmpWaves];
+
+  float m = -INFINITY;
+  for (int i = threadIdx.x; i < U; i += kSmpWaves * kWave) {
+    const Stat q = stats[(size_t)i * M + p];
+    if (q.s > 0.f) m = fmaxf(m, q.m);
+  }
+  m = wave_max(m);
+  if (lane == 0) wmax[wave] = m;
+  __syncthreads();
+  m = wmax[0];
+#pragma unroll
+  for (int w = 1; w < kSmpWaves; ++w) m = fmaxf(m, wmax[w]);
+
+  // wave w sums the units [ua, ub) in order
+  const int ua = (int)((int64_t)U * wave / kSmpWaves), ub = (int)((int64_t)U * (wave + 1) / kSmpWaves);
+  auto mass = [&](int i) { return i < ub ? unit_mass(stats, i, U, M, p, m) : 0.0; };
+  double carry = 0.0;
+  for (int base = ua; base < ub; base += 64) {
+    const double incl = wave_incl_scan(mass(base + lane), lane);
+    carry += __shfl(incl, 63, kWave);
+  }
+  if (lane == 0) wtot[wave] = carry;
+  __syncthreads();
+  double Zs = 0.0, start = 0.0;
+#pragma unroll
+  for (int w = 0; w < kSmpWaves; ++w) {
+    if (w == wave) start = Zs;
+    Zs += wtot[w];
+  }
+  if (threadIdx.x == 0) lse[p] = (double)m + log(Zs);
+  if (!pick) return;
+  const double target = (double)u_draft[p] * Zs;
+  // the first wave whose running total exceeds the target (the last wave
+  // with units when rounding leaves none)
+  int wstar = kSmpWaves - 1;
+  while (wstar > 0 && (int64_t)U * wstar / kSmpWaves >= (int64_t)U * (wstar + 1) / kSmpWaves) --wstar;
+  {
+    double run = 0.0;
+#pragma unroll
+    for (int w = 0; w < kSmpWaves; ++w) {
+      if (run + wtot[w] > target) {
+        wstar = w;
+        break;
+      }
+      run += wtot[w];
+    }
+  }
+  if (wave != wstar) return;
+  // redo this wave's scans (same arithmetic) to find the crossing unit;
+  // when rounding leaves none, the wave's last unit is rescanned from the
+  // wave's total and yields its last row of nonzero mass
+  int ustar = ub - 1;
+  carry = 0.0;
+  double pre = start + carry;
+  for (int base = ua; base < ub; base += 64) {
+    const double incl = wave_incl_scan(mass(base + lane), lane);
+    const double tot = start + (carry + incl);
+    const unsigned long long hit = __ballot(base + lane < ub && tot > target);
+    if (hit) {
+      const int first = __ffsll((long long)hit) - 1;
+      const double prev = __shfl_up(tot, 1, kWave);
+      const double excl = (lane == 0) ? start + carry : prev;
+      ustar = base + first;
+      pre = __shfl(excl, first, kWave);
+      break;
+    }
+    carry += __shfl(incl, 63, kWave);
+    pre = start + carry;
+  }
+  const int y = rescan_unit<T>(mode, p, ustar, pre, target, m, S, Ms, W_r, Z, M, V, ntiles, U);
+  if (lane == 0) Ynew[p] = y;
 }
 
 // One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
@@ -182,8 +243,6 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
         if (lane == 0) atomicOr(err, XP_DEVERR_TOKEN);
         y = 0;
       }
-      if (sample)
-        sample_position<T>(0, p, 0.f, S, Ms, W_r, Z, M, V, stats, ntiles, U, lse + p, false);
     } else if (!sample) {
       uint64_t best = kv[m][0];
 #pragma unroll
@@ -194,8 +253,7 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
       for (int o = 1; o < 64; o <<= 1) best = umax64(best, shfl_xor_u64(best, o));
       y = (int)key_index(best);
     } else {
-      y = sample_position<T>(mode, p, u_draft[p], S, Ms, W_r, Z, M, V, stats, ntiles, U, lse + p,
-                             true);
+      y = Ynew[p];                                // chosen by k_sample
     }
     if (lane == 0) {
       Ynew[p] = y;
@@ -239,6 +297,18 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
   const int nkeys = mode == 0 ? h->lm_units_cur : h->read_wgs;
   const int U = mode == 0 ? h->lm_units_cur : h->read_units;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
+  if (temp) {
+    if (h->dtype == XP_BF16)
+      hipLaunchKernelGGL((k_sample<uint16_t>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
+                         h->V, M, h->ws.s, M, (const uint16_t*)h->W_r, (const uint16_t*)h->ws.z,
+                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
+                         Ynew, h->ws.lse, h->ws.ctrl, early);
+    else
+      hipLaunchKernelGGL((k_sample<float>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
+                         h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
+                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
+                         Ynew, h->ws.lse, h->ws.ctrl, early);
+  }
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,
                        h->B, h->V, M, h->ws.s, M, (const uint16_t*)h->W_r,

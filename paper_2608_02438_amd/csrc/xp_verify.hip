@@ -13,33 +13,57 @@
 
 namespace xp {
 
-// lseT[b][k] = log sum_v exp(T[b][k][v]) for sampled rows, k = 0..B.
-__global__ __launch_bounds__(256) void k_vtarget(const float* __restrict__ tl, int B, int V,
-                                                 const uint8_t* __restrict__ temp,
-                                                 double* __restrict__ lseT) {
-  const int k = blockIdx.x, b = blockIdx.y;
-  if (temp == nullptr || temp[b] == 0) return;
+// lseT[b][k] = log sum_v exp(T[b][k][v]) for sampled rows, k = 0..B, in two
+// steps: every workgroup reduces one chunk of kVChunk entries of a row to
+// (max, sum of exp(T - max) in fp64), then one thread per row merges the
+// chunks in order.
+__global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ tl, int B, int V,
+                                                      const uint8_t* __restrict__ temp,
+                                                      double* __restrict__ part) {
+  constexpr int PER = kVChunk / 256;
+  const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z, nc = gridDim.x;
+  if (temp[b] == 0) return;
   const float* row = tl + ((size_t)b * (B + 1) + k) * V;
+  float x[PER];
   float m = -INFINITY;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, row[v]);
-  __shared__ float sm[256];
-  __shared__ double sd[256];
-  sm[threadIdx.x] = m;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (threadIdx.x < s) sm[threadIdx.x] = fmaxf(sm[threadIdx.x], sm[threadIdx.x + s]);
-    __syncthreads();
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int v = c * kVChunk + i * 256 + threadIdx.x;
+    x[i] = v < V ? row[v] : -INFINITY;
+    m = fmaxf(m, x[i]);
   }
-  m = sm[0];
+  __shared__ float sm[4];
+  __shared__ double sd[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+  if (lane == 0) sm[wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
   double acc = 0.0;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) acc += exp((double)row[v] - (double)m);
-  sd[threadIdx.x] = acc;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc += x[i] == -INFINITY ? 0.0 : exp((double)x[i] - (double)m);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) acc += __shfl_xor(acc, o, kWave);
+  if (lane == 0) sd[wave] = acc;
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (threadIdx.x < s) sd[threadIdx.x] += sd[threadIdx.x + s];
-    __syncthreads();
+  if (threadIdx.x == 0) {
+    double* q = part + (((size_t)b * (B + 1) + k) * nc + c) * 2;
+    q[0] = (double)m;
+    q[1] = (sd[0] + sd[1]) + (sd[2] + sd[3]);
   }
-  if (threadIdx.x == 0) lseT[(size_t)b * (B + 1) + k] = (double)m + log(sd[0]);
+}
+
+__global__ void k_vtarget_comb(int batch, int B, int nc, const uint8_t* __restrict__ temp,
+                               const double* __restrict__ part, double* __restrict__ lseT) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= batch * (B + 1) || temp[i / (B + 1)] == 0) return;
+  const double* q = part + (size_t)i * nc * 2;
+  double m = q[0];
+  for (int c = 1; c < nc; ++c) m = fmax(m, q[2 * c]);
+  double sum = 0.0;
+  for (int c = 0; c < nc; ++c) sum += q[2 * c + 1] > 0.0 ? q[2 * c + 1] * exp(q[2 * c] - m) : 0.0;
+  lseT[i] = m + log(sum);
 }
 
 // l = s (+ W_r z) for position p at vocabulary row v, through the Read tile of
@@ -308,9 +332,14 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
                            const float* ures, int32_t* out_n, int32_t* out_next, hipStream_t st) {
   const int M = batch * h->B;
   const int with_read = h->state_k0 ? 0 : 1;
-  if (temp)
-    hipLaunchKernelGGL(k_vtarget, dim3(h->B + 1, batch), dim3(256), 0, st, tl, h->B, h->V, temp,
-                       h->ws.vstat);
+  if (temp) {
+    const int nc = (h->V + kVChunk - 1) / kVChunk;
+    hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1, batch), dim3(256), 0, st, tl, h->B,
+                       h->V, temp, h->ws.vpart);
+    const int rows = batch * (h->B + 1);
+    hipLaunchKernelGGL(k_vtarget_comb, dim3((rows + 255) / 256), dim3(256), 0, st, batch, h->B, nc,
+                       temp, h->ws.vpart, h->ws.vstat);
+  }
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
                      draft, temp, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
                      (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
