@@ -2,13 +2,23 @@
 // (v_mfma_f32_32x32x16_bf16), fused with the first stage of token selection.
 //
 // Once the position count M exceeds one 16-position block, streaming W_lm per
-// block (the A1 stream kernels) would read the 1.2 GB head M/16 times; here
-// every workgroup owns one selection unit of up to 256 vocabulary rows (16
-// tiles, the unit partition of unit_tile_lo) and 256 positions, so W_lm is
-// read once per 256 positions and the matrix cores, not HBM, bound the time
-// at M = 512.  The tile order is XCD-aware: the position tiles of one unit run
-// on the same XCD at the same time, so their reads of the unit's W_lm rows
-// share that XCD's L2.
+// block (the A1 stream kernels) would read the 1.2 GB head M/16 times; here a
+// tile is 256 vocabulary rows x 256 positions, so W_lm is read once per 256
+// positions and the matrix cores, not HBM, bound the time at M = 512.
+//
+// Selection units: the vocabulary tiles are split into U2 = 2 ceil(ntiles/16)
+// half-units (unit_tile_lo partition, at most 8 tiles each); a workgroup tile
+// covers the half-units 2u and 2u+1, LDS rows 0-127 holding the first and
+// rows 128-255 the second.  Each wave owns 128 rows (one half-unit) x 64
+// positions, so it forms the selection partials of its half-unit directly
+// from its accumulators: no reduction across waves.
+//
+// The kernel is persistent: one workgroup per CU walks its list of tiles, and
+// the global-to-LDS stage ring runs on across tile boundaries, so the next
+// tile's first stages load while the previous tile's epilogue (the s stores
+// and the selection partials) runs.  The tile order is XCD-aware: the
+// position tiles of one unit run on the same XCD at the same time, so their
+// reads of the unit's W_lm rows share that XCD's L2.
 //
 // Layout of the 32x32x16 operation (checked on gfx950): lane l holds row
 // l % 32 of A and column l % 32 of B, k = 8 (l / 32) .. + 8; result register
@@ -22,7 +32,8 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kGK = 32;             // k per LDS stage
 constexpr int kGWaves = 8;          // each wave: 128 rows x 64 positions (4 x 2 tiles of 32 x 32)
-constexpr int kGLds = 163840 / 16;  // all of the 160 KB, in 16-byte slots
+constexpr int kGNS = 5;             // stages of the ring (5 x 32 KB = all of the 160 KB)
+constexpr int kGPerXcd = 32;        // workgroups per XCD (one per CU)
 
 __device__ __forceinline__ floatx16 mma32(u32x4 a, u32x4 b, floatx16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
@@ -31,75 +42,87 @@ __device__ __forceinline__ floatx16 mma32(u32x4 a, u32x4 b, floatx16 c) {
 
 // A stage row holds 32 k (64 B = four 16-byte chunks); chunk c of row r sits in
 // slot 4 r + (c ^ swz(r)).  The swizzle makes the operand reads (32 rows, one
-// chunk) conflict-free for both 32- and 64-bank LDS grouping.
+// chunk) conflict-free.
 __device__ __forceinline__ int gslot(int r, int c) { return 4 * r + (c ^ (((r >> 1) ^ (r >> 3)) & 3)); }
 
-// Workgroup tile BN vocabulary rows (one selection unit of BN / 16 tiles) x BM
-// positions; the 8 waves form a (BN / 128) x (BM / 64) grid, each owning a
-// 128 x 64 block of D (128 accumulator registers), and per 16-wide k step a
-// wave reads 4 + 2 operand fragments from LDS for 8 matrix operations.
-//   BN = 256, BM = 256: up to 256 positions (one position tile).
-//   BN = 128, BM = 512: 512 positions per tile, so W_lm is read once per 512
-//     positions (the L2 cannot keep one workgroup's W_lm stages for a second
-//     position tile) and h, 4 MB, is what the workgroups share through L2.
-// Global data goes straight to LDS (global_load_lds_dwordx4, no staging
-// registers) NS - 1 stages ahead of the stage being computed; a wave waits
-// only for its own loads of the next stage, and the stage barrier does not
-// drain the others.
-template <int BN, int BM>
+// Workgroup (XCD xcd, index k8 on it) -> its i-th tile: unit slot
+// s = i * gpx + k8 / nMb (unit u = 8 s + xcd), position tile k8 % nMb.
+struct GemmSched {
+  int xcd, k8q, mb, gpx;
+  __device__ int unit(int i) const { return 8 * (i * gpx + k8q) + xcd; }
+};
+
 __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M,
-    int ntiles, int U, int nMb, float* __restrict__ S, int Ms, uint64_t* __restrict__ keys,
-    Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B) {
-  constexpr int WS = BN * kGK * 2 / 16, HS = BM * kGK * 2 / 16;  // slots per operand stage
-  constexpr int NS = kGLds / (WS + HS);                          // stages (5 or 4)
-  constexpr int NWR = BN / 128;                                  // waves along the rows
-  constexpr int WI = WS / 64 / kGWaves, HI = HS / 64 / kGWaves;  // 1 KB loads per wave and stage
-  static_assert(NWR * (BM / 64) == kGWaves, "wave grid");
-  __shared__ u32x4 lds[NS * (WS + HS)];                          // [stage][W | h]
-  // XCD-aware tile order: workgroup b runs on XCD b % 8; its k-th workgroup
-  // there takes unit 8 (k / nMb) + xcd and position tile k % nMb.
-  const int b = blockIdx.x, xcd = b & 7, k8 = b >> 3;
-  const int u = 8 * (k8 / nMb) + xcd, mb = k8 % nMb;
-  if (u >= U) return;                                            // whole workgroup
-  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
-  const int r0 = tlo * kTile, nrows = (thi - tlo) * kTile;      // <= BN rows
-  const int p0 = mb * BM;
+    int ntiles, int U2, int nMb, int gpx, float* __restrict__ S, int Ms,
+    uint64_t* __restrict__ keys, Stat* __restrict__ stats, const uint8_t* __restrict__ temp,
+    int B) {
+  constexpr int NS = kGNS;
+  constexpr int WS = 256 * kGK * 2 / 16, HS = 256 * kGK * 2 / 16;  // slots per operand stage
+  constexpr int WI = WS / 64 / kGWaves, HI = HS / 64 / kGWaves;    // 1 KB loads per wave
+  static_assert(NS * (WS + HS) * 16 <= 163840, "LDS");
+  __shared__ u32x4 lds[NS * (WS + HS)];                            // [stage][W | h]
+
+  const int Upair = U2 / 2;
+  GemmSched sc;
+  sc.xcd = blockIdx.x & 7;
+  const int k8 = blockIdx.x >> 3;
+  sc.k8q = k8 / nMb;
+  sc.mb = k8 % nMb;
+  sc.gpx = gpx;
+  // tiles of this workgroup: i with unit(i) < Upair
+  const int first = 8 * sc.k8q + sc.xcd;
+  const int ntl = first < Upair ? (Upair - first + 8 * gpx - 1) / (8 * gpx) : 0;
+  if (ntl == 0) return;                                            // whole workgroup
+  const int nk = H / kGK;
+  const int nstages = ntl * nk;
+  const int p0 = sc.mb * 256;
+
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wv = wave % NWR, wp = wave / NWR;                    // 128-row block, 64-position block
+  const int wv = wave & 1, wp = wave >> 1;                         // half-unit, 64-position block
 
-  // loads of a stage: wave w fills W slots [64 WI w, 64 WI (w + 1)) and h slots
+  // stage loads: wave w fills W slots [64 WI w, 64 WI (w + 1)) and h slots
   // [64 HI w, 64 HI (w + 1)) with 1 KB instructions; lane l of an instruction
-  // writes the next slot, i.e. row slot / 4, stored chunk l % 4, which holds
-  // logical chunk (l % 4) ^ swz(row)
-  int woff[WI], hoff[HI];
+  // writes the next slot, i.e. LDS row slot / 4, stored chunk l % 4, which
+  // holds logical chunk (l % 4) ^ swz(row).  LDS W row R is row R % 128 of
+  // half-unit 2u + R / 128 (rows past the half-unit are loaded, never used).
+  int wrow[WI], wcol[WI], hrow[HI];
 #pragma unroll
   for (int j = 0; j < WI; ++j) {
     const int row = (64 * (WI * wave + j) + lane) >> 2;
-    const int c = (lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3);
-    int wr = r0 + row;
-    wr = wr < V ? wr : V - 1;
-    woff[j] = wr * H + 8 * c;
+    wrow[j] = row;
+    wcol[j] = 8 * ((lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3));
   }
 #pragma unroll
   for (int j = 0; j < HI; ++j) {
     const int row = (64 * (HI * wave + j) + lane) >> 2;
-    const int c = (lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3);
     int hr = p0 + row;
     hr = hr < M ? hr : M - 1;
-    hoff[j] = hr * H + 8 * c;
+    hrow[j] = hr * H + 8 * ((lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3));
   }
-  const int nk = H / kGK;
-  auto issue = [&](int kc) {                                     // chunk kc (clamped) -> its stage
-    const int st = kc % NS;
-    const int kk = (kc < nk ? kc : nk - 1) * kGK;
+  // first rows of the two half-units of the tile being issued (cached per tile)
+  int iss_tile = -1, iss_r0 = 0, iss_r1 = 0;
+  auto issue = [&](int gs) {                                       // global stage gs (clamped)
+    gs = gs < nstages ? gs : nstages - 1;
+    const int ti = gs / nk, kc = gs - ti * nk;
+    if (ti != iss_tile) {                                          // wave-uniform
+      const int u = sc.unit(ti);
+      iss_tile = ti;
+      iss_r0 = unit_tile_lo(2 * u, ntiles, U2) * kTile;
+      iss_r1 = unit_tile_lo(2 * u + 1, ntiles, U2) * kTile;
+    }
+    const int st = gs % NS;
 #pragma unroll
-    for (int j = 0; j < WI; ++j)
-      lds_dma16(W + (size_t)(unsigned)woff[j] + kk, &lds[st * (WS + HS) + 64 * (WI * wave + j)]);
+    for (int j = 0; j < WI; ++j) {
+      int r = (wrow[j] < 128 ? iss_r0 : iss_r1) + (wrow[j] & 127);
+      r = r < V ? r : V - 1;
+      lds_dma16(W + (size_t)r * H + kc * kGK + wcol[j], &lds[st * (WS + HS) + 64 * (WI * wave + j)]);
+    }
 #pragma unroll
     for (int j = 0; j < HI; ++j)
-      lds_dma16(X + (size_t)(unsigned)hoff[j] + kk, &lds[st * (WS + HS) + WS + 64 * (HI * wave + j)]);
+      lds_dma16(X + (size_t)(unsigned)hrow[j] + kc * kGK,
+                &lds[st * (WS + HS) + WS + 64 * (HI * wave + j)]);
   };
 
   floatx16 acc[4][2];
@@ -111,126 +134,140 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
       for (int i = 0; i < 16; ++i) acc[a][c][i] = 0.f;
 
   const int lr = lane & 31, lk = lane >> 5;
-  int arow[4], brow[2];
+  // fragment reads of k step ks of global stage gs
+  auto rd = [&](int gs, int ks, u32x4 (&av)[4], u32x4 (&bv)[2]) {
+    const int base = (gs % NS) * (WS + HS);
+    const int c = 2 * ks + lk;
 #pragma unroll
-  for (int a = 0; a < 4; ++a) arow[a] = wv * 128 + a * 32 + lr;
+    for (int a = 0; a < 4; ++a) av[a] = lds[base + gslot(wv * 128 + a * 32 + lr, c)];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) brow[c] = wp * 64 + c * 32 + lr;
+    for (int cc = 0; cc < 2; ++cc) bv[cc] = lds[base + WS + gslot(wp * 64 + cc * 32 + lr, c)];
+  };
+  auto mm = [&](const u32x4 (&av)[4], const u32x4 (&bv)[2]) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) acc[a][cc] = mma32(av[a], bv[cc], acc[a][cc]);
+  };
 
+  // epilogue of tile ti: s from the accumulators, and the selection partials
+  // of this wave's half-unit for its 64 positions
+  auto epilogue = [&](int ti) {
+    const int hu = 2 * sc.unit(ti) + wv;
+    const int rbase = unit_tile_lo(hu, ntiles, U2) * kTile;
+    const int nr = unit_tile_lo(hu + 1, ntiles, U2) * kTile - rbase;   // <= 128, multiple of 16
+    bool psamp[2];
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s) issue(s);
-  constexpr int kPend = (WI + HI) * (NS - 2);                    // loads of later stages in flight
-  static_assert(kPend < 64, "vmcnt field");
-  for (int kc = 0; kc < nk; ++kc) {
-    // this wave's loads of chunk kc are done once at most kPend later loads
-    // are outstanding; the barrier then covers every wave's loads of chunk kc
-    // and every wave's reads of chunk kc - 1
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0x0f70 | (kPend & 15) | ((kPend >> 4) << 14));
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    issue(kc + NS - 1);                                          // into the stage read at kc - 1
-    const int st = kc % NS;
-    // both k steps' fragments first, so the second set of LDS reads overlaps
-    // the first matrix operations
-    u32x4 av[kGK / 16][4], bv[kGK / 16][2];
-#pragma unroll
-    for (int ks = 0; ks < kGK / 16; ++ks) {
-      const int c = 2 * ks + lk;
-#pragma unroll
-      for (int a = 0; a < 4; ++a) av[ks][a] = lds[st * (WS + HS) + gslot(arow[a], c)];
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc) bv[ks][cc] = lds[st * (WS + HS) + WS + gslot(brow[cc], c)];
+    for (int c = 0; c < 2; ++c) {
+      const int p = p0 + wp * 64 + c * 32 + lr;
+      psamp[c] = p < M && load_flag(temp, (p < M ? p : M - 1) / B, W) != 0;
     }
+    const bool any_sample = __ballot(psamp[0] || psamp[1]) != 0;
 #pragma unroll
-    for (int ks = 0; ks < kGK / 16; ++ks)
+    for (int c = 0; c < 2; ++c) {
+      const int p = p0 + wp * 64 + c * 32 + lr;
+      const bool pact = p < M;
+      const bool psample = psamp[c];
+      // running maximum and its row: rows increase along (a, q, e) in every
+      // lane, so a strict comparison keeps the lowest index of a tie
+      float bvv = -INFINITY;
+      uint32_t bix = 0xFFFFFFFFu;
+      Stat st = stat_empty();
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < 4; ++a) {
 #pragma unroll
-        for (int cc = 0; cc < 2; ++cc) acc[a][cc] = mma32(av[ks][a], bv[ks][cc], acc[a][cc]);
-  }
-  // drain the (clamped) loads issued past the last chunk before LDS is reused
-  __builtin_amdgcn_s_waitcnt(0x0070);                            // vmcnt(0) lgkmcnt(0)
-  __syncthreads();
-
-  // --- epilogue: s straight from the accumulators; selection partials per
-  //     position over this unit's rows (lanes l, l+32, then the row blocks) ---
-  bool psamp[2];
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int p = p0 + brow[c];
-    psamp[c] = p < M && load_flag(temp, (p < M ? p : M - 1) / B, W) != 0;
-  }
-  const bool any_sample = __ballot(psamp[0] || psamp[1]) != 0;
-  uint64_t* kr = reinterpret_cast<uint64_t*>(lds);               // [row block][BM positions]
-  Stat* sr = reinterpret_cast<Stat*>(kr + NWR * BM);
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int p = p0 + brow[c];
-    const bool pact = p < M;
-    const bool psample = psamp[c];
-    uint64_t best = kKeyMin;
-    Stat st = stat_empty();
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int rl = wv * 128 + a * 32 + 8 * q + 4 * lk;       // local row of acc[a][c][4q]
-        const bool rv = pact && rl < nrows;                      // nrows is a multiple of 16
-        if (rv)
-          *reinterpret_cast<float4*>(S + s_index(p, r0 + rl, Ms)) =
-              make_float4(acc[a][c][4 * q], acc[a][c][4 * q + 1], acc[a][c][4 * q + 2],
-                          acc[a][c][4 * q + 3]);
-        // rows past V (the last unit's padding, computed from the clamped
-        // row V-1) are stored into the padding of s but never selected
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ev = rv && r0 + rl + e < V;
-          const uint64_t key = umax64(best, argmax_key(acc[a][c][4 * q + e], (uint32_t)(r0 + rl + e)));
-          best = (ev && !psample) ? key : best;
-        }
-        if (any_sample) {
+        for (int q = 0; q < 4; ++q) {
+          const int rl = a * 32 + 8 * q + 4 * lk;                  // local row of acc[a][c][4q]
+          const bool rv = pact && rl < nr;
+          if (rv)
+            *reinterpret_cast<float4*>(S + s_index(p, rbase + rl, Ms)) =
+                make_float4(acc[a][c][4 * q], acc[a][c][4 * q + 1], acc[a][c][4 * q + 2],
+                            acc[a][c][4 * q + 3]);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const bool ev = rv && r0 + rl + e < V && psample;
-            const Stat nx = stat_merge(st, Stat{acc[a][c][4 * q + e], 1.f});
-            st.m = ev ? nx.m : st.m;
-            st.s = ev ? nx.s : st.s;
+            const float x = acc[a][c][4 * q + e];
+            const bool take = rv && !psample && rbase + rl + e < V && x > bvv;
+            bvv = take ? x : bvv;
+            bix = take ? (uint32_t)(rbase + rl + e) : bix;
+          }
+          if (any_sample) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bool ev = rv && psample && rbase + rl + e < V;
+              const Stat nx = stat_merge(st, Stat{acc[a][c][4 * q + e], 1.f});
+              st.m = ev ? nx.m : st.m;
+              st.s = ev ? nx.s : st.s;
+            }
           }
         }
       }
-    }
-    best = umax64(best, shfl_xor_u64(best, 32));
-    const Stat o{__shfl_xor(st.m, 32, kWave), __shfl_xor(st.s, 32, kWave)};
-    st = stat_merge(st, o);
-    if (lk == 0) {
-      kr[wv * BM + brow[c]] = best;
-      sr[wv * BM + brow[c]] = st;
-    }
-  }
-  __syncthreads();
-  for (int pl = tid; pl < BM; pl += kGWaves * kWave) {
-    const int p = p0 + pl;
-    if (p < M) {
-      uint64_t bb = kr[pl];
-      Stat ss = sr[pl];
-#pragma unroll
-      for (int w = 1; w < NWR; ++w) {
-        bb = umax64(bb, kr[w * BM + pl]);
-        ss = stat_merge(ss, sr[w * BM + pl]);
+      uint64_t best = bix == 0xFFFFFFFFu ? kKeyMin : argmax_key(bvv, bix);
+      best = umax64(best, shfl_xor_u64(best, 32));
+      const Stat o{__shfl_xor(st.m, 32, kWave), __shfl_xor(st.s, 32, kWave)};
+      st = stat_merge(st, o);
+      if (lk == 0 && pact) {
+        keys[(size_t)hu * M + p] = best;
+        if (psample) stats[(size_t)hu * M + p] = st;
       }
-      keys[(size_t)u * M + p] = bb;
-      stats[(size_t)u * M + p] = ss;
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[a][c][i] = 0.f;
+  };
+
+#pragma unroll
+  for (int s = 0; s < NS; ++s) issue(s);
+  constexpr int kP0 = (WI + HI) * (NS - 1), kP = (WI + HI) * (NS - 2);
+  static_assert(kP0 < 64, "vmcnt field");
+  // stage 0 landed (this wave's loads), then every wave's
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0070 | (kP0 & 15) | ((kP0 >> 4) << 14));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  u32x4 fa[2][4], fb[2][2];                 // fragment sets of the two k steps of a stage
+  rd(0, 0, fa[0], fb[0]);
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  int ti = 0, kc = 0;
+  for (int gs = 0; gs < nstages; ++gs) {
+    // k step 1 of stage gs is read while k step 0 multiplies; the barrier
+    // between the two k steps (wait: stage gs + 1 landed for this wave, and
+    // this wave's reads of stage gs are done) makes stage gs + 1 readable for
+    // everyone and frees the slot of stage gs for stage gs + NS.  Other
+    // vector-memory operations (the epilogue's stores) only make the wait
+    // stricter.
+    rd(gs, 1, fa[1], fb[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mm(fa[0], fb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0x0070 | (kP & 15) | ((kP >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(gs + NS);
+    rd(gs + 1, 0, fa[0], fb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    mm(fa[1], fb[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_sched_barrier(0);
+    if (++kc == nk) {                                              // wave-uniform
+      epilogue(ti);
+      kc = 0;
+      ++ti;
     }
   }
+  __builtin_amdgcn_s_waitcnt(0x0070);        // the clamped loads past the end
 }
 
 // ---------------------------------------------------------------------------
-// Selection units of the GEMM path: 16 tiles (256 rows).  The launch and
-// every reader of the per-unit partials use this one function.
+// Selection units of the GEMM path: the half-units (at most 8 tiles each).
+// The launch and every reader of the per-unit partials use this one function.
 int gemm_units(const xp_handle* h, int M) {
   (void)M;
-  return (h->ntiles + 15) / 16;
+  return 2 * ((h->ntiles + 15) / 16);
 }
 
 bool lmhead_gemm_ok(const xp_handle* h, int M) {
@@ -239,20 +276,15 @@ bool lmhead_gemm_ok(const xp_handle* h, int M) {
 
 hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
                               hipStream_t st) {
-  const int U = gemm_units(h, M);
-  if (true) {                                  // 256 x 256 tiles for every M (measured faster)
-    const int nMb = (M + 255) / 256;
-    hipLaunchKernelGGL((k_lmhead_gemm<256, 256>), dim3(8 * nMb * ((U + 7) / 8)),
-                       dim3(kGWaves * kWave), 0, st, (const uint16_t*)h->W_lm,
-                       (const uint16_t*)hidden, h->V, h->H, M, h->ntiles, U, nMb, h->ws.s,
-                       M, h->ws.keys, h->ws.stats, temp, h->B);
-  } else {
-    const int nMb = (M + 511) / 512;
-    hipLaunchKernelGGL((k_lmhead_gemm<128, 512>), dim3(8 * nMb * ((U + 7) / 8)),
-                       dim3(kGWaves * kWave), 0, st, (const uint16_t*)h->W_lm,
-                       (const uint16_t*)hidden, h->V, h->H, M, h->ntiles, U, nMb, h->ws.s,
-                       M, h->ws.keys, h->ws.stats, temp, h->B);
-  }
+  const int U2 = gemm_units(h, M);
+  const int nMb = (M + 255) / 256;
+  // workgroups per XCD: a multiple of the position tiles per unit
+  int per = kGPerXcd / nMb * nMb;
+  per = per > 0 ? per : nMb;
+  const int gpx = per / nMb;
+  hipLaunchKernelGGL(k_lmhead_gemm, dim3(8 * per), dim3(kGWaves * kWave), 0, st,
+                     (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M, h->ntiles,
+                     U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
   return hipGetLastError();
 }
 
