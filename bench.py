@@ -8,9 +8,11 @@ The default workload is the Qwen3-8B shape at batch 1 (H = 4096, V = 151936,
 r = 256, block 16, greedy, K = 6).
 
 Prints one JSON line.  `value` is refined draft blocks per second; `roofline`
-rates the dominant kernel (the LM-head stream) by its algorithmic bytes over
-its own duration, measured with HIP events recorded by the library on the
-stream the kernel runs on; `cpu_baseline` times the fp64 oracle on one block.
+rates the dominant kernel, the LM-head launch (the stream kernel for one
+16-position block, the GEMM for more), by its algorithmic bytes (HBM-bound
+workloads) or flops (MFMA-bound ones, above the ridge) over its own duration,
+measured with HIP events recorded by the library on the stream the kernel runs
+on; `cpu_baseline` times the fp64 oracle on one block.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
     python bench.py --copy-probe BYTES      (a plain device copy, for counter scaling)
@@ -28,27 +30,36 @@ sys.path.insert(0, ROOT)
 
 METRIC = "refined draft blocks/sec (refine+LM-head+verify), Qwen3-8B shape; % HBM/MFMA peak"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md")
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc", "xp_lmhead.hip")
+MFMA_BF16_PEAK_TFS = 2517.0          # dense bf16 matrix peak of the MI355X
+CSRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc")
+# committed counter summaries of the LM-head kernel, per workload: (file, kernel source)
+TRAFFIC = {
+    "qwen3-8b-bf16-B16-b1-greedy": ("k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md", "xp_lmhead.hip"),
+    "qwen3-8b-bf16-B16-b32-greedy": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b32_traffic.md", "xp_gemm.hip"),
+}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_source_hash(src: str) -> str:
+    return hashlib.sha256(open(os.path.join(CSRC, src), "rb").read()).hexdigest()[:16]
 
 
-def committed_traffic():
-    """HBM bytes per LM-head launch from the committed counter summary, if it
-    was taken on the current kernel source; otherwise None."""
-    if not os.path.exists(TRAFFIC_FILE):
+def committed_traffic(workload: str):
+    """HBM bytes per LM-head launch from the committed counter summary of this
+    workload, if it was taken on the current kernel source; otherwise None."""
+    if workload not in TRAFFIC:
         return None
-    txt = open(TRAFFIC_FILE).read()
+    fn, src = TRAFFIC[workload]
+    path = os.path.join(ROOT, "profiles", fn)
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
     m = re.search(r"source_sha256_16:\s*([0-9a-f]{16})", txt)
     t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
-    if not m or not t or m.group(1) != kernel_source_hash():
+    if not m or not t or m.group(1) != kernel_source_hash(src):
         return None
     return float(t.group(1))
 
@@ -169,11 +180,29 @@ def main():
     lm_us = lm_ms * 1e3 / max(lm_n, 1)
     M = wl.batch * wl.B
     es = 2 if wl.dtype == "bf16" else 4
-    # algorithmic bytes of one LM-head launch: W_lm once, h once, s written once
+    # algorithmic bytes of one LM-head launch: W_lm once, h once, s written once;
+    # algorithmic flops 2 M V H.  The launch is HBM-bound below the ridge
+    # (peak flops / peak bytes, about 315 flop/B) and MFMA-bound above it.
     lm_bytes = wl.V * wl.H * es + M * wl.H * es + M * wl.V * 4
-    achieved = lm_bytes / (lm_us * 1e-6) / 1e9
+    lm_flops = 2.0 * M * wl.V * wl.H
+    mfma_bound = wl.dtype == "bf16" and lm_flops / lm_bytes > MFMA_BF16_PEAK_TFS * 1e3 / HBM_PEAK_GBS
+    if mfma_bound:
+        achieved = lm_flops / (lm_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFS,
+                "kernel": "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)",
+                "algorithmic_flops_per_launch": lm_flops}
+    else:
+        achieved = lm_bytes / (lm_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS,
+                "kernel": "k_lmhead (base readout s = W_lm h)" if M <= 16 else
+                          "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)"}
+    roof.update({"traffic": committed_traffic(wl.name), "algorithmic_bytes_per_launch": lm_bytes,
+                 "launch_us": lm_us})
     n_acc = vout[0].cpu().numpy()
-    log(f"[bench] {ms_step:.3f} ms/step, LM head {lm_us:.1f} us ({achieved:.0f} GB/s)")
+    log(f"[bench] {ms_step:.3f} ms/step, LM head {lm_us:.1f} us "
+        f"({achieved:.0f} {roof['unit']}, {100 * roof['frac']:.1f}% of peak)")
 
     line = {
         "metric": METRIC, "value": blocks_s, "unit": "blocks/s", "n_gpus": 1,
@@ -184,10 +213,7 @@ def main():
                 "rank-256 refiner, N(0,1) drafter hidden states, uniform anchors",
         "config": {"workload": wl.name, "batch": wl.batch, "block": wl.B, "K": wl.K,
                    "H": wl.H, "V": wl.V, "r": wl.r, "temperature": wl.temp},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": committed_traffic(),
-                     "kernel": "k_lmhead (base readout s = W_lm h)",
-                     "algorithmic_bytes_per_launch": lm_bytes, "launch_us": lm_us},
+        "roofline": roof,
         "refined_tokens_per_s": blocks_s * wl.B,
         "stage_ms_per_step": {k: v[0] / max(1, 3) for k, v in breakdown.items()},
         "accepted_mean": float(np.mean(n_acc)),
