@@ -118,6 +118,15 @@ __device__ __forceinline__ Stat stat_merge(Stat a, Stat b) {
   float m = fmaxf(a.m, b.m);
   return Stat{m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
 }
+// Four values at once (absent ones passed as -inf): one rescale of the running
+// sum instead of one per value.
+__device__ __forceinline__ Stat stat_add4(Stat a, float x0, float x1, float x2, float x3) {
+  const float m = fmaxf(a.m, fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
+  const float s = a.s * __expf(a.m - m) +
+                  ((__expf(x0 - m) + __expf(x1 - m)) + (__expf(x2 - m) + __expf(x3 - m)));
+  const bool none = m == -INFINITY;              // nothing present so far
+  return Stat{none ? a.m : m, none ? a.s : s};
+}
 
 // ---------------------------------------------------------------------------
 // Vocabulary partition.  The ntiles = ceil(V/16) tiles are cut into U

@@ -191,13 +191,11 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
             bix = take ? (uint32_t)(rbase + rl + e) : bix;
           }
           if (any_sample) {
+            float x[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bool ev = rv && psample && rbase + rl + e < V;
-              const Stat nx = stat_merge(st, Stat{acc[a][c][4 * q + e], 1.f});
-              st.m = ev ? nx.m : st.m;
-              st.s = ev ? nx.s : st.s;
-            }
+            for (int e = 0; e < 4; ++e)
+              x[e] = (rv && psample && rbase + rl + e < V) ? acc[a][c][4 * q + e] : -INFINITY;
+            st = stat_add4(st, x[0], x[1], x[2], x[3]);
           }
         }
       }

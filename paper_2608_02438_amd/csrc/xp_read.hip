@@ -370,13 +370,11 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
         bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
       }
       if (any_sample) {
+        float x[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bool v = act[pb] && row0 + i < V && sample[pb];
-          const Stat nx = stat_merge(st[pb], Stat{acc[i], 1.f});
-          st[pb].m = v ? nx.m : st[pb].m;
-          st[pb].s = v ? nx.s : st[pb].s;
-        }
+        for (int i = 0; i < 4; ++i)
+          x[i] = (sample[pb] && (!last || row0 + i < V)) ? acc[i] : -INFINITY;
+        st[pb] = stat_add4(st[pb], x[0], x[1], x[2], x[3]);
       }
       if (out_logits) {
         const int p = pw + kTile * pb + (lane & 15);
