@@ -359,13 +359,21 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     const int t = t0 + j;
     const int row0 = t * kTile + 4 * (lane >> 4);
     const bool last = (t + 1) * kTile > V;         // wave-uniform: rows past V in this tile
+    // the P chains interleaved (each is RT::chain's sequence of operations)
+    floatx4 accs[P];
+#pragma unroll
+    for (int pb = 0; pb < P; ++pb) accs[pb] = c[pb];
+#pragma unroll
+    for (int i = 0; i < NU; ++i)
+#pragma unroll
+      for (int pb = 0; pb < P; ++pb) accs[pb] = Mfma<uint16_t>::mma(a[i], zf[pb][i], accs[pb]);
 #pragma unroll
     for (int pb = 0; pb < P; ++pb) {
-      const floatx4 acc = RT::chain(a, zf[pb], c[pb]);
-      const bool gv = act[pb] && !sample[pb];
+      const floatx4 acc = accs[pb];
+      const bool gv = act[pb] & !sample[pb];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bool take = gv && (!last || row0 + i < V) && acc[i] > bv[pb];
+        const bool take = gv & (!last | (row0 + i < V)) & (acc[i] > bv[pb]);
         bv[pb] = take ? acc[i] : bv[pb];
         bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
       }
@@ -373,7 +381,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
         float x[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          x[i] = (sample[pb] && (!last || row0 + i < V)) ? acc[i] : -INFINITY;
+          x[i] = (sample[pb] & (!last | (row0 + i < V))) ? acc[i] : -INFINITY;
         st[pb] = stat_add4(st[pb], x[0], x[1], x[2], x[3]);
       }
       if (out_logits) {
