@@ -99,6 +99,38 @@ def cpu_baseline(wl, weights, inp):
                       f"passes and verification, {dt:.1f} s"}
 
 
+def k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout):
+    """Cost of K Jacobi passes (the latency-vs-K table of the paper's evaluation):
+    ms per refine + verify at fixed K and with the early exit, the mean number of
+    passes the early exit runs, and the share of sequences at a fixed point."""
+    import numpy as np
+    import torch
+    rows = []
+    for K in range(1, 9):
+        for early in (False, True):
+            def st():
+                ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=K,
+                                 early_exit=early, out=out)
+                ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
+                                 u_resample=u_res, out=vout)
+            for _ in range(max(args.warmup, 2)):
+                st()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                st()
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / args.steps
+            it = out.iters.cpu().numpy()
+            rows.append({"K": K, "early_exit": early, "ms_per_step": dt * 1e3,
+                         "blocks_per_s": wl.batch / dt, "iters_mean": float(np.mean(it)),
+                         "fixed_point_before_K": float(np.mean(it < K))})
+            log(f"[k-sweep] K={K} early_exit={early}: {dt * 1e3:.3f} ms/step, "
+                f"iters {np.mean(it):.2f}")
+    print(json.dumps({"k_sweep": rows, "workload": wl.name, "batch": wl.batch, "block": wl.B,
+                      "steps": args.steps, "data": "synthetic"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,6 +139,9 @@ def main():
     ap.add_argument("--workload", default="qwen3-8b-bf16-B16-b1-greedy")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--k-sweep", action="store_true",
+                    help="time refine + verify for K = 1..8 passes, fixed K and with the "
+                         "per-batch early exit, and print that table as one JSON line instead")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -150,6 +185,11 @@ def main():
         ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=wl.K, out=out)
         ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
                          u_resample=u_res, out=vout)
+
+    if args.k_sweep:
+        k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout)
+        ref.close()
+        return
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
