@@ -118,7 +118,7 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
   const size_t npairs = (size_t)w->B * (w->B - 1) / 2;
   size_t nk = (size_t)(h->lm_chunks > h->read_wgs ? h->lm_chunks : h->read_wgs);
   size_t nu = (size_t)(h->lm_chunks > h->read_units ? h->lm_chunks : h->read_units);
-  const size_t ng = (size_t)gemm_units(h, 1 << 30);     // the larger (8-tile) partition
+  const size_t ng = (size_t)gemm_units_max(h);          // the finest GEMM unit partition
   nk = nk > ng ? nk : ng;
   nu = nu > ng ? nu : ng;
   struct Slice {

@@ -3,15 +3,18 @@
 //
 // Once the position count M exceeds one 16-position block, streaming W_lm per
 // block (the A1 stream kernels) would read the 1.2 GB head M/16 times; here a
-// tile is 256 vocabulary rows x 256 positions, so W_lm is read once per 256
-// positions and the matrix cores, not HBM, bound the time at M = 512.
+// tile is BN vocabulary rows x BM positions, so W_lm is read once per BM
+// positions.  Two shapes: 256 x 256 for more than 128 positions (the matrix
+// cores, not HBM, bound the time at M = 512), and 128 x 128 up to 128
+// positions, where the launch is HBM-bound and the smaller tile gives 4x more
+// tiles to balance over the CUs and a deeper stage ring.
 //
-// Selection units: the vocabulary tiles are split into U2 = 2 ceil(ntiles/16)
-// half-units (unit_tile_lo partition, at most 8 tiles each); a workgroup tile
-// covers the half-units 2u and 2u+1, LDS rows 0-127 holding the first and
-// rows 128-255 the second.  Each wave owns 128 rows (one half-unit) x 64
-// positions, so it forms the selection partials of its half-unit directly
-// from its accumulators: no reduction across waves.
+// Selection units: the vocabulary tiles are split into U = 2 ceil(ntiles /
+// (BN/16)) units (unit_tile_lo partition, at most BN/32 tiles each); a
+// workgroup tile covers the units 2u and 2u+1, LDS rows [0, BN/2) holding the
+// first and [BN/2, BN) the second.  Each wave owns BN/2 rows (one unit) x BM/4
+// positions, so it forms the selection partials of its unit directly from its
+// accumulators: no reduction across waves.
 //
 // The kernel is persistent: one workgroup per CU walks its list of tiles, and
 // the global-to-LDS stage ring runs on across tile boundaries, so the next
@@ -31,8 +34,7 @@ namespace xp {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kGK = 32;             // k per LDS stage
-constexpr int kGWaves = 8;          // each wave: 128 rows x 64 positions (4 x 2 tiles of 32 x 32)
-constexpr int kGNS = 5;             // stages of the ring (5 x 32 KB = all of the 160 KB)
+constexpr int kGWaves = 8;          // 2 (rows) x 4 (positions) waves
 constexpr int kGPerXcd = 32;        // workgroups per XCD (one per CU)
 
 __device__ __forceinline__ floatx16 mma32(u32x4 a, u32x4 b, floatx16 c) {
@@ -52,14 +54,19 @@ struct GemmSched {
   __device__ int unit(int i) const { return 8 * (i * gpx + k8q) + xcd; }
 };
 
+template <int BN, int BM>
 __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M,
     int ntiles, int U2, int nMb, int gpx, float* __restrict__ S, int Ms,
     uint64_t* __restrict__ keys, Stat* __restrict__ stats, const uint8_t* __restrict__ temp,
     int B) {
-  constexpr int NS = kGNS;
-  constexpr int WS = 256 * kGK * 2 / 16, HS = 256 * kGK * 2 / 16;  // slots per operand stage
+  constexpr int RW = BN / 2, PW = BM / 4;                          // rows, positions per wave
+  constexpr int NA = RW / 32, NB = PW / 32;                        // 32 x 32 blocks per wave
+  constexpr int WS = BN * kGK * 2 / 16, HS = BM * kGK * 2 / 16;    // slots per operand stage
   constexpr int WI = WS / 64 / kGWaves, HI = HS / 64 / kGWaves;    // 1 KB loads per wave
+  constexpr int NS0 = 163840 / ((WS + HS) * 16);
+  constexpr int NS = NS0 < 8 ? NS0 : 8;                            // ring stages
+  static_assert(WI >= 1 && HI >= 1 && NA >= 1 && NB >= 1, "tile shape");
   static_assert(NS * (WS + HS) * 16 <= 163840, "LDS");
   __shared__ u32x4 lds[NS * (WS + HS)];                            // [stage][W | h]
 
@@ -76,17 +83,17 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
   if (ntl == 0) return;                                            // whole workgroup
   const int nk = H / kGK;
   const int nstages = ntl * nk;
-  const int p0 = sc.mb * 256;
+  const int p0 = sc.mb * BM;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wv = wave & 1, wp = wave >> 1;                         // half-unit, 64-position block
+  const int wv = wave & 1, wp = wave >> 1;                         // unit, position block
 
   // stage loads: wave w fills W slots [64 WI w, 64 WI (w + 1)) and h slots
   // [64 HI w, 64 HI (w + 1)) with 1 KB instructions; lane l of an instruction
   // writes the next slot, i.e. LDS row slot / 4, stored chunk l % 4, which
-  // holds logical chunk (l % 4) ^ swz(row).  LDS W row R is row R % 128 of
-  // half-unit 2u + R / 128 (rows past the half-unit are loaded, never used).
+  // holds logical chunk (l % 4) ^ swz(row).  LDS W row R is row R % RW of
+  // unit 2u + R / RW (rows past the unit are loaded, never used).
   int wrow[WI], wcol[WI], hrow[HI];
 #pragma unroll
   for (int j = 0; j < WI; ++j) {
@@ -101,7 +108,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     hr = hr < M ? hr : M - 1;
     hrow[j] = hr * H + 8 * ((lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3));
   }
-  // first rows of the two half-units of the tile being issued (cached per tile)
+  // first rows of the two units of the tile being issued (cached per tile)
   int iss_tile = -1, iss_r0 = 0, iss_r1 = 0;
   auto issue = [&](int gs) {                                       // global stage gs (clamped)
     gs = gs < nstages ? gs : nstages - 1;
@@ -115,7 +122,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const int st = gs % NS;
 #pragma unroll
     for (int j = 0; j < WI; ++j) {
-      int r = (wrow[j] < 128 ? iss_r0 : iss_r1) + (wrow[j] & 127);
+      int r = (wrow[j] < RW ? iss_r0 : iss_r1) + (wrow[j] % RW);
       r = r < V ? r : V - 1;
       lds_dma16(W + (size_t)r * H + kc * kGK + wcol[j], &lds[st * (WS + HS) + 64 * (WI * wave + j)]);
     }
@@ -125,47 +132,49 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
                 &lds[st * (WS + HS) + WS + 64 * (HI * wave + j)]);
   };
 
-  floatx16 acc[4][2];
+  floatx16 acc[NA][NB];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < NA; ++a)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < NB; ++c)
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][c][i] = 0.f;
 
   const int lr = lane & 31, lk = lane >> 5;
   // fragment reads of k step ks of global stage gs
-  auto rd = [&](int gs, int ks, u32x4 (&av)[4], u32x4 (&bv)[2]) {
+  auto rd = [&](int gs, int ks, u32x4 (&av)[NA], u32x4 (&bv)[NB]) {
     const int base = (gs % NS) * (WS + HS);
     const int c = 2 * ks + lk;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) av[a] = lds[base + gslot(wv * 128 + a * 32 + lr, c)];
+    for (int a = 0; a < NA; ++a) av[a] = lds[base + gslot(wv * RW + a * 32 + lr, c)];
 #pragma unroll
-    for (int cc = 0; cc < 2; ++cc) bv[cc] = lds[base + WS + gslot(wp * 64 + cc * 32 + lr, c)];
+    for (int cc = 0; cc < NB; ++cc) bv[cc] = lds[base + WS + gslot(wp * PW + cc * 32 + lr, c)];
   };
-  auto mm = [&](const u32x4 (&av)[4], const u32x4 (&bv)[2]) {
+  auto mm = [&](const u32x4 (&av)[NA], const u32x4 (&bv)[NB]) {
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < NA; ++a)
 #pragma unroll
-      for (int cc = 0; cc < 2; ++cc) acc[a][cc] = mma32(av[a], bv[cc], acc[a][cc]);
+      for (int cc = 0; cc < NB; ++cc) acc[a][cc] = mma32(av[a], bv[cc], acc[a][cc]);
   };
 
   // epilogue of tile ti: s from the accumulators, and the selection partials
-  // of this wave's half-unit for its 64 positions
+  // of this wave's unit for its PW positions
   auto epilogue = [&](int ti) {
     const int hu = 2 * sc.unit(ti) + wv;
     const int rbase = unit_tile_lo(hu, ntiles, U2) * kTile;
-    const int nr = unit_tile_lo(hu + 1, ntiles, U2) * kTile - rbase;   // <= 128, multiple of 16
-    bool psamp[2];
+    const int nr = unit_tile_lo(hu + 1, ntiles, U2) * kTile - rbase;   // <= RW, multiple of 16
+    bool psamp[NB];
+    bool anyp = false;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int p = p0 + wp * 64 + c * 32 + lr;
+    for (int c = 0; c < NB; ++c) {
+      const int p = p0 + wp * PW + c * 32 + lr;
       psamp[c] = p < M && load_flag(temp, (p < M ? p : M - 1) / B, W) != 0;
+      anyp = anyp || psamp[c];
     }
-    const bool any_sample = __ballot(psamp[0] || psamp[1]) != 0;
+    const bool any_sample = __ballot(anyp) != 0;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int p = p0 + wp * 64 + c * 32 + lr;
+    for (int c = 0; c < NB; ++c) {
+      const int p = p0 + wp * PW + c * 32 + lr;
       const bool pact = p < M;
       const bool psample = psamp[c];
       // running maximum and its row: rows increase along (a, q, e) in every
@@ -174,7 +183,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
       uint32_t bix = 0xFFFFFFFFu;
       Stat st = stat_empty();
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+      for (int a = 0; a < NA; ++a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int rl = a * 32 + 8 * q + 4 * lk;                  // local row of acc[a][c][4q]
@@ -209,9 +218,9 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
       }
     }
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < NA; ++a)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < NB; ++c)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[a][c][i] = 0.f;
   };
@@ -225,7 +234,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
   __builtin_amdgcn_s_waitcnt(0x0070 | (kP0 & 15) | ((kP0 >> 4) << 14));
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  u32x4 fa[2][4], fb[2][2];                 // fragment sets of the two k steps of a stage
+  u32x4 fa[2][NA], fb[2][NB];               // fragment sets of the two k steps of a stage
   rd(0, 0, fa[0], fb[0]);
   __builtin_amdgcn_s_waitcnt(0xc07f);
   int ti = 0, kc = 0;
@@ -261,12 +270,17 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
 }
 
 // ---------------------------------------------------------------------------
-// Selection units of the GEMM path: the half-units (at most 8 tiles each).
-// The launch and every reader of the per-unit partials use this one function.
+// Tile shape for M positions: 128 x 128 up to 128 positions, 256 x 256 above.
+static int gemm_bn(int M) { return M <= 128 ? 128 : 256; }
+
+// Selection units of the GEMM path for M positions: 2 per workgroup tile of
+// BN rows (at most BN/32 tiles each).  The launch and every reader of the
+// per-unit partials use this one function; gemm_units_max bounds it.
 int gemm_units(const xp_handle* h, int M) {
-  (void)M;
-  return 2 * ((h->ntiles + 15) / 16);
+  const int bn = gemm_bn(M);
+  return 2 * ((h->ntiles + bn / 16 - 1) / (bn / 16));
 }
+int gemm_units_max(const xp_handle* h) { return gemm_units(h, 1); }
 
 bool lmhead_gemm_ok(const xp_handle* h, int M) {
   return h->dtype == XP_BF16 && M > kTile && h->H % kGK == 0;
@@ -275,14 +289,20 @@ bool lmhead_gemm_ok(const xp_handle* h, int M) {
 hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
                               hipStream_t st) {
   const int U2 = gemm_units(h, M);
-  const int nMb = (M + 255) / 256;
+  const int bm = gemm_bn(M);
+  const int nMb = (M + bm - 1) / bm;
   // workgroups per XCD: a multiple of the position tiles per unit
   int per = kGPerXcd / nMb * nMb;
   per = per > 0 ? per : nMb;
   const int gpx = per / nMb;
-  hipLaunchKernelGGL(k_lmhead_gemm, dim3(8 * per), dim3(kGWaves * kWave), 0, st,
-                     (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M, h->ntiles,
-                     U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
+  if (bm == 128)
+    hipLaunchKernelGGL((k_lmhead_gemm<128, 128>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
+                       (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
+                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
+  else
+    hipLaunchKernelGGL((k_lmhead_gemm<256, 256>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
+                       (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
+                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
   return hipGetLastError();
 }
 

@@ -88,6 +88,7 @@ hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, cons
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
 int gemm_units(const xp_handle* h, int M);
+int gemm_units_max(const xp_handle* h);
 bool lmhead_gemm_ok(const xp_handle* h, int M);
 hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,
                               hipStream_t st);
