@@ -15,8 +15,8 @@ namespace xp {
 
 // lseT[b][k] = log sum_v exp(T[b][k][v]) for sampled rows, k = 0..B, in two
 // steps: every workgroup reduces one chunk of kVChunk entries of a row to
-// (max, sum of exp(T - max) in fp64), then one thread per row merges the
-// chunks in order.
+// (max, sum of exp(T - max)), the exponentials in fp32 and the sums in fp64;
+// then one wave per row merges the chunks in a fixed order.
 __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ tl, int B, int V,
                                                       const uint8_t* __restrict__ temp,
                                                       double* __restrict__ part) {
@@ -42,7 +42,7 @@ __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ 
   m = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
   double acc = 0.0;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) acc += x[i] == -INFINITY ? 0.0 : exp((double)x[i] - (double)m);
+  for (int i = 0; i < PER; ++i) acc += x[i] == -INFINITY ? 0.0 : (double)expf(x[i] - m);
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) acc += __shfl_xor(acc, o, kWave);
   if (lane == 0) sd[wave] = acc;
@@ -54,16 +54,21 @@ __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ 
   }
 }
 
-__global__ void k_vtarget_comb(int batch, int B, int nc, const uint8_t* __restrict__ temp,
-                               const double* __restrict__ part, double* __restrict__ lseT) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= batch * (B + 1) || temp[i / (B + 1)] == 0) return;
+__global__ __launch_bounds__(64) void k_vtarget_comb(int B, int nc, const uint8_t* __restrict__ temp,
+                                                     const double* __restrict__ part,
+                                                     double* __restrict__ lseT) {
+  const int i = blockIdx.x, lane = threadIdx.x;           // one wave per row
+  if (temp[i / (B + 1)] == 0) return;
   const double* q = part + (size_t)i * nc * 2;
-  double m = q[0];
-  for (int c = 1; c < nc; ++c) m = fmax(m, q[2 * c]);
+  double m = -INFINITY;
+  for (int c = lane; c < nc; c += kWave) m = fmax(m, q[2 * c]);
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) m = fmax(m, __shfl_xor(m, o, kWave));
   double sum = 0.0;
-  for (int c = 0; c < nc; ++c) sum += q[2 * c + 1] > 0.0 ? q[2 * c + 1] * exp(q[2 * c] - m) : 0.0;
-  lseT[i] = m + log(sum);
+  for (int c = lane; c < nc; c += kWave) sum += q[2 * c + 1] > 0.0 ? q[2 * c + 1] * exp(q[2 * c] - m) : 0.0;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o, kWave);
+  if (lane == 0) lseT[i] = m + log(sum);
 }
 
 // l = s (+ W_r z) for position p at vocabulary row v, through the Read tile of
@@ -226,56 +231,82 @@ __device__ __forceinline__ double wave_scan_d(double x, int lane) {
   return x;
 }
 
-// One wave per sampled sequence: crossing unit, then an in-order rescan.
+// One workgroup of 8 waves per sampled sequence: each wave sums the unit
+// masses of a contiguous range of units (in-order fp64 wave scans), the wave
+// totals are added in wave order; the first wave whose running total passes
+// u Z redoes its scans (same arithmetic) to find the crossing unit and
+// rescans that unit's rows in vocabulary order.
+constexpr int kVfWaves = 8;
+
 template <typename T>
-__global__ __launch_bounds__(64) void k_vfinal(
+__global__ __launch_bounds__(kVfWaves * kWave) void k_vfinal(
     int batch, int B, int V, int M, int with_read, int ntiles, int U,
     const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
     const float* __restrict__ tl, const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
     const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
     const double* __restrict__ vmass, const float* __restrict__ u_res,
     int32_t* __restrict__ out_next) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+  const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (temp == nullptr || temp[b] == 0) return;
+  __shared__ double wt[2][kVfWaves];
   const int k = vpos[b];
   bool resid = k < B;
   const int p = b * B + (k < B ? k : 0);
-  // residual with no mass falls back to p (component 1)
-  int comp = 0;
-  {
+  const int ua = (int)((int64_t)U * wave / kVfWaves), ub = (int)((int64_t)U * (wave + 1) / kVfWaves);
+  auto mass = [&](int i, int comp) {
+    return i < ub ? vmass[((size_t)i * batch + b) * 2 + comp] : 0.0;
+  };
+  // per-wave totals of both components (residual, plain p)
+#pragma unroll
+  for (int comp = 0; comp < 2; ++comp) {
     double c = 0.0;
-    for (int base = 0; base < U; base += 64) {
-      const int i = base + lane;
-      const double w = i < U ? vmass[((size_t)i * batch + b) * 2] : 0.0;
-      c += __shfl(wave_scan_d(w, lane), 63, kWave);
-    }
-    if (!(c > 0.0)) comp = 1;
+    for (int base = ua; base < ub; base += 64) c += __shfl(wave_scan_d(mass(base + lane, comp), lane), 63, kWave);
+    if (lane == 0) wt[comp][wave] = c;
   }
+  __syncthreads();
+  // residual with no mass falls back to p (component 1)
+  double tot0 = 0.0;
+#pragma unroll
+  for (int w = 0; w < kVfWaves; ++w) tot0 += wt[0][w];
+  const int comp = tot0 > 0.0 ? 0 : 1;
   const bool use_resid = resid && comp == 0;
-  double carry = 0.0;
-  for (int base = 0; base < U; base += 64) {
-    const int i = base + lane;
-    const double w = i < U ? vmass[((size_t)i * batch + b) * 2 + comp] : 0.0;
-    carry += __shfl(wave_scan_d(w, lane), 63, kWave);
+  double Zs = 0.0, start = 0.0;
+#pragma unroll
+  for (int w = 0; w < kVfWaves; ++w) {
+    if (w == wave) start = Zs;
+    Zs += wt[comp][w];
   }
-  const double target = (double)u_res[b] * carry;
-  double run = 0.0, pre = 0.0;
-  int ustar = U - 1;
-  for (int base = 0; base < U; base += 64) {
-    const int i = base + lane;
-    const double w = i < U ? vmass[((size_t)i * batch + b) * 2 + comp] : 0.0;
-    const double tot = run + wave_scan_d(w, lane);
-    const unsigned long long hit = __ballot(i < U && tot > target);
+  const double target = (double)u_res[b] * Zs;
+  int wstar = kVfWaves - 1;
+  while (wstar > 0 && (int64_t)U * wstar / kVfWaves >= (int64_t)U * (wstar + 1) / kVfWaves) --wstar;
+  {
+    double run = 0.0;
+#pragma unroll
+    for (int w = 0; w < kVfWaves; ++w) {
+      if (run + wt[comp][w] > target) {
+        wstar = w;
+        break;
+      }
+      run += wt[comp][w];
+    }
+  }
+  if (wave != wstar) return;
+  int ustar = ub - 1;
+  double carry = 0.0, pre = start;
+  for (int base = ua; base < ub; base += 64) {
+    const double incl = wave_scan_d(mass(base + lane, comp), lane);
+    const double tot = start + (carry + incl);
+    const unsigned long long hit = __ballot(base + lane < ub && tot > target);
     if (hit) {
       const int first = __ffsll((long long)hit) - 1;
       const double prev = __shfl_up(tot, 1, kWave);
-      const double excl = lane == 0 ? run : prev;
+      const double excl = lane == 0 ? start + carry : prev;
       ustar = base + first;
       pre = __shfl(excl, first, kWave);
       break;
     }
-    run = __shfl(tot, 63, kWave);
-    pre = run;
+    carry += __shfl(incl, 63, kWave);
+    pre = start + carry;
   }
   const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
   const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
@@ -337,8 +368,8 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
     hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1, batch), dim3(256), 0, st, tl, h->B,
                        h->V, temp, h->ws.vpart);
     const int rows = batch * (h->B + 1);
-    hipLaunchKernelGGL(k_vtarget_comb, dim3((rows + 255) / 256), dim3(256), 0, st, batch, h->B, nc,
-                       temp, h->ws.vpart, h->ws.vstat);
+    hipLaunchKernelGGL(k_vtarget_comb, dim3(rows), dim3(kWave), 0, st, h->B, nc, temp,
+                       h->ws.vpart, h->ws.vstat);
   }
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
                      draft, temp, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
@@ -349,7 +380,7 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
                        dim3(kReadWaves * kWave), 0, st, batch, h->B, h->V, M, with_read,
                        h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s, M,
                        (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vmass);
-    hipLaunchKernelGGL((k_vfinal<T>), dim3(batch), dim3(64), 0, st, batch, h->B, h->V, M,
+    hipLaunchKernelGGL((k_vfinal<T>), dim3(batch), dim3(kVfWaves * kWave), 0, st, batch, h->B, h->V, M,
                        with_read, h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s,
                        M, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
                        h->ws.vmass, ures, out_next);
