@@ -111,6 +111,15 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
   const int rw = (h->ntiles + kReadWaves - 1) / kReadWaves;
   h->read_wgs = rw < h->cus ? rw : h->cus;
   h->read_units = h->read_wgs * kReadWaves;
+  // the temperature-1 selection scans at most 4096 units per position and
+  // rescans Read units of at most 8 tiles
+  if (h->read_units > 4096 || gemm_units_max(h) > 4096 || h->lm_chunks > 4096 ||
+      (h->ntiles + h->read_units - 1) / h->read_units > 8) {
+    const int V = w->V;
+    delete h;
+    return fail(nullptr, XP_EUNSUPPORTED, "V=%d: vocabularies above %d rows are not built", V,
+                8 * 16 * 8 * 256);
+  }
 
   // workspace layout: one allocation, 256-byte aligned slices
   const size_t es = w->dtype == XP_BF16 ? 2 : 4;

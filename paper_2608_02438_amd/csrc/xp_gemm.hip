@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
       st = stat_merge(st, o);
       if (lk == 0 && pact) {
         keys[(size_t)hu * M + p] = best;
-        if (psample) stats[(size_t)hu * M + p] = st;
+        if (psample) stats[(size_t)p * U2 + hu] = st;
       }
     }
 #pragma unroll

@@ -30,7 +30,7 @@ struct Workspace {
   void* z = nullptr;          // [Mmax][r]     Trans output (dtype)
   int32_t* Y[2] = {nullptr, nullptr};   // [Mmax] iterates, ping-pong by pass parity
   uint64_t* keys = nullptr;   // [max chunks][Mmax]  greedy partials
-  Stat* stats = nullptr;      // [max units][Mmax]   sampling partials
+  Stat* stats = nullptr;      // [Mmax][units]   sampling partials (position-major)
   double* lse = nullptr;      // [Mmax]        log-sum-exp of the last pass (sampled rows)
   int32_t* iters = nullptr;   // [max_batch]
   int32_t* ctrl = nullptr;    // [0] converged-sequence count, [1] all-converged flag

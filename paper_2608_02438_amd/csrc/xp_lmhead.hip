@@ -88,7 +88,7 @@ __global__ __launch_bounds__(1024) void k_lmhead(
     }
     if (erow == 0 && ep < M) {
       keys[(size_t)u * M + ep] = best;
-      stats[(size_t)u * M + ep] = st;
+      stats[(size_t)ep * U + u] = st;
     }
   }
 }
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
     }
     if (erow == 0 && ep < M) {
       keys[(size_t)u * M + ep] = best;
-      stats[(size_t)u * M + ep] = st;
+      stats[(size_t)ep * U + u] = st;
     }
   }
 }
@@ -430,7 +430,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
     const int pp = p0 + threadIdx.x;
     if (pp < M) {
       keys[(size_t)u * M + pp] = bb;
-      stats[(size_t)u * M + pp] = ss;
+      stats[(size_t)pp * U + u] = ss;
     }
   }
 }

@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
     Stat o{__shfl_xor(st.m, m, kWave), __shfl_xor(st.s, m, kWave)};
     st = stat_merge(st, o);
   }
-  if (lane < 16 && sample) stats[(size_t)u * M + p] = st;
+  if (lane < 16 && sample) stats[(size_t)p * U + u] = st;
 
   if (lane < 16) kred[wave][lane] = best;
   __syncthreads();
@@ -324,7 +324,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
             q = stat_merge(q, o);
           }
           const int p = pw + kTile * pb + (lane & 15);
-          if (lane < 16 && sample[pb]) stats[(size_t)uc * M + p] = q;
+          if (lane < 16 && sample[pb]) stats[(size_t)p * U + uc] = q;
           st[pb] = stat_empty();
         }
       }

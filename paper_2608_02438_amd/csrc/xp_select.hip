@@ -33,73 +33,17 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// Mass of unit i for position p relative to the global max m (0 for empty units).
-__device__ __forceinline__ double unit_mass(const Stat* __restrict__ stats, int i, int U, int M,
-                                            int p, float m) {
-  if (i >= U) return 0.0;
-  const Stat s = stats[(size_t)i * M + p];
-  return s.s > 0.f ? (double)s.s * exp((double)s.m - (double)m) : 0.0;
-}
-
-// Rows of unit ustar for position p, scanned in vocabulary order from the
-// cumulative mass `pre` of the units before it, until the cumulative mass
-// exceeds `target` (one wave; every lane returns the row).  mode 0 reads
-// l = s, mode 1 recomputes l = s + W_r z with the stream's tile code.
-template <typename T>
-__device__ int rescan_unit(int mode, int p, int ustar, double pre, double target, float m,
-                           const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
-                           const T* __restrict__ Z, int M, int V, int ntiles, int U) {
-  const int lane = threadIdx.x & 63;
-  const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
-  const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
-  int chosen = -1, last_pos = -1;
-  double cum = pre;
-  for (int base = rlo; base < rhi; base += 64) {
-    const int row = base + lane;
-    float l = 0.f;
-    if (mode == 0) {
-      if (row < rhi) l = S[s_index(p, row, Ms)];
-    } else {
-      // four 16-row tiles cover these 64 rows; lane (r/4)*16 + p%16 holds row r
-      constexpr int NU = ReadTile<T>::NU;
-      u32x4 bf[NU], a[NU];
-      ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
-      float mine = 0.f;
-      const int rr = lane & 15, src = (rr >> 2) * 16 + (p & 15), comp = rr & 3;
-      const int pl = (p & ~15) + (lane & 15);
-      for (int tt = 0; tt < 4; ++tt) {
-        const int t = (base - rlo) / kTile + tlo + tt;
-        if (t >= thi) break;                         // wave-uniform
-        ReadTile<T>::load_w(W_r, V, t, lane, a);
-        const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, pl, pl < M, t, lane));
-        const float c0 = __shfl(acc[0], src, kWave), c1 = __shfl(acc[1], src, kWave);
-        const float c2 = __shfl(acc[2], src, kWave), c3 = __shfl(acc[3], src, kWave);
-        const float v = comp == 0 ? c0 : comp == 1 ? c1 : comp == 2 ? c2 : c3;
-        if ((lane >> 4) == tt) mine = v;
-      }
-      if (row < rhi) l = mine;
-    }
-    const double w = (row < rhi) ? exp((double)l - (double)m) : 0.0;
-    const double tot = cum + wave_incl_scan(w, lane);
-    const unsigned long long hit = __ballot(row < rhi && tot > target);
-    const unsigned long long nz = __ballot(row < rhi && w > 0.0);
-    if (nz) last_pos = base + 63 - __clzll((long long)nz);
-    if (hit) {
-      chosen = base + __ffsll((long long)hit) - 1;
-      break;
-    }
-    cum = __shfl(tot, 63, kWave);
-  }
-  if (chosen < 0) chosen = last_pos >= 0 ? last_pos : rlo;   // rounding left no crossing
-  return chosen;
-}
-
 // Inverse-CDF selection at temperature 1, one workgroup per position (rows at
 // temperature 0, and every row of a batch that is at its fixed point, return
 // at once).  mode 0: the seed Y^(0) from the base logits (with caller seeds
 // only the log-sum-exp is kept); mode 1: the selection of a Jacobi pass.  The
 // chosen row goes to Ynew, where the selection kernel that follows picks it up.
+// Every wave loads all of its unit partials at once, and the crossing unit's
+// logits are recomputed by one wave per tile into LDS before one wave scans
+// them, so a selection costs a few memory round trips.
 constexpr int kSmpWaves = 8;
+constexpr int kSmpChunks = 8;        // 64-unit chunks per wave: up to 4096 units
+constexpr int kSmpRows = 128;        // rows of the largest unit (8 tiles)
 
 template <typename T>
 __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
@@ -115,12 +59,23 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ float wmax[kSmpWaves];
   __shared__ double wtot[kSmpWaves];
+  __shared__ int s_ustar;
+  __shared__ double s_pre;
+  __shared__ float lrow[kSmpRows];
 
-  float m = -INFINITY;
-  for (int i = threadIdx.x; i < U; i += kSmpWaves * kWave) {
-    const Stat q = stats[(size_t)i * M + p];
-    if (q.s > 0.f) m = fmaxf(m, q.m);
+  // wave w owns the units [ua, ub) (in order), all loaded at once
+  const int ua = (int)((int64_t)U * wave / kSmpWaves), ub = (int)((int64_t)U * (wave + 1) / kSmpWaves);
+  Stat q[kSmpChunks];
+#pragma unroll
+  for (int j = 0; j < kSmpChunks; ++j) {
+    const int i = ua + 64 * j + lane;
+    q[j] = stats[(size_t)p * U + (i < ub ? i : (ub > 0 ? ub - 1 : 0))];
+    if (i >= ub) q[j] = stat_empty();
   }
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kSmpChunks; ++j)
+    if (q[j].s > 0.f) m = fmaxf(m, q[j].m);
   m = wave_max(m);
   if (lane == 0) wmax[wave] = m;
   __syncthreads();
@@ -128,13 +83,15 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
 #pragma unroll
   for (int w = 1; w < kSmpWaves; ++w) m = fmaxf(m, wmax[w]);
 
-  // wave w sums the units [ua, ub) in order
-  const int ua = (int)((int64_t)U * wave / kSmpWaves), ub = (int)((int64_t)U * (wave + 1) / kSmpWaves);
-  auto mass = [&](int i) { return i < ub ? unit_mass(stats, i, U, M, p, m) : 0.0; };
+  // unit masses sum_u e^{max_u - m} in fp64; in-order wave scans per chunk
+  double incl[kSmpChunks], carry_before[kSmpChunks];
   double carry = 0.0;
-  for (int base = ua; base < ub; base += 64) {
-    const double incl = wave_incl_scan(mass(base + lane), lane);
-    carry += __shfl(incl, 63, kWave);
+#pragma unroll
+  for (int j = 0; j < kSmpChunks; ++j) {
+    const double w = q[j].s > 0.f ? (double)q[j].s * exp((double)q[j].m - (double)m) : 0.0;
+    incl[j] = wave_incl_scan(w, lane);
+    carry_before[j] = carry;
+    if (ua + 64 * j < ub) carry += __shfl(incl[j], 63, kWave);
   }
   if (lane == 0) wtot[wave] = carry;
   __syncthreads();
@@ -162,30 +119,73 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
       run += wtot[w];
     }
   }
-  if (wave != wstar) return;
-  // redo this wave's scans (same arithmetic) to find the crossing unit;
-  // when rounding leaves none, the wave's last unit is rescanned from the
-  // wave's total and yields its last row of nonzero mass
-  int ustar = ub - 1;
-  carry = 0.0;
-  double pre = start + carry;
-  for (int base = ua; base < ub; base += 64) {
-    const double incl = wave_incl_scan(mass(base + lane), lane);
-    const double tot = start + (carry + incl);
-    const unsigned long long hit = __ballot(base + lane < ub && tot > target);
+  if (wave == wstar) {
+    // the crossing unit within this wave's range, from the same scans; when
+    // rounding leaves none, the wave's last unit is rescanned from the wave's
+    // total and yields its last row of nonzero mass
+    int ustar = ub - 1;
+    double pre = start + carry;
+    bool found = false;
+#pragma unroll
+    for (int j = 0; j < kSmpChunks; ++j) {
+      const int base = ua + 64 * j;
+      const double tot = start + (carry_before[j] + incl[j]);
+      const unsigned long long hit = __ballot(!found && base + lane < ub && tot > target);
+      if (hit) {
+        const int first = __ffsll((long long)hit) - 1;
+        const double prev = __shfl_up(tot, 1, kWave);
+        const double excl = lane == 0 ? start + carry_before[j] : prev;
+        ustar = base + first;
+        pre = __shfl(excl, first, kWave);
+        found = true;
+      }
+    }
+    if (lane == 0) {
+      s_ustar = ustar;
+      s_pre = pre;
+    }
+  }
+  __syncthreads();
+  const int ustar = s_ustar;
+  const int tlo = unit_tile_lo(ustar, ntiles, U), thi = unit_tile_lo(ustar + 1, ntiles, U);
+  const int rlo = tlo * kTile, rhi = min(V, thi * kTile);
+  // logits of the unit's rows: mode 1 recomputes l = s + W_r z with the
+  // stream's tile code, one wave per tile (a unit of a Read partition has at
+  // most kSmpRows / 16 tiles); mode 0 reads s while scanning
+  if (mode == 1 && wave < thi - tlo) {
+    constexpr int NU = ReadTile<T>::NU;
+    u32x4 bf[NU], a[NU];
+    const int t = tlo + wave;
+    ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
+    ReadTile<T>::load_w(W_r, V, t, lane, a);
+    const int pl = (p & ~15) + (lane & 15);
+    const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, pl, pl < M, t, lane));
+    if ((lane & 15) == (p & 15)) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lrow[kTile * wave + 4 * (lane >> 4) + i] = acc[i];
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  // scan the rows in vocabulary order from the mass of the units before
+  int chosen = -1, last_pos = -1;
+  double cum = s_pre;
+  for (int base = rlo; base < rhi; base += 64) {
+    const int row = base + lane;
+    const float l = row < rhi ? (mode == 0 ? S[s_index(p, row, Ms)] : lrow[row - rlo]) : 0.f;
+    const double w = (row < rhi) ? exp((double)l - (double)m) : 0.0;
+    const double tot = cum + wave_incl_scan(w, lane);
+    const unsigned long long hit = __ballot(row < rhi && tot > target);
+    const unsigned long long nz = __ballot(row < rhi && w > 0.0);
+    if (nz) last_pos = base + 63 - __clzll((long long)nz);
     if (hit) {
-      const int first = __ffsll((long long)hit) - 1;
-      const double prev = __shfl_up(tot, 1, kWave);
-      const double excl = (lane == 0) ? start + carry : prev;
-      ustar = base + first;
-      pre = __shfl(excl, first, kWave);
+      chosen = base + __ffsll((long long)hit) - 1;
       break;
     }
-    carry += __shfl(incl, 63, kWave);
-    pre = start + carry;
+    cum = __shfl(tot, 63, kWave);
   }
-  const int y = rescan_unit<T>(mode, p, ustar, pre, target, m, S, Ms, W_r, Z, M, V, ntiles, U);
-  if (lane == 0) Ynew[p] = y;
+  if (chosen < 0) chosen = last_pos >= 0 ? last_pos : rlo;   // rounding left no crossing
+  if (lane == 0) Ynew[p] = chosen;
 }
 
 // One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
