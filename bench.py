@@ -12,9 +12,12 @@ rates the dominant kernel, the LM-head launch (the stream kernel for one
 16-position block, the GEMM for more), by its algorithmic bytes (HBM-bound
 workloads) or flops (MFMA-bound ones, above the ridge) over its own duration,
 measured with HIP events recorded by the library on the stream the kernel runs
-on; `cpu_baseline` times the fp64 oracle on one block.
+on, against the published peak and against the peak measured on this GPU by
+the library's probes (an HBM read stream, an MFMA loop); `cpu_baseline` times
+the fp64 oracle on blocks of the workload for about 10 s (all threads), and
+`cpu_baseline_1thread` on one block with one thread.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu] [--no-peaks]
     python bench.py --copy-probe BYTES      (a plain device copy, for counter scaling)
 """
 import argparse
@@ -74,29 +77,93 @@ def copy_probe(nbytes: int):
     print(json.dumps({"copy_bytes": src.numel() * 4, "dispatches": 3}), flush=True)
 
 
-def cpu_baseline(wl, weights, inp):
-    """The oracle, as it stands, on one block of the workload (refine + verify)."""
+def cpu_baseline(wl, weights, inp, min_seconds=10.0, threads=None):
+    """The oracle, as it stands, on blocks of the workload (refine + verify of
+    batch rows 0, 1, ... in turn) until at least `min_seconds` have passed;
+    `threads` limits the BLAS pool (None: as configured)."""
+    import contextlib
+
     import numpy as np
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     import oracle as O
-    t0 = time.perf_counter()
-    P = O.Params.from_arrays(weights)
-    res = O.refine_batch(P, inp.h[:1], inp.anchor[:1], inp.temp[:1], inp.u_draft[:1], wl.K,
-                         seed_ids=None if inp.seed_ids is None else inp.seed_ids[:1],
-                         early_exit=False)
-    r0 = res.refined[0]
-    tid = inp.target_ids(r0.ids[None, :])
-    if inp.temp[0]:
-        O.verify_sample(r0.logits, r0.ids, inp.target_logits[0].astype(np.float64),
-                        inp.r_accept[0], float(inp.u_res[0]))
-    else:
-        O.verify_greedy(r0.ids, tid[0])
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": 1.0 / dt, "unit": "blocks/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"1 block (batch row 0) of {wl.name}: fp64 base readout, {wl.K} Jacobi "
-                      f"passes and verification, {dt:.1f} s"}
+    limit = threadpool_limits(limits=threads) if threads else contextlib.nullcontext()
+    with limit:
+        used = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        t0 = time.perf_counter()
+        P = O.Params.from_arrays(weights)
+        n = 0
+        while True:
+            b = n % wl.batch
+            sl = slice(b, b + 1)
+            res = O.refine_batch(P, inp.h[sl], inp.anchor[sl], inp.temp[sl], inp.u_draft[sl], wl.K,
+                                 seed_ids=None if inp.seed_ids is None else inp.seed_ids[sl],
+                                 early_exit=False)
+            r0 = res.refined[0]
+            if inp.temp[b]:
+                O.verify_sample(r0.logits, r0.ids, inp.target_logits[b].astype(np.float64),
+                                inp.r_accept[b], float(inp.u_res[b]))
+            else:
+                O.verify_greedy(r0.ids, inp.target_ids(r0.ids[None, :])[0])
+            n += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_seconds:
+                break
+    return {"value": n / dt, "unit": "blocks/s", "cores": int(used), "kind": "oracle",
+            "sample": f"{n} block(s) of {wl.name} (batch rows in turn): fp64 base readout, "
+                      f"{wl.K} Jacobi passes and verification, {dt:.1f} s including the fp64 "
+                      f"weight conversion",
+            "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def measured_peaks(lib_probe_read, lib_probe_mfma):
+    """What this GPU delivers on the two resources: HBM read bandwidth (a 2 GiB
+    stream, best of three launch shapes) and the bf16 MFMA rate on random
+    operands (8 independent 32x32x16 chains per wave, 2048 workgroups)."""
+    import numpy as np
+    import torch
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
+    nbytes = 2 << 30
+    buf = torch.randint(-2**31, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device="cuda")
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    gbs = max(nbytes / timed(lambda: lib_probe_read(buf, out, wgs)) / 1e9
+              for wgs in (1024, 2048, 4096))
+    del buf
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((8, 64, 2, 8)).astype(np.float32)
+    bits = ((x.view(np.uint32).astype(np.uint64) + 0x7FFF + ((x.view(np.uint32) >> 16) & 1))
+            >> 16).astype(np.uint16)
+    ops = torch.from_numpy(bits.view(np.int16)).cuda()
+    wgs, iters = 2048, 2000
+    mout = torch.empty(wgs * 4 * 64 * 16, dtype=torch.float32, device="cuda")
+    t = timed(lambda: lib_probe_mfma(ops, wgs, iters, mout))
+    tfs = wgs * 4 * iters * 8 * 32768 / t / 1e12
+    return {"hbm_read_GBs": gbs, "mfma_bf16_TFs": tfs,
+            "how": "xp_probe_hbm_read over 2 GiB (best of 1024/2048/4096 workgroups, each "
+                   "streaming a contiguous range); xp_probe_mfma_bf16, 2048 workgroups x 4 "
+                   "waves (2 per SIMD) x 8 chains x 2000 v_mfma_f32_32x32x16_bf16 on random "
+                   "bf16 operands"}
 
 
 def k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout):
@@ -138,6 +205,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3-8b-bf16-B16-b1-greedy")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measured HBM and MFMA peaks")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES")
     ap.add_argument("--k-sweep", action="store_true",
                     help="time refine + verify for K = 1..8 passes, fixed K and with the "
@@ -206,11 +275,21 @@ def main():
     ref.timing_enable(("lmhead",), capacity=max(args.steps, 1))
     torch.cuda.synchronize()
     log(f"[bench] timing {args.steps} steps")
+    # up to 5 rounds of equal length inside the timed steps, each bracketed by
+    # events on the stream the steps run on (the mean of the rounds and the
+    # fastest are reported beside the wall-clock figure)
+    nr = min(5, args.steps)
+    bounds = [args.steps * i // nr for i in range(nr + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nr + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if i in bounds:
+            evs[bounds.index(i)].record()
         step()
+    evs[nr].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    rounds = [evs[j].elapsed_time(evs[j + 1]) / (bounds[j + 1] - bounds[j]) for j in range(nr)]
     tm = ref.timing_read()
     ref.timing_enable((), 1)
     elapsed = t1 - t0
@@ -240,6 +319,13 @@ def main():
                           "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)"}
     roof.update({"traffic": committed_traffic(wl.name), "algorithmic_bytes_per_launch": lm_bytes,
                  "launch_us": lm_us})
+    if not args.no_peaks:
+        from paper_2608_02438_amd.xpress import probe_hbm_read, probe_mfma_bf16
+        log("[bench] measured peaks (HBM read stream, MFMA loop)")
+        mp = measured_peaks(probe_hbm_read, probe_mfma_bf16)
+        peak = mp["mfma_bf16_TFs"] if roof["bound"] == "mfma" else mp["hbm_read_GBs"]
+        roof.update({"measured_peak": peak, "frac_of_measured": achieved / peak,
+                     "measured_peaks": mp})
     n_acc = vout[0].cpu().numpy()
     log(f"[bench] {ms_step:.3f} ms/step, LM head {lm_us:.1f} us "
         f"({achieved:.0f} {roof['unit']}, {100 * roof['frac']:.1f}% of peak)")
@@ -256,11 +342,16 @@ def main():
         "roofline": roof,
         "refined_tokens_per_s": blocks_s * wl.B,
         "stage_ms_per_step": {k: v[0] / max(1, 3) for k, v in breakdown.items()},
+        "rounds_ms_per_step": rounds,
+        "ms_per_step_rounds_mean": sum(rounds) / len(rounds),
+        "ms_per_step_rounds_min": min(rounds),
         "accepted_mean": float(np.mean(n_acc)),
     }
     if not args.no_cpu:
-        log("[bench] CPU oracle baseline (one block)")
+        log("[bench] CPU oracle baseline (all threads)")
         line["cpu_baseline"] = cpu_baseline(wl, weights, inp)
+        log("[bench] CPU oracle baseline (one thread)")
+        line["cpu_baseline_1thread"] = cpu_baseline(wl, weights, inp, min_seconds=0.0, threads=1)
     else:
         line["cpu_baseline"] = None
     ref.close()

@@ -32,6 +32,7 @@
 #ifndef XPRESS_H
 #define XPRESS_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -189,6 +190,36 @@ xp_status xp_timing_read(xp_handle* h, float* ms_total, int32_t* pairs);
  * (host).  Synchronizes `stream`.
  */
 xp_status xp_device_errors(xp_handle* h, uint32_t* out, void* stream);
+
+/*
+ * Measurement probes (not part of the method).  They give the measured peaks
+ * that roofline fractions are also quoted against: the paper reports its
+ * kernels' time on its own hardware (evaluation section, latency table), and a
+ * fraction of a published peak says little without the attainable one.
+ *
+ * xp_probe_hbm_read: streams `bytes` (a multiple of 16) of the device buffer
+ * `buf` (16-byte aligned) once with 16-byte non-temporal loads, `workgroups`
+ * workgroups of 256 threads each taking a contiguous range, and writes the sum of its
+ * 32-bit words modulo 2^32 to the device word *out_sum (cleared first by the
+ * call).  Bandwidth = bytes / the launch's duration.
+ *
+ * xp_probe_mfma_bf16: `workgroups` workgroups of 4 waves; every wave runs 8
+ * independent accumulator chains of `iters` v_mfma_f32_32x32x16_bf16
+ * operations, chain j on the register operands operands[j][lane][0] (A, 16
+ * bytes: 8 bf16 of row lane % 32, k = 8 (lane / 32) .. + 8) and
+ * operands[j][lane][1] (B, the same for column lane % 32), i.e. a device
+ * array of 8 x 64 x 2 x 16 bytes.  Wave w (global index) writes the sum of its
+ * 8 accumulators to out[w][lane][16] (fp32; element i of lane l is
+ * D[8 (i / 4) + 4 (l / 32) + i % 4][l % 32]), so out must hold workgroups x 4
+ * x 64 x 16 floats.  Work = workgroups x 4 x iters x 8 x 32768 flops.
+ *
+ * Both return XP_EINVAL for null or misaligned pointers and out-of-range
+ * sizes, before any HIP call, and XP_EHIP if the launch fails.
+ */
+xp_status xp_probe_hbm_read(const void* buf, size_t bytes, uint32_t* out_sum, int32_t workgroups,
+                            void* stream);
+xp_status xp_probe_mfma_bf16(const void* operands, int32_t workgroups, int32_t iters, float* out,
+                             void* stream);
 
 #ifdef __cplusplus
 }

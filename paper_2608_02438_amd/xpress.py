@@ -23,7 +23,7 @@ XP_DEVERR_TOKEN = 1
 
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
-           "xp_timing_read")
+           "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16")
 STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
 
 
@@ -71,6 +71,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_timing_enable.restype = i32
     L.xp_timing_read.argtypes = [vp, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
     L.xp_timing_read.restype = i32
+    L.xp_probe_hbm_read.argtypes = [vp, ctypes.c_size_t, vp, i32, vp]
+    L.xp_probe_hbm_read.restype = i32
+    L.xp_probe_mfma_bf16.argtypes = [vp, i32, i32, vp, vp]
+    L.xp_probe_mfma_bf16.restype = i32
     _lib = L
     return L
 
@@ -229,3 +233,28 @@ def refiner_from_arrays(weights: Dict[str, np.ndarray], H, r, V, B, max_batch, d
     """Upload stored weights (bf16 bits or float32) and create a Refiner."""
     return Refiner({n: device_tensor(weights[n], device) for n in WEIGHT_NAMES}, H, r, V, B,
                    max_batch)
+
+
+def _check(st: int, what: str):
+    if st != XP_OK:
+        raise XpError(st, what)
+
+
+def probe_hbm_read(buf, out_sum, workgroups: int, stream=None):
+    """Launch the HBM read probe over the whole of `buf` (a contiguous device
+    tensor); `out_sum` (a device int32/uint32 tensor of one element) receives
+    the sum of its 32-bit words modulo 2^32."""
+    L = load_library()
+    nbytes = buf.numel() * buf.element_size()
+    _check(L.xp_probe_hbm_read(_ptr(buf), nbytes, _ptr(out_sum), workgroups, _stream(stream)),
+           "xp_probe_hbm_read")
+
+
+def probe_mfma_bf16(operands, workgroups: int, iters: int, out, stream=None):
+    """Launch the bf16 MFMA probe; `operands` holds 8 x 64 x 2 x 16 bytes
+    (8 x 64 x 2 x 8 bf16), `out` workgroups x 4 x 64 x 16 floats."""
+    L = load_library()
+    assert operands.numel() * operands.element_size() == 8 * 64 * 2 * 16
+    assert out.numel() >= workgroups * 4 * 64 * 16
+    _check(L.xp_probe_mfma_bf16(_ptr(operands), workgroups, iters, _ptr(out), _stream(stream)),
+           "xp_probe_mfma_bf16")

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     src = open(os.path.join(ROOT, "include", "xpress.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(xp_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(xp_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_declares_the_boundary():
@@ -76,3 +76,16 @@ def test_status_strings():
     L = X.load_library()
     assert L.xp_status_string(X.XP_EHIP) == b"XP_EHIP"
     assert L.xp_status_string(X.XP_OK) == b"XP_OK"
+
+
+def test_probes_reject_bad_arguments_without_a_gpu():
+    L = X.load_library()
+    assert L.xp_probe_hbm_read(None, 16, 0x1000, 1, None) == X.XP_EINVAL
+    assert L.xp_probe_hbm_read(0x1000, 24, 0x1000, 1, None) == X.XP_EINVAL
+    assert L.xp_probe_hbm_read(0x1008, 16, 0x1000, 1, None) == X.XP_EINVAL
+    assert L.xp_probe_hbm_read(0x1000, 16, None, 1, None) == X.XP_EINVAL
+    assert L.xp_probe_hbm_read(0x1000, 16, 0x1000, 0, None) == X.XP_EINVAL
+    assert L.xp_probe_mfma_bf16(None, 1, 1, 0x1000, None) == X.XP_EINVAL
+    assert L.xp_probe_mfma_bf16(0x1000, 0, 1, 0x1000, None) == X.XP_EINVAL
+    assert L.xp_probe_mfma_bf16(0x1000, 1, -1, 0x1000, None) == X.XP_EINVAL
+    assert L.xp_probe_mfma_bf16(0x1000, 1, 1, None, None) == X.XP_EINVAL
