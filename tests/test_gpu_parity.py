@@ -127,6 +127,19 @@ def test_early_exit_run_to_run_and_batch_invariance():
     np.testing.assert_allclose(out.logits.cpu().numpy()[0], a.logits[2], rtol=1e-5, atol=1e-4)
 
 
+@pytest.mark.parametrize("batch,temp", [(5, "mixed"), (20, "mixed"), (20, "greedy")])
+def test_lmhead_gemm_and_read_multi_ragged_positions(batch, temp):
+    # 80 positions: the 128 x 128 GEMM tile and one read group of 128 with 48
+    # idle positions; 320 positions: two 256 x 256 GEMM position tiles (the
+    # second 64 of 256 used) and a read group of 3 x 128 positions (64 idle),
+    # over a vocabulary that ends inside a tile
+    _say(f"case: GEMM + read_multi, bf16 H=512 V=1000 B=16 batch={batch} temp={temp} K=6")
+    prob = custom_problem("bf16", H=512, V=1000, B=16, batch=batch, K=6, sigmas=STRESS,
+                          temp=temp, seed=11 + batch)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
 @pytest.mark.parametrize("B,batch", [(16, 4), (8, 3)])
 def test_fused_greedy_pass_matches_separate_kernels(B, batch):
     """All-greedy batches run selection + Fuse + Mix + W_1 as one kernel; an
