@@ -166,6 +166,23 @@ def measured_peaks(lib_probe_read, lib_probe_mfma):
                    "bf16 operands"}
 
 
+def read_per_pass(wl, breakdown):
+    """A7 (Read + Correct + the select partials) per launch, from the stage
+    events of the breakdown steps: algorithmic bytes W_r once, s once, z once;
+    flops 2 M r V."""
+    ms, n = breakdown["read"]
+    if n == 0:
+        return None
+    us = ms * 1e3 / n
+    es = 2 if wl.dtype == "bf16" else 4
+    M = wl.batch * wl.B
+    nbytes = wl.V * wl.r * es + M * wl.V * 4 + M * wl.r * es
+    flops = 2.0 * M * wl.r * wl.V
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"launch_us": us, "launches": n, "algorithmic_bytes": nbytes, "GB_s": gbs,
+            "frac_hbm_peak": gbs / HBM_PEAK_GBS, "TFLOP_s": flops / (us * 1e-6) / 1e12}
+
+
 def k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout):
     """Cost of K Jacobi passes (the latency-vs-K table of the paper's evaluation):
     ms per refine + verify at fixed K and with the early exit, the mean number of
@@ -342,6 +359,7 @@ def main():
         "roofline": roof,
         "refined_tokens_per_s": blocks_s * wl.B,
         "stage_ms_per_step": {k: v[0] / max(1, 3) for k, v in breakdown.items()},
+        "read_per_pass": read_per_pass(wl, breakdown),
         "rounds_ms_per_step": rounds,
         "ms_per_step_rounds_mean": sum(rounds) / len(rounds),
         "ms_per_step_rounds_min": min(rounds),
