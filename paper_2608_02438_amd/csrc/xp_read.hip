@@ -251,16 +251,24 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ Z, const float* __restrict__ S,
     int Ms, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B,
-    float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done) {
+    float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done,
+    int nwg, int ny) {
   static_assert(kReadWaves == 8, "one 1 KB load per wave fills a 16-row tile");
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   using RT = ReadTile<uint16_t>;
   constexpr int NU = RT::NU;
   constexpr int WSL = 512, SSL = kReadWaves * P * 64;          // 16-byte slots per stage
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = blockIdx.x, u_lo = g * kReadWaves, u_hi = u_lo + kReadWaves;
+  // workgroup b runs on XCD b % 8; the ny position groups of one read
+  // workgroup g are b = 8 (ny (g / 8) + y) + g % 8, y < ny: the same XCD at
+  // about the same time, so W_r tiles read by the first come from L2 for the
+  // others
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int g = (slot / ny) * 8 + xcd, py = slot - (slot / ny) * ny;
+  if (g >= nwg) return;                           // whole workgroup
+  const int u_lo = g * kReadWaves, u_hi = u_lo + kReadWaves;
   const int t0 = unit_tile_lo(u_lo, ntiles, U), n = unit_tile_lo(u_hi, ntiles, U) - t0;
-  const int pw = blockIdx.y * (kReadWaves * kTile * P) + wave * (kTile * P);
+  const int pw = py * (kReadWaves * kTile * P) + wave * (kTile * P);
   __shared__ u32x4 lds[kRmStages * (WSL + SSL)];                // [stage][W tile | s]
 
   u32x4 zf[P][NU];
@@ -415,29 +423,30 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     const int per = kReadWaves * kTile;
     int P = (M + per - 1) / per;
     P = P < 4 ? P : 4;
-    grid.y = (M + per * P - 1) / (per * P);
+    const int ny = (M + per * P - 1) / (per * P);
+    grid = dim3((h->read_wgs + 7) / 8 * 8 * ny);
     const uint16_t* Wr = (const uint16_t*)h->W_r;
     const uint16_t* Zb = (const uint16_t*)h->ws.z;
     switch (P) {
       case 1:
         hipLaunchKernelGGL((k_read_multi<1>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
         break;
       case 2:
         hipLaunchKernelGGL((k_read_multi<2>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
         break;
       case 3:
         hipLaunchKernelGGL((k_read_multi<3>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
         break;
       default:
         hipLaunchKernelGGL((k_read_multi<4>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
     }
     return hipGetLastError();
   }
