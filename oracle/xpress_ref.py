@@ -266,23 +266,24 @@ def inverse_cdf(w: np.ndarray, u: float):
     return y, float(min(t - lo, C[y] - t) / Z)
 
 
-def softmax_weights(l: np.ndarray) -> np.ndarray:
-    """exp(l_v - max l) in fp64 from the fp32-rounded logits."""
+def softmax_weights(l: np.ndarray, T: float = 1.0) -> np.ndarray:
+    """exp((l_v - max l) / T) in fp64 from the fp32-rounded logits: the
+    unnormalised softmax of the logits at temperature T > 0."""
     l32 = l.astype(np.float32).astype(F64)
-    return np.exp(l32 - l32.max())
+    return np.exp((l32 - l32.max()) / float(T))
 
 
-def select_sample(l: np.ndarray, u: float):
-    """Inverse-CDF sample of softmax(l) at the uniform u; returns (token, margin)."""
-    return inverse_cdf(softmax_weights(l), u)
+def select_sample(l: np.ndarray, u: float, T: float = 1.0):
+    """Inverse-CDF sample of softmax(l / T) at the uniform u; returns (token, margin)."""
+    return inverse_cdf(softmax_weights(l, T), u)
 
 
-def select(l: np.ndarray, sample: bool, u: float):
-    return select_sample(l, u) if sample else select_greedy(l)
+def select(l: np.ndarray, sample: bool, u: float, T: float = 1.0):
+    return select_sample(l, u, T) if sample else select_greedy(l)
 
 
-def softmax(l: np.ndarray) -> np.ndarray:
-    w = softmax_weights(l)
+def softmax(l: np.ndarray, T: float = 1.0) -> np.ndarray:
+    w = softmax_weights(l, T)
     return w / w.sum()
 
 
@@ -307,14 +308,15 @@ class Refined:
 
 def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
                  sample: bool = False, u=None, K: int = 6,
-                 early_exit: bool = True) -> Refined:
+                 early_exit: bool = True, T: float = 1.0) -> Refined:
     """Algorithm 1 for one sequence.
 
     Y^(0) is ``seed`` when given, otherwise each position's selection from the
     base logits s_k.  Pass j runs the refiner on Y^(j) (prefix x_0 = anchor,
     x_{k-1} = y^(j)_{k-1}), re-selects every position from s_k + delta_k in
     parallel, and stops once Y^(j+1) = Y^(j).  With ``early_exit`` False the
-    loop always runs K passes, which must not change the result.
+    loop always runs K passes, which must not change the result.  Sampled
+    sequences draw from softmax(l / T).
     """
     B = s_b.shape[0]
     u = np.zeros(B) if u is None else np.asarray(u, dtype=F64)
@@ -323,7 +325,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
         Y = np.asarray(seed, dtype=np.int64).copy()
         mg = np.full(B, np.inf)
     else:
-        sel = [select(s_b[k], sample, u[k]) for k in range(B)]
+        sel = [select(s_b[k], sample, u[k], T) for k in range(B)]
         Y = np.array([t for t, _ in sel], dtype=np.int64)
         mg = np.array([m for _, m in sel])
     traj, margins = [Y.copy()], [mg]
@@ -332,7 +334,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
         x_prev = np.concatenate([[anchor], Y[:-1]])
         delta, Z = refiner(P, st, x_prev)
         l = s_b + delta
-        sel = [select(l[k], sample, u[k]) for k in range(B)]
+        sel = [select(l[k], sample, u[k], T) for k in range(B)]
         Yn = np.array([t for t, _ in sel], dtype=np.int64)
         traj.append(Yn.copy())
         margins.append(np.array([m for _, m in sel]))
@@ -349,7 +351,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
 
 
 def sequential_decode(P: Params, s_b: np.ndarray, h_b, anchor: int,
-                      sample: bool = False, u=None) -> np.ndarray:
+                      sample: bool = False, u=None, T: float = 1.0) -> np.ndarray:
     """y*_k = select(s_k + delta_k(x_0, y*_1..y*_{k-1})) for k = 1..B, in order.
 
     Positions after k are filled with token 0; by the causal structure of the
@@ -362,11 +364,11 @@ def sequential_decode(P: Params, s_b: np.ndarray, h_b, anchor: int,
     for k in range(B):
         x_prev = np.concatenate([[anchor], Y[:-1]])
         delta, _ = refiner(P, st, x_prev)
-        Y[k], _ = select(s_b[k] + delta[k], sample, u[k])
+        Y[k], _ = select(s_b[k] + delta[k], sample, u[k], T)
     return Y
 
 
-def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u):
+def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u, T: float = 1.0):
     """One Jacobi pass from a given iterate: (new ids, margins, logits).
 
     Used to check a device trajectory decision by decision.
@@ -377,7 +379,7 @@ def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u):
     x_prev = np.concatenate([[anchor], np.asarray(Y_prev, dtype=np.int64)[:-1]])
     delta, _ = refiner(P, st, x_prev)
     l = s_b + delta
-    sel = [select(l[k], sample, u[k]) for k in range(B)]
+    sel = [select(l[k], sample, u[k], T) for k in range(B)]
     return (np.array([t for t, _ in sel], dtype=np.int64),
             np.array([m for _, m in sel]), l)
 
@@ -407,21 +409,21 @@ class Verified:
     resample_margin: float
 
 
-def verify_sample(q_logits, ids, p_logits, r_accept, u_res) -> Verified:
+def verify_sample(q_logits, ids, p_logits, r_accept, u_res, T: float = 1.0) -> Verified:
     """Speculative accept / reject of a sampled block (section 3.1).
 
     For k = 1..B: accept y_k iff r_k * q_k(y_k) <= p_k(y_k), where q_k is the
     refined distribution the draft token was sampled from and p_k the target
-    distribution after the same prefix.  At the first rejection the next token
-    is an inverse-CDF sample (at u_res) of max(0, p_k - q_k), or of p_k if that
-    residual has no mass.  If all B are accepted the bonus token is sampled
-    from p_{B+1}.
+    distribution after the same prefix, both at temperature T.  At the first
+    rejection the next token is an inverse-CDF sample (at u_res) of
+    max(0, p_k - q_k), or of p_k if that residual has no mass.  If all B are
+    accepted the bonus token is sampled from p_{B+1}.
     """
     B = len(ids)
     am = []
     for k in range(B):
-        q = softmax(q_logits[k])
-        p = softmax(p_logits[k])
+        q = softmax(q_logits[k], T)
+        p = softmax(p_logits[k], T)
         y = int(ids[k])
         rq = float(r_accept[k]) * q[y]
         am.append(abs(rq - p[y]) / max(p[y], rq))
@@ -431,7 +433,7 @@ def verify_sample(q_logits, ids, p_logits, r_accept, u_res) -> Verified:
                 res = p
             t, m = inverse_cdf(res, u_res)
             return Verified(n=k, next=t, accept_margins=np.array(am), resample_margin=m)
-    t, m = inverse_cdf(softmax(p_logits[B]), u_res)
+    t, m = inverse_cdf(softmax(p_logits[B], T), u_res)
     return Verified(n=B, next=t, accept_margins=np.array(am), resample_margin=m)
 
 
@@ -447,8 +449,9 @@ class BatchResult:
 
 
 def refine_batch(P: Params, h, anchor, temp, u_draft, K: int, seed_ids=None,
-                 seqs=None, early_exit: bool = True) -> BatchResult:
-    """Run Algorithm 1 on the chosen sequences of a batch (default: all)."""
+                 seqs=None, early_exit: bool = True, temperature=None) -> BatchResult:
+    """Run Algorithm 1 on the chosen sequences of a batch (default: all);
+    sampled sequences use temperature[b] (1 when None)."""
     bsz, B, H = h.shape
     seqs = list(range(bsz)) if seqs is None else list(seqs)
     s = base_logits(P.W_lm, h[seqs].reshape(len(seqs) * B, H)).reshape(len(seqs), B, -1)
@@ -457,5 +460,6 @@ def refine_batch(P: Params, h, anchor, temp, u_draft, K: int, seed_ids=None,
         out.refined.append(refine_block(
             P, s[i], h[b], int(anchor[b]),
             seed=None if seed_ids is None else seed_ids[b],
-            sample=bool(temp[b]), u=u_draft[b], K=K, early_exit=early_exit))
+            sample=bool(temp[b]), u=u_draft[b], K=K, early_exit=early_exit,
+            T=1.0 if temperature is None else float(temperature[b])))
     return out

@@ -232,17 +232,17 @@ def _all_stress(n):
         yield seed, stress_params(100 + seed, H=6, r=4, V=5, B=4)
 
 
-@pytest.mark.parametrize("sample", [False, True])
-def test_thm1_jacobi_pins_one_position_per_pass_and_reaches_sequential(sample):
+@pytest.mark.parametrize("sample,T", [(False, 1.0), (True, 1.0), (True, 0.5)])
+def test_thm1_jacobi_pins_one_position_per_pass_and_reaches_sequential(sample, T):
     long_traj = 0
     for seed, (P, h) in _all_stress(40):
         g = np.random.default_rng(seed)
         s = O.base_logits(P.W_lm, h)
         u = g.random(4)
-        ystar = O.sequential_decode(P, s, h, anchor=3, sample=sample, u=u)
+        ystar = O.sequential_decode(P, s, h, anchor=3, sample=sample, u=u, T=T)
         seed_ids = g.integers(0, 5, 4)
         res = O.refine_block(P, s, h, 3, seed=seed_ids, sample=sample, u=u, K=4,
-                             early_exit=False)
+                             early_exit=False, T=T)
         traj = res.traj_padded(4)
         for j in range(5):
             assert np.array_equal(traj[j][:j], ystar[:j])      # y_k^(j) = y*_k, k <= j
@@ -316,6 +316,32 @@ def test_select_sample_is_softmax_sampling():
     assert np.allclose(np.bincount(toks, minlength=6) / toks.size, p, atol=1e-4)
 
 
+@pytest.mark.parametrize("T", [0.3, 0.7, 2.5])
+def test_select_sample_at_temperature_is_tempered_softmax_sampling(T):
+    g = np.random.default_rng(12)
+    l = g.normal(0, 2, 6)
+    p = scipy.special.softmax(l.astype(np.float32).astype(np.float64) / T)
+    us = (np.arange(50000) + 0.5) / 50000
+    toks = np.array([O.select_sample(l, u, T)[0] for u in us])
+    assert np.allclose(np.bincount(toks, minlength=6) / toks.size, p, atol=1e-4)
+
+
+def test_low_temperature_sampling_is_the_argmax():
+    """T -> 0: all mass on the largest logit (gaps >= 0.08 against T = 1e-3)."""
+    g = np.random.default_rng(13)
+    for _ in range(50):
+        l = g.permutation(11) * 0.1 + g.uniform(-0.01, 0.01, 11)
+        for u in (0.001, 0.3, 0.999):
+            assert O.select_sample(l, u, 1e-3)[0] == int(np.argmax(l))
+
+
+def test_high_temperature_sampling_is_uniform():
+    """T -> infinity: every token has mass 1/V, so u picks floor(u V)."""
+    l = np.random.default_rng(14).normal(0, 1, 7)
+    for u in (np.arange(70) + 0.5) / 70:
+        assert O.select_sample(l, u, 1e9)[0] == int(np.floor(u * 7))
+
+
 # ------------------------------------------------------------ verification ----
 
 def test_verify_greedy_is_brute_force_longest_prefix():
@@ -336,14 +362,14 @@ def _cells(probs):
     return [(c[v], c[v + 1]) for v in range(len(probs)) if c[v + 1] > c[v]]
 
 
-def _exact_sd_law(P, h, s, anchor, table, B, V, m):
+def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0):
     """Law of the first m emitted tokens of one SD round + target continuation.
 
     Enumerates every cell of (u_draft, r_accept, u_res) exactly and evaluates
     the oracle at the cell's midpoint.  ``table[prefix]`` are target logits.
     """
     law = {}
-    p_of = lambda pre: scipy.special.softmax(table[tuple(pre)])
+    p_of = lambda pre: scipy.special.softmax(table[tuple(pre)] / T)
 
     def cont(prefix, prob):
         if len(prefix) >= m:
@@ -360,13 +386,13 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m):
             yield np.array(u_pre), prob
             return
         u_try = np.array(u_pre + [0.5] + [0.5] * (B - k - 1))
-        res = O.refine_block(P, s, h, anchor, sample=True, u=u_try, K=B)
-        q = O.softmax(res.logits[k])
+        res = O.refine_block(P, s, h, anchor, sample=True, u=u_try, K=B, T=T)
+        q = O.softmax(res.logits[k], T)
         for lo, hi in _cells(q):
             yield from draft_cells(k + 1, u_pre + [(lo + hi) / 2], prob * (hi - lo))
 
     for u, pu in draft_cells(0, [], 1.0):
-        res = O.refine_block(P, s, h, anchor, sample=True, u=u, K=B)
+        res = O.refine_block(P, s, h, anchor, sample=True, u=u, K=B, T=T)
         y = [int(t) for t in res.ids]
         plog = np.stack([table[tuple(y[:k])] for k in range(B + 1)])
 
@@ -375,10 +401,10 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m):
             if k == B:
                 pb = p_of(y)
                 for lo, hi in _cells(pb):
-                    v = O.verify_sample(res.logits, y, plog, r_pre + [0.5] * (B - k), (lo + hi) / 2)
+                    v = O.verify_sample(res.logits, y, plog, r_pre + [0.5] * (B - k), (lo + hi) / 2, T)
                     cont(y[:v.n] + [v.next], prob * (hi - lo))
                 return
-            q = O.softmax(res.logits[k])
+            q = O.softmax(res.logits[k], T)
             p = p_of(y[:k])
             a = min(1.0, p[y[k]] / q[y[k]])
             branch(k + 1, r_pre + [a / 2], prob * a)                  # accept cell
@@ -387,7 +413,7 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m):
                 resid = np.maximum(p - q, 0.0)
                 resid = resid / resid.sum()
                 for lo, hi in _cells(resid):
-                    v = O.verify_sample(res.logits, y, plog, rr, (lo + hi) / 2)
+                    v = O.verify_sample(res.logits, y, plog, rr, (lo + hi) / 2, T)
                     assert v.n == k
                     cont(y[:k] + [v.next], prob * (1 - a) * (hi - lo))
 
@@ -412,6 +438,27 @@ def test_speculative_verify_is_lossless_by_exact_enumeration(seed):
         target = 1.0
         for t in range(m):
             target *= scipy.special.softmax(table[x[:t]])[x[t]]
+        assert abs(law.get(x, 0.0) - target) < 1e-12
+
+
+@pytest.mark.parametrize("T", [0.6, 1.8])
+def test_speculative_verify_at_temperature_is_lossless_by_exact_enumeration(T):
+    """At temperature T the emitted tokens follow softmax(target / T) exactly."""
+    V, B = 3, 2
+    P, h = stress_params(210, H=5, r=3, V=V, B=B, we_sigma=2.0)
+    s = O.base_logits(P.W_lm, h)
+    g = np.random.default_rng(11)
+    table = {}
+    for n in range(B + 2):
+        for pre in itertools.product(range(V), repeat=n):
+            table[pre] = g.normal(0, 1.5, V).astype(np.float32).astype(np.float64)
+    m = B + 1
+    law = _exact_sd_law(P, h, s, 1, table, B, V, m, T=T)
+    assert abs(sum(law.values()) - 1.0) < 1e-12
+    for x in itertools.product(range(V), repeat=m):
+        target = 1.0
+        for t in range(m):
+            target *= scipy.special.softmax(table[x[:t]] / T)[x[t]]
         assert abs(law.get(x, 0.0) - target) < 1e-12
 
 
