@@ -55,6 +55,7 @@ typedef enum { XP_F32 = 0, XP_BF16 = 1 } xp_dtype;
 
 /* bits of the device error word */
 #define XP_DEVERR_TOKEN 1u  /* a token id outside [0, V) was read and replaced by 0 */
+#define XP_DEVERR_TEMPERATURE 2u  /* a sampled row's temperature was not finite and > 0; 1 was used */
 
 typedef struct xp_handle xp_handle;
 
@@ -115,7 +116,11 @@ const char* xp_status_string(xp_status s);
  *   anchor     [batch] int32           x_0, the token before the block
  *   seed_ids   [batch][B] int32 or NULL  Y^(0); NULL: select from the base logits
  *   temp       [batch] uint8 or NULL   per sequence 0 = greedy (argmax, ties to the
- *              lowest index), nonzero = temperature-1 sampling; NULL = all greedy
+ *              lowest index), nonzero = sampling; NULL = all greedy
+ *   temperature [batch] float or NULL  the temperature T > 0 of each sampled
+ *              sequence: it samples softmax(l / T) (greedy rows ignore it);
+ *              NULL = 1 for every sampled row.  A value that is not finite and
+ *              positive is replaced by 1 and sets XP_DEVERR_TEMPERATURE.
  *   u_draft    [batch][B] float in [0,1), required iff temp != NULL: the uniform of
  *              each position; a sampled position takes the smallest v whose
  *              cumulative softmax mass exceeds u (fixed across passes)
@@ -133,6 +138,7 @@ const char* xp_status_string(xp_status s);
 xp_status xp_refine_block(xp_handle* h, int32_t batch,
                           const void* hidden, const int32_t* anchor,
                           const int32_t* seed_ids, const uint8_t* temp,
+                          const float* temperature,
                           const float* u_draft, int32_t K, uint32_t flags,
                           int32_t* out_ids, int32_t* out_iters,
                           float* out_logits, int32_t* out_traj, void* stream);
@@ -147,7 +153,7 @@ xp_status xp_refine_block(xp_handle* h, int32_t batch,
  *                  (t_k is the target's choice after the draft prefix y_{<k});
  *                  always required (only greedy rows read it)
  *   target_logits  [batch][B+1][V] float: sampled rows' target logits after each
- *                  prefix (temperature 1); required iff temp != NULL
+ *                  prefix; required iff temp != NULL
  *   r_accept       [batch][B] float in [0,1), required iff temp != NULL
  *   u_resample     [batch] float in [0,1), required iff temp != NULL
  *   out_accept_len [batch] int32 n in [0, B] (the paper's tau counts n + 1)
@@ -155,7 +161,8 @@ xp_status xp_refine_block(xp_handle* h, int32_t batch,
  *                  the bonus token when all B are accepted
  * Greedy rows: n = longest prefix with y_i = t_i, next = t_{n+1}.
  * Sampled rows: accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k the refined
- * distribution of refine's last pass and p_k = softmax(target logits k); at the
+ * distribution of refine's last pass and p_k = softmax(target logits k / T),
+ * T the row's temperature given to that refine (section 3.1 at T > 0); at the
  * first rejection next is the inverse-CDF sample at u_resample of max(0, p_k - q_k)
  * (of p_k if that has no mass); if all are accepted next samples p_{B+1}.
  */

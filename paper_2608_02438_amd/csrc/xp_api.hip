@@ -151,6 +151,7 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
       {(void**)&ws.keys, nk * Mmax * 8},
       {(void**)&ws.stats, nu * Mmax * sizeof(Stat)},
       {(void**)&ws.lse, Mmax * 8},
+      {(void**)&ws.invT, (size_t)max_batch * 4},
       {(void**)&ws.iters, (size_t)max_batch * 4},
       {(void**)&ws.ctrl, 16},
       {(void**)&ws.err, 16},
@@ -281,7 +282,8 @@ extern "C" xp_status xp_timing_read(xp_handle* h, float* ms_total, int32_t* pair
 
 extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hidden,
                                      const int32_t* anchor, const int32_t* seed_ids,
-                                     const uint8_t* temp, const float* u_draft, int32_t K,
+                                     const uint8_t* temp, const float* temperature,
+                                     const float* u_draft, int32_t K,
                                      uint32_t flags, int32_t* out_ids, int32_t* out_iters,
                                      float* out_logits, int32_t* out_traj, void* stream) {
   if (!h) return XP_EINVAL;
@@ -301,7 +303,7 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
   h->state_valid = false;
   // All-greedy batches run the selection of pass j-1, Fuse, Mix and the first
   // Trans product of pass j as one kernel; the others use separate kernels.
-  XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, st));
+  XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, temp, temperature, st));
   XP_TIMED(XP_STAGE_LMHEAD, launch_lmhead(h, batch * h->B, hidden, temp, st));
   const bool fused = K > 0 && pass_fused_ok(h, temp);
   if (!fused)

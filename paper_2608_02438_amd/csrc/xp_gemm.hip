@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M,
     int ntiles, int U2, int nMb, int gpx, float* __restrict__ S, int Ms,
     uint64_t* __restrict__ keys, Stat* __restrict__ stats, const uint8_t* __restrict__ temp,
-    int B) {
+    int B, const float* __restrict__ invT) {
   constexpr int RW = BN / 2, PW = BM / 4;                          // rows, positions per wave
   constexpr int NA = RW / 32, NB = PW / 32;                        // 32 x 32 blocks per wave
   constexpr int WS = BN * kGK * 2 / 16, HS = BM * kGK * 2 / 16;    // slots per operand stage
@@ -164,11 +164,13 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     const int rbase = unit_tile_lo(hu, ntiles, U2) * kTile;
     const int nr = unit_tile_lo(hu + 1, ntiles, U2) * kTile - rbase;   // <= RW, multiple of 16
     bool psamp[NB];
+    float pit[NB];                                   // sampled rows: softmax(s / T)
     bool anyp = false;
 #pragma unroll
     for (int c = 0; c < NB; ++c) {
       const int p = p0 + wp * PW + c * 32 + lr;
       psamp[c] = p < M && load_flag(temp, (p < M ? p : M - 1) / B, W) != 0;
+      pit[c] = invT[(p < M ? p : M - 1) / B];
       anyp = anyp || psamp[c];
     }
     const bool any_sample = __ballot(anyp) != 0;
@@ -203,7 +205,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
             float x[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              x[e] = (rv && psample && rbase + rl + e < V) ? acc[a][c][4 * q + e] : -INFINITY;
+              x[e] = (rv && psample && rbase + rl + e < V) ? acc[a][c][4 * q + e] * pit[c] : -INFINITY;
             st = stat_add4(st, x[0], x[1], x[2], x[3]);
           }
         }
@@ -298,11 +300,13 @@ hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uin
   if (bm == 128)
     hipLaunchKernelGGL((k_lmhead_gemm<128, 128>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
                        (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
-                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
+                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B,
+                       h->ws.invT);
   else
     hipLaunchKernelGGL((k_lmhead_gemm<256, 256>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
                        (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
-                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B);
+                       h->ntiles, U2, nMb, gpx, h->ws.s, M, h->ws.keys, h->ws.stats, temp, h->B,
+                       h->ws.invT);
   return hipGetLastError();
 }
 

@@ -31,7 +31,8 @@ struct Workspace {
   int32_t* Y[2] = {nullptr, nullptr};   // [Mmax] iterates, ping-pong by pass parity
   uint64_t* keys = nullptr;   // [max chunks][Mmax]  greedy partials
   Stat* stats = nullptr;      // [Mmax][units]   sampling partials (position-major)
-  double* lse = nullptr;      // [Mmax]        log-sum-exp of the last pass (sampled rows)
+  double* lse = nullptr;      // [Mmax]        log-sum-exp of the last pass (sampled rows, l / T)
+  float* invT = nullptr;      // [max_batch]   1 / temperature of each sequence (1 if none)
   int32_t* iters = nullptr;   // [max_batch]
   int32_t* ctrl = nullptr;    // [0] converged-sequence count, [1] all-converged flag
   uint32_t* err = nullptr;    // device error word
@@ -78,7 +79,8 @@ namespace xp {
 
 // launchers (each returns hipGetLastError() of its launch)
 hipError_t launch_fold(xp_handle* h, hipStream_t st);
-hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t st);
+hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, const uint8_t* temp,
+                       const float* temperature, hipStream_t st);
 hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t* temp, hipStream_t st);
 hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
                          const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,

@@ -21,7 +21,7 @@ template <typename T, int NU>
 __global__ __launch_bounds__(1024) void k_lmhead(
     const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
     float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
-    const uint8_t* __restrict__ temp, int B) {
+    const uint8_t* __restrict__ temp, int B, const float* __restrict__ invT) {
   using MF = Mfma<T>;
   constexpr int EPB = 16 / sizeof(T);
   constexpr int KS = NU * MF::KU;
@@ -43,6 +43,7 @@ __global__ __launch_bounds__(1024) void k_lmhead(
   const int ep = p0 + epos;
   const bool eact = threadIdx.x < 256 && ep < M;
   const bool esample = eact && temp != nullptr && temp[ep / B] != 0;
+  const float eit = esample ? invT[ep / B] : 1.f;         // sampled rows: softmax(s / T)
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
 
@@ -70,7 +71,7 @@ __global__ __launch_bounds__(1024) void k_lmhead(
       if (eact && row < V) {
         S[s_index(ep, row, Ms)] = v;
         if (esample)
-          st = stat_merge(st, Stat{v, 1.f});
+          st = stat_merge(st, Stat{v * eit, 1.f});
         else
           best = umax64(best, argmax_key(v, (uint32_t)row));
       }
@@ -106,7 +107,7 @@ template <typename T, int NU>
 __global__ __launch_bounds__(1024) void k_lmhead_lds(
     const T* __restrict__ W, const T* __restrict__ X, int V, int H, int M, int ntiles, int U,
     float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
-    const uint8_t* __restrict__ temp, int B) {
+    const uint8_t* __restrict__ temp, int B, const float* __restrict__ invT) {
   using MF = Mfma<T>;
   constexpr int EPB = 16 / sizeof(T);
   constexpr int KS = NU * MF::KU;
@@ -133,6 +134,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
   const int ep = p0 + epos;
   const bool eact = threadIdx.x < 256 && ep < M;
   const bool esample = eact && temp != nullptr && temp[ep / B] != 0;
+  const float eit = esample ? invT[ep / B] : 1.f;         // sampled rows: softmax(s / T)
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
   int buf = 0;
@@ -163,7 +165,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_lds(
       if (eact && row < V) {
         S[s_index(ep, row, Ms)] = v;
         if (esample)
-          st = stat_merge(st, Stat{v, 1.f});
+          st = stat_merge(st, Stat{v * eit, 1.f});
         else
           best = umax64(best, argmax_key(v, (uint32_t)row));
       }
@@ -233,7 +235,7 @@ template <int PF>
 __global__ __launch_bounds__(1024) void k_lmhead_sk(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M, int ntiles,
     int U, float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
-    const uint8_t* __restrict__ temp, int B) {
+    const uint8_t* __restrict__ temp, int B, const float* __restrict__ invT) {
   using MF = Mfma<uint16_t>;
   __shared__ u32x4 lds[16 * kHChunks + kSkWaves * 128];   // h (128 KB) + transpose tiles (32 KB)
   u32x4* hl = lds;
@@ -253,6 +255,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   // other load), then h, then the first items of W_lm
   const int p_flag = p0 + (lane & 15);
   const int tvf = load_flag(temp, (p_flag < M ? p_flag : M - 1) / B, X);
+  const float pit = invT[(p_flag < M ? p_flag : M - 1) / B];   // sampled rows: softmax(s / T)
   asm volatile("" ::: "memory");
   // h: every thread issues its (at most 8) chunk loads at once; rows past M
   // are loaded from row M-1 and zeroed
@@ -310,7 +313,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool v = pact && row0 + i < V && psample;
-        const Stat nx = stat_merge(st, Stat{acc[i], 1.f});
+        const Stat nx = stat_merge(st, Stat{acc[i] * pit, 1.f});
         st.m = v ? nx.m : st.m;
         st.s = v ? nx.s : st.s;
       }
@@ -470,14 +473,14 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
       hipLaunchKernelGGL((k_lmhead_sk<kSkPF>), grid, dim3(kSkWaves * kWave), 0, st,
                          (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
                          h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
-                         h->B);
+                         h->B, h->ws.invT);
       return hipGetLastError();
     }
   }
   auto args = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, block, 0, st, (const T*)h->W_lm, (const T*)hidden, h->V, h->H,
                        M, h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
-                       h->B);
+                       h->B, h->ws.invT);
   };
   if (lds) {
     switch (NU) {

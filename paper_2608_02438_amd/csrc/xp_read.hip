@@ -25,7 +25,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
     const T* __restrict__ W, const T* __restrict__ Z, const float* __restrict__ S, int Ms, int V,
     int M, int ntiles, int U, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
     const uint8_t* __restrict__ temp, int B, float* __restrict__ out_logits,
-    const int32_t* __restrict__ ctrl, int skip_when_done) {
+    const int32_t* __restrict__ ctrl, int skip_when_done, const float* __restrict__ invT) {
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   constexpr int NU = ReadTile<T>::NU;
   constexpr int NR = sizeof(T) == 2 ? 5 : 2;      // resident tiles per wave (32 / 64 VGPRs each)
@@ -42,6 +42,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
   const int p = p0 + (lane & 15);
   const bool act = p < M;
   const int pc = act ? p : M - 1;
+  const float pit = invT[pc / B];               // sampled rows: softmax(l / T)
   uint64_t best = kKeyMin;
   Stat st = stat_empty();
   bool sample = false;
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool v = act && row0 + i < V && sample;
-        const Stat nx = stat_merge(st, Stat{acc[i], 1.f});
+        const Stat nx = stat_merge(st, Stat{acc[i] * pit, 1.f});
         st.m = v ? nx.m : st.m;
         st.s = v ? nx.s : st.s;
       }
@@ -252,7 +253,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     int Ms, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B,
     float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done,
-    int nwg, int ny) {
+    int nwg, int ny, const float* __restrict__ invT) {
   static_assert(kReadWaves == 8, "one 1 KB load per wave fills a 16-row tile");
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   using RT = ReadTile<uint16_t>;
@@ -275,12 +276,14 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) RT::load_z(Z, M, pw + kTile * pb, lane, zf[pb]);
   bool act[P], sample[P];
+  float pit[P];                                   // sampled rows: softmax(l / T)
   bool any = false;
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
     const int p = pw + kTile * pb + (lane & 15);
     act[pb] = p < M;
     sample[pb] = act[pb] && load_flag(temp, (act[pb] ? p : M - 1) / B, S) != 0;
+    pit[pb] = invT[(act[pb] ? p : M - 1) / B];
     any = any || sample[pb];
   }
   const bool any_sample = __ballot(any) != 0;    // wave-uniform
@@ -389,7 +392,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
         float x[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          x[i] = (sample[pb] & (!last | (row0 + i < V))) ? acc[i] : -INFINITY;
+          x[i] = (sample[pb] & (!last | (row0 + i < V))) ? acc[i] * pit[pb] : -INFINITY;
         st[pb] = stat_add4(st[pb], x[0], x[1], x[2], x[3]);
       }
       if (out_logits) {
@@ -431,22 +434,22 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
       case 1:
         hipLaunchKernelGGL((k_read_multi<1>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
         break;
       case 2:
         hipLaunchKernelGGL((k_read_multi<2>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
         break;
       case 3:
         hipLaunchKernelGGL((k_read_multi<3>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
         break;
       default:
         hipLaunchKernelGGL((k_read_multi<4>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
                            M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny);
+                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
     }
     return hipGetLastError();
   }
@@ -454,11 +457,12 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     hipLaunchKernelGGL((k_read<uint16_t>), grid, block, 0, st, (const uint16_t*)h->W_r,
                        (const uint16_t*)h->ws.z, h->ws.s, M, h->V, M, h->ntiles,
                        h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl,
-                       skip);
+                       skip, h->ws.invT);
   else
     hipLaunchKernelGGL((k_read<float>), grid, block, 0, st, (const float*)h->W_r,
                        (const float*)h->ws.z, h->ws.s, M, h->V, M, h->ntiles, h->read_units,
-                       h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl, skip);
+                       h->ws.keys, h->ws.stats, temp, h->B, out_logits, h->ws.ctrl, skip,
+                       h->ws.invT);
   return hipGetLastError();
 }
 

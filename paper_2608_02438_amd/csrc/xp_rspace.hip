@@ -55,11 +55,23 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
                                               const T* __restrict__ hid, int H, int M,
                                               int ksp, float* __restrict__ part, int batch,
                                               int32_t* __restrict__ iters,
-                                              int32_t* __restrict__ ctrl) {
+                                              int32_t* __restrict__ ctrl,
+                                              const uint8_t* __restrict__ temp,
+                                              const float* __restrict__ temperature,
+                                              float* __restrict__ invT,
+                                              uint32_t* __restrict__ err) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rt = blockIdx.x, ks = blockIdx.y, mat = blockIdx.z & 1, pbg = blockIdx.z >> 1;
   if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
-    for (int i = threadIdx.x; i < batch; i += blockDim.x) iters[i] = 0;
+    for (int i = threadIdx.x; i < batch; i += blockDim.x) {
+      iters[i] = 0;
+      // 1 / T of the sequence, the factor its sampled logits are scaled by
+      // (softmax(l / T)); T must be finite and positive
+      const float tau = temperature != nullptr ? temperature[i] : 1.f;
+      const bool ok = tau > 0.f && tau <= 3.4e38f;             // false for NaN too
+      if (!ok && temp != nullptr && temp[i] != 0) atomicOr(err, XP_DEVERR_TEMPERATURE);
+      invT[i] = ok ? 1.f / tau : 1.f;
+    }
     if (threadIdx.x < 2) ctrl[threadIdx.x] = 0;
   }
   const float* F = mat ? Fg : Fh;
@@ -432,7 +444,8 @@ __global__ __launch_bounds__(256) void k_trans2(int B, const T* __restrict__ W2,
 }
 
 // ---------------------------------------------------------------------------
-hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t st) {
+hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, const uint8_t* temp,
+                       const float* temperature, hipStream_t st) {
   const int M = batch * h->B;
   const int npb = (M + 15) / 16;
   const int ksp = prep_ksp(h->H);
@@ -440,11 +453,11 @@ hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, hipStream_t 
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_prep<uint16_t>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
                        (const uint16_t*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
-                       h->ws.ctrl);
+                       h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
   else
     hipLaunchKernelGGL((k_prep<float>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
                        (const float*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
-                       h->ws.ctrl);
+                       h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
   if (h->B <= 16)
     hipLaunchKernelGGL((k_prep_sum<16>), dim3(batch, 16), dim3(256), 0, st, h->B, M, ksp,
                        h->ws.ppart, h->ws.Pa);

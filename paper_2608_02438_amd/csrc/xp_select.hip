@@ -3,8 +3,9 @@
 //
 // Greedy rows: the maximum 64-bit key over the stream's workgroups gives
 // argmax_v l_v with ties to the lowest index.
-// Sampled rows (temperature 1): y = min{v : sum_{w<=v} e^{l_w - m} > u Z},
-// one workgroup per position (k_sample):
+// Sampled rows at temperature T: with x_v = l_v / T (the fp32 product of l_v
+// and the fp32 1/T, the same in every kernel), y = min{v : sum_{w<=v}
+// e^{x_w - m} > u Z}, one workgroup per position (k_sample):
 //   1. m = max over units; the unit masses sum_u e^{max_u - m} are summed in
 //      fp64, each wave over a contiguous range of units (in-order wave
 //      scans), then the wave totals in wave order: Z;
@@ -12,7 +13,8 @@
 //      arithmetic) to find the crossing unit;
 //   3. that unit's rows are recomputed with the stream's own MFMA tile code
 //      (same fp32 logits) and scanned in vocabulary order in fp64.
-// The log-sum-exp m + log Z of the chosen pass is kept for verification.
+// The log-sum-exp m + log Z of the x of the chosen pass is kept for
+// verification.
 #include "xp_internal.h"
 #include "xp_tiles.h"
 
@@ -33,7 +35,7 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// Inverse-CDF selection at temperature 1, one workgroup per position (rows at
+// Inverse-CDF selection of softmax(l / T), one workgroup per position (rows at
 // temperature 0, and every row of a batch that is at its fixed point, return
 // at once).  mode 0: the seed Y^(0) from the base logits (with caller seeds
 // only the log-sum-exp is kept); mode 1: the selection of a Jacobi pass.  The
@@ -51,9 +53,10 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
     const T* __restrict__ W_r, const T* __restrict__ Z, const Stat* __restrict__ stats,
     int ntiles, int U, const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
     const float* __restrict__ u_draft, int32_t* __restrict__ Ynew, double* __restrict__ lse,
-    const int32_t* __restrict__ ctrl, int early_exit) {
+    const int32_t* __restrict__ ctrl, int early_exit, const float* __restrict__ invT) {
   const int p = blockIdx.x;
   if (temp[p / B] == 0) return;
+  const float it = invT[p / B];                   // the unit partials hold l / T
   if (mode == 1 && early_exit && ctrl[1] != 0) return;     // the selection keeps Y^(j)
   const bool pick = !(mode == 0 && seed_ids != nullptr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -172,7 +175,7 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
   double cum = s_pre;
   for (int base = rlo; base < rhi; base += 64) {
     const int row = base + lane;
-    const float l = row < rhi ? (mode == 0 ? S[s_index(p, row, Ms)] : lrow[row - rlo]) : 0.f;
+    const float l = row < rhi ? (mode == 0 ? S[s_index(p, row, Ms)] : lrow[row - rlo]) * it : 0.f;
     const double w = (row < rhi) ? exp((double)l - (double)m) : 0.0;
     const double tot = cum + wave_incl_scan(w, lane);
     const unsigned long long hit = __ballot(row < rhi && tot > target);
@@ -302,12 +305,12 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
       hipLaunchKernelGGL((k_sample<uint16_t>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const uint16_t*)h->W_r, (const uint16_t*)h->ws.z,
                          h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
-                         Ynew, h->ws.lse, h->ws.ctrl, early);
+                         Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
     else
       hipLaunchKernelGGL((k_sample<float>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
                          h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
-                         Ynew, h->ws.lse, h->ws.ctrl, early);
+                         Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
   }
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,

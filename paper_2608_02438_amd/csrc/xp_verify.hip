@@ -1,9 +1,12 @@
 // Block verification (section 3.1).
 //
 // Greedy rows: n = longest prefix with y_i = t_i, next = t_{n+1}.
-// Sampled rows (temperature 1), speculative accept / reject:
-//   accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k = softmax(l_k) of the refine's
-//   last pass, p_k = softmax(target logits after the prefix y_{<k});
+// Sampled rows at temperature T (that of the refine), speculative accept /
+// reject:
+//   accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k = softmax(l_k / T) of the
+//   refine's last pass, p_k = softmax(target logits after the prefix y_{<k},
+//   over T); every l / T is the fp32 product of l and the fp32 1/T, as in the
+//   refine's kernels;
 //   at the first rejection next ~ max(0, p_k - q_k) (p_k if that has no mass),
 //   if all B are accepted next ~ p_{B+1}; both by inverse CDF at u_res.
 // Kernels: target log-sum-exp per row -> accept scan -> residual mass per
@@ -13,23 +16,26 @@
 
 namespace xp {
 
-// lseT[b][k] = log sum_v exp(T[b][k][v]) for sampled rows, k = 0..B, in two
-// steps: every workgroup reduces one chunk of kVChunk entries of a row to
-// (max, sum of exp(T - max)), the exponentials in fp32 and the sums in fp64;
+// lseT[b][k] = log sum_v exp(t[b][k][v] / T) for sampled rows, k = 0..B (t
+// the target logits), in two steps: every workgroup reduces one chunk of
+// kVChunk entries of a row to (max, sum of exp(x - max)), the exponentials in
+// fp32 and the sums in fp64;
 // then one wave per row merges the chunks in a fixed order.
 __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ tl, int B, int V,
                                                       const uint8_t* __restrict__ temp,
+                                                      const float* __restrict__ invT,
                                                       double* __restrict__ part) {
   constexpr int PER = kVChunk / 256;
   const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z, nc = gridDim.x;
   if (temp[b] == 0) return;
+  const float it = invT[b];
   const float* row = tl + ((size_t)b * (B + 1) + k) * V;
   float x[PER];
   float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int v = c * kVChunk + i * 256 + threadIdx.x;
-    x[i] = v < V ? row[v] : -INFINITY;
+    x[i] = v < V ? row[v] * it : -INFINITY;
     m = fmaxf(m, x[i]);
   }
   __shared__ float sm[4];
@@ -104,7 +110,7 @@ __global__ __launch_bounds__(64) void k_vaccept(
     const float* __restrict__ tl, const float* __restrict__ racc, const float* __restrict__ S,
     int Ms, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
     const double* __restrict__ lseT, int32_t* __restrict__ vpos, int32_t* __restrict__ out_n,
-    int32_t* __restrict__ out_next, uint32_t* __restrict__ err) {
+    int32_t* __restrict__ out_next, uint32_t* __restrict__ err, const float* __restrict__ invT) {
   const int b = blockIdx.x, lane = threadIdx.x;
   const bool sample = temp != nullptr && temp[b] != 0;
   int bad = 0;
@@ -129,6 +135,7 @@ __global__ __launch_bounds__(64) void k_vaccept(
     }
     return;
   }
+  const float it = invT[b];
   int n = B;
   for (int k = 0; k < B; ++k) {
     const int p = b * B + k;
@@ -138,9 +145,9 @@ __global__ __launch_bounds__(64) void k_vaccept(
       y = 0;
     }
     const float l = refined_logit<T>(with_read, S, Ms, W_r, Z, M, V, p, y);
-    const double q = exp((double)l - lse[p]);
+    const double q = exp((double)(l * it) - lse[p]);
     const double pt =
-        exp((double)tl[((size_t)b * (B + 1) + k) * V + y] - lseT[(size_t)b * (B + 1) + k]);
+        exp((double)(tl[((size_t)b * (B + 1) + k) * V + y] * it) - lseT[(size_t)b * (B + 1) + k]);
     if (!((double)racc[p] * q <= pt)) {
       n = k;
       break;
@@ -175,12 +182,13 @@ __global__ __launch_bounds__(1024) void k_vresid(
     const uint8_t* __restrict__ temp, const int32_t* __restrict__ vpos,
     const float* __restrict__ tl, const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
     const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
-    double* __restrict__ vmass) {
+    double* __restrict__ vmass, const float* __restrict__ invT) {
   constexpr int NU = ReadTile<T>::NU;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, NW = blockDim.x >> 6;
   const int u = blockIdx.x * NW + wave;
   const int b = blockIdx.y * 16 + (lane & 15);
   const bool act = b < batch && temp != nullptr && temp[b] != 0;
+  const float it = invT[act ? b : 0];
   const int k = act ? vpos[b] : 0;
   const bool resid = act && k < B;
   const int p = b * B + (k < B ? k : 0);
@@ -204,7 +212,7 @@ __global__ __launch_bounds__(1024) void k_vresid(
         if (row < V) {
           const float l = resid ? acc[i] : 0.f;
           double res, pw;
-          resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
+          resample_weights(trow[row] * it, lk, resid, l * it, lp, &res, &pw);
           mr += res;
           mp += pw;
         }
@@ -245,9 +253,10 @@ __global__ __launch_bounds__(kVfWaves * kWave) void k_vfinal(
     const float* __restrict__ tl, const float* __restrict__ S, int Ms, const T* __restrict__ W_r,
     const T* __restrict__ Z, const double* __restrict__ lse, const double* __restrict__ lseT,
     const double* __restrict__ vmass, const float* __restrict__ u_res,
-    int32_t* __restrict__ out_next) {
+    int32_t* __restrict__ out_next, const float* __restrict__ invT) {
   const int b = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (temp == nullptr || temp[b] == 0) return;
+  const float it = invT[b];
   __shared__ double wt[2][kVfWaves];
   const int k = vpos[b];
   bool resid = k < B;
@@ -339,7 +348,7 @@ __global__ __launch_bounds__(kVfWaves * kWave) void k_vfinal(
     if (row < rhi) {
       const float l = resid ? mine : 0.f;
       double res, pw;
-      resample_weights(trow[row], lk, resid, l, lp, &res, &pw);
+      resample_weights(trow[row] * it, lk, resid, l * it, lp, &res, &pw);
       w = use_resid ? res : pw;
     }
     const double tot = cum + wave_scan_d(w, lane);
@@ -366,7 +375,7 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
   if (temp) {
     const int nc = (h->V + kVChunk - 1) / kVChunk;
     hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1, batch), dim3(256), 0, st, tl, h->B,
-                       h->V, temp, h->ws.vpart);
+                       h->V, temp, h->ws.invT, h->ws.vpart);
     const int rows = batch * (h->B + 1);
     hipLaunchKernelGGL(k_vtarget_comb, dim3(rows), dim3(kWave), 0, st, h->B, nc, temp,
                        h->ws.vpart, h->ws.vstat);
@@ -374,16 +383,17 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
                      draft, temp, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
                      (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
-                     h->ws.err);
+                     h->ws.err, h->ws.invT);
   if (temp) {
     hipLaunchKernelGGL((k_vresid<T>), dim3(h->read_wgs, (batch + 15) / 16),
                        dim3(kReadWaves * kWave), 0, st, batch, h->B, h->V, M, with_read,
                        h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s, M,
-                       (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vmass);
+                       (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vmass,
+                       h->ws.invT);
     hipLaunchKernelGGL((k_vfinal<T>), dim3(batch), dim3(kVfWaves * kWave), 0, st, batch, h->B, h->V, M,
                        with_read, h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s,
                        M, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
-                       h->ws.vmass, ures, out_next);
+                       h->ws.vmass, ures, out_next, h->ws.invT);
   }
   return hipGetLastError();
 }

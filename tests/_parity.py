@@ -53,10 +53,14 @@ class Problem:
     weights: dict
     inp: synth.Inputs
     seed_given: bool
+    tau: np.ndarray | None = None       # [batch] float32 temperatures (None: 1)
+
+    def T(self, b) -> float:
+        return 1.0 if self.tau is None else float(self.tau[b])
 
 
 def custom_problem(dtype, H, V, B, batch, K, sigmas=None, temp="greedy", seed=0,
-                   seed_given=False, h_sigma=1.0, index=500):
+                   seed_given=False, h_sigma=1.0, index=500, tau=None):
     """A problem with per-matrix weight scales (stress trajectories, ragged V)."""
     w = synth.scaled(synth.configs.QWEN_B1, index=index + seed, dtype=dtype, H=H, V=V, B=B,
                      batch=batch, K=K, temp=temp, h_sigma=h_sigma,
@@ -72,14 +76,21 @@ def custom_problem(dtype, H, V, B, batch, K, sigmas=None, temp="greedy", seed=0,
             f[:, ~keep] = 0.0
         weights[n] = gen.f32_to_bf16_bits(f) if dtype == "bf16" else f
     inp = synth.make_inputs(w)
-    return Problem(dtype, H, 256, V, B, batch, K, weights, inp, seed_given)
+    return Problem(dtype, H, 256, V, B, batch, K, weights, inp, seed_given, temperatures(tau, batch))
 
 
-def workload_problem(wl, batch=None):
+def temperatures(tau, batch):
+    """[batch] float32 temperatures from a scalar or a sequence (None stays None)."""
+    if tau is None:
+        return None
+    return np.broadcast_to(np.asarray(tau, dtype=np.float32), (batch,)).copy()
+
+
+def workload_problem(wl, batch=None, tau=None):
     weights = synth.make_weights(wl)
     inp = synth.make_inputs(wl, batch=batch)
     return Problem(wl.dtype, wl.H, wl.r, wl.V, wl.B, batch or wl.batch, wl.K, weights, inp,
-                   wl.seed_mode == "given")
+                   wl.seed_mode == "given", temperatures(tau, batch or wl.batch))
 
 
 # ---------------------------------------------------------------------------
@@ -104,6 +115,7 @@ def upload(prob: Problem):
     d["r_accept"] = device_tensor(i.r_accept)
     d["u_res"] = device_tensor(i.u_res)
     d["target_logits"] = device_tensor(i.target_logits) if sample_rows else None
+    d["temperature"] = device_tensor(prob.tau) if prob.tau is not None else None
     torch.cuda.synchronize()
     return d
 
@@ -119,7 +131,8 @@ def run_device(ref, prob: Problem, dev: dict, K=None, early_exit=False, write_lo
     K = prob.K if K is None else K
     out = ref.refine_block(dev["hidden"], dev["anchor"], seed_ids=dev["seed_ids"],
                            temp=dev["temp"], u_draft=dev["u_draft"], K=K,
-                           early_exit=early_exit, write_logits=write_logits, want_traj=True)
+                           early_exit=early_exit, write_logits=write_logits, want_traj=True,
+                           temperature=dev.get("temperature"))
     torch.cuda.synchronize()
     return DeviceRun(ids=out.ids.cpu().numpy(), iters=out.iters.cpu().numpy(),
                      traj=out.traj.cpu().numpy(),
@@ -191,28 +204,34 @@ def pass_logits(P, s_b, h_b, anchor, Y_prev):
     return l, E
 
 
-def _decision_ok(l, E, y_dev, sample, u):
-    y_o, _ = O.select(l, sample, u)
+def tempered_bound(l, E, T):
+    """Bound on |x_device - l / T| when the device forms x as the fp32 product
+    of l_device and the fp32 1/T: E / T plus two roundings of |l| / T."""
+    return E / T + 2 * U32 * np.abs(l) / T
+
+
+def _decision_ok(l, E, y_dev, sample, u, T=1.0):
+    y_o, _ = O.select(l, sample, u, T)
     if y_o == y_dev:
         return "exact"
     if not sample:
         ok = (l[y_o] - l[y_dev]) <= E[y_o] + E[y_dev]
     else:
-        w = O.softmax_weights(l)
+        w = O.softmax_weights(l, T)
         C = np.cumsum(w)
         Z = C[-1]
         lo = C[y_dev - 1] if y_dev > 0 else 0.0
-        f = np.exp(4 * E.max())
+        f = np.exp(4 * tempered_bound(l, E, T).max())
         ok = lo / f <= u * Z <= C[y_dev] * f
     return "excused" if ok else "wrong"
 
 
-def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits):
+def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits, T=1.0):
     """Validate one sequence's device trajectory; returns (Tally, final logits, final E)."""
     B = s_b.shape[0]
     t = Tally(seqs=1)
     ref = O.refine_block(P, s_b, h_b, anchor, seed=seed, sample=sample, u=u, K=K,
-                         early_exit=False)
+                         early_exit=False, T=T)
     tro = ref.traj_padded(K)
     first = 0 if seed is None else 1
     exact_traj = np.array_equal(tro, traj)
@@ -225,7 +244,7 @@ def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits)
         if exact_traj:
             continue
         for k in range(B):
-            r = _decision_ok(l[k], E[k], int(traj[j][k]), sample, float(u[k]))
+            r = _decision_ok(l[k], E[k], int(traj[j][k]), sample, float(u[k]), T)
             assert r != "wrong", f"pass {j} position {k}: device token {traj[j][k]} is not a valid selection"
             t.decisions += 1
             t.exact += r == "exact"
@@ -261,7 +280,8 @@ def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None):
         seed = i.seed_ids[b] if prob.seed_given else None
         t, lf, Ef = check_sequence(P, s[n], i.h[b], int(i.anchor[b]), seed, bool(i.temp[b]),
                                    i.u_draft[b], run.traj.shape[0] - 1, run.traj[:, b],
-                                   run.iters[b], None if run.logits is None else run.logits[b])
+                                   run.iters[b], None if run.logits is None else run.logits[b],
+                                   prob.T(b))
         tot.add(t)
         finals[b] = (lf, Ef)
     return tot, finals
@@ -283,17 +303,20 @@ def check_verify(prob: Problem, run: DeviceRun, finals: dict, n_dev, next_dev, t
             assert (int(n_dev[b]), int(next_dev[b])) == (n, nx), f"seq {b}"
             continue
         lf, Ef = finals[b]
+        T = prob.T(b)
         pl = i.target_logits[b].astype(np.float64)
-        v = O.verify_sample(lf, y, pl, i.r_accept[b], float(i.u_res[b]))
+        v = O.verify_sample(lf, y, pl, i.r_accept[b], float(i.u_res[b]), T)
         if (int(n_dev[b]), int(next_dev[b])) == (v.n, v.next):
             continue
         k = min(int(n_dev[b]), v.n)
-        tol = np.exp(2 * Ef[min(k, prob.B - 1)].max()) - 1 + 1e-6
+        kq = min(k, prob.B - 1)
+        tol = (np.exp(2 * tempered_bound(lf[kq], Ef[kq], T).max()) - 1 + 1e-6
+               + 4 * U32 * np.abs(pl[k]).max() / T)
         if int(n_dev[b]) != v.n:
             assert v.accept_margins[k] <= tol, f"seq {b}: accept decision at {k} is not a near-tie"
         else:
-            p = O.softmax(pl[k])
-            res = np.maximum(p - O.softmax(lf[k]), 0.0) if k < prob.B else p
+            p = O.softmax(pl[k], T)
+            res = np.maximum(p - O.softmax(lf[k], T), 0.0) if k < prob.B else p
             if not res.sum() > 0:
                 res = p
             C = np.cumsum(res)

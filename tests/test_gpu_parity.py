@@ -82,6 +82,48 @@ def test_stress_sampling_mixed_rows(dtype):
     _full_check(prob, ref, upload(prob), min_exact=0.97)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stress_sampling_at_temperatures(dtype):
+    tau = [0.5, 0.8, 1.6, 3.0]
+    _say(f"case: stress sampling {dtype} H=256 V=777 B=8 batch=4 K=8 temperatures {tau}")
+    prob = custom_problem(dtype, H=256, V=777, B=8, batch=4, K=8, sigmas=STRESS, temp="sample",
+                          seed=21, tau=tau)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
+@pytest.mark.parametrize("batch,tau", [(5, 1.7), (20, 0.6)])
+def test_lmhead_gemm_and_read_multi_at_temperature(batch, tau):
+    _say(f"case: GEMM + read_multi at T={tau}, bf16 H=512 V=1000 B=16 batch={batch} K=6")
+    prob = custom_problem("bf16", H=512, V=1000, B=16, batch=batch, K=6, sigmas=STRESS,
+                          temp="sample", seed=31 + batch, tau=tau)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
+def test_invalid_temperature_sets_device_error_and_samples_at_one():
+    import torch
+    from paper_2608_02438_amd.xpress import XP_DEVERR_TEMPERATURE
+    _say("case: invalid temperatures on sampled rows (0, NaN, -1, inf), greedy row with NaN")
+    prob = custom_problem("bf16", H=256, V=500, B=8, batch=4, K=4, sigmas=STRESS, temp="mixed",
+                          seed=41, tau=1.0)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    base = run_device(ref, prob, dev)
+    assert ref.device_errors() == 0
+    # rows 1 and 3 sample, rows 0 and 2 are greedy
+    for bad in ([1.0, 0.0, 1.0, float("nan")], [1.0, -1.0, 1.0, float("inf")]):
+        dev["temperature"] = torch.tensor(bad, dtype=torch.float32, device="cuda")
+        run = run_device(ref, prob, dev)
+        assert np.array_equal(run.ids, base.ids) and np.array_equal(run.traj, base.traj)
+        assert ref.device_errors() == XP_DEVERR_TEMPERATURE
+    dev["temperature"] = torch.tensor([float("nan"), 1.0, 0.0, 1.0], dtype=torch.float32,
+                                      device="cuda")
+    run = run_device(ref, prob, dev)
+    assert np.array_equal(run.ids, base.ids)
+    assert ref.device_errors() == 0, "greedy rows ignore their temperature"
+
+
 def test_block_of_one_and_K0():
     _say("case: B=1 and K=0")
     prob = custom_problem("bf16", H=256, V=300, B=1, batch=5, K=3, sigmas=STRESS, seed=3)
@@ -201,6 +243,15 @@ def test_qwen3_shape_batch1_greedy(qwen_b1):
 def test_qwen3_shape_batch8_sampled():
     _say("case: Qwen3-8B shape, batch 8, B=16, temperature 1, K=6")
     prob = workload_problem(QWEN_B8_T1)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.8)
+
+
+def test_qwen3_shape_batch1_sampled_at_temperature():
+    from synth.configs import scaled
+    _say("case: Qwen3-8B shape, batch 1, B=16, sampled at T=0.6, K=6 (LM-head and Read streams)")
+    wl = scaled(QWEN_B1, name="qwen3-8b-bf16-B16-b1-sample", temp="sample", h_sigma=1.5625)
+    prob = workload_problem(wl, tau=0.6)
     ref = make_refiner(prob)
     _full_check(prob, ref, upload(prob), min_exact=0.8)
 
