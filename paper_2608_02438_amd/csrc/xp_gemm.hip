@@ -157,23 +157,29 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
       for (int cc = 0; cc < NB; ++cc) acc[a][cc] = mma32(av[a], bv[cc], acc[a][cc]);
   };
 
+  // The position tile is fixed per workgroup, so the sampling flags and 1/T
+  // of this wave's positions are loaded once, before the stage loads, and
+  // waited for here: no epilogue then waits for a load.
+  bool psamp[NB];
+  float pit[NB];                                   // sampled rows: softmax(s / T)
+  bool anyp = false;
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int p = p0 + wp * PW + c * 32 + lr;
+    const int pc = p < M ? p : M - 1;
+    psamp[c] = (p < M) & (load_flag(temp, pc / B, W) != 0);
+    pit[c] = invT[pc / B];
+    anyp = anyp | psamp[c];
+  }
+  const bool any_sample = __ballot(anyp) != 0;
+#pragma unroll
+  for (int c = 0; c < NB; ++c) asm volatile("" ::"v"(pit[c]));
   // epilogue of tile ti: s from the accumulators, and the selection partials
   // of this wave's unit for its PW positions
   auto epilogue = [&](int ti) {
     const int hu = 2 * sc.unit(ti) + wv;
     const int rbase = unit_tile_lo(hu, ntiles, U2) * kTile;
     const int nr = unit_tile_lo(hu + 1, ntiles, U2) * kTile - rbase;   // <= RW, multiple of 16
-    bool psamp[NB];
-    float pit[NB];                                   // sampled rows: softmax(s / T)
-    bool anyp = false;
-#pragma unroll
-    for (int c = 0; c < NB; ++c) {
-      const int p = p0 + wp * PW + c * 32 + lr;
-      psamp[c] = p < M && load_flag(temp, (p < M ? p : M - 1) / B, W) != 0;
-      pit[c] = invT[(p < M ? p : M - 1) / B];
-      anyp = anyp || psamp[c];
-    }
-    const bool any_sample = __ballot(anyp) != 0;
 #pragma unroll
     for (int c = 0; c < NB; ++c) {
       const int p = p0 + wp * PW + c * 32 + lr;
