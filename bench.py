@@ -364,6 +364,10 @@ def main():
         "ms_per_step_rounds_mean": sum(rounds) / len(rounds),
         "ms_per_step_rounds_min": min(rounds),
         "accepted_mean": float(np.mean(n_acc)),
+        # tokens committed per second (accepted draft tokens plus the
+        # correction or bonus token of each sequence): context only, the
+        # synthetic targets fix the acceptance
+        "committed_tokens_per_s": float(np.sum(n_acc + 1)) * args.steps / elapsed,
     }
     if not args.no_cpu:
         log("[bench] CPU oracle baseline (all threads)")
