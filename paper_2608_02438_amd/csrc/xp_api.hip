@@ -301,6 +301,7 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
     return fail(h, XP_EINVAL, "out_logits given without XP_WRITE_LOGITS");
   hipStream_t st = (hipStream_t)stream;
   h->state_valid = false;
+  h->call_tempered = temp != nullptr && temperature != nullptr;
   // All-greedy batches run the selection of pass j-1, Fuse, Mix and the first
   // Trans product of pass j as one kernel; the others use separate kernels.
   XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, temp, temperature, st));

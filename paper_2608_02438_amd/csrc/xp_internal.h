@@ -70,7 +70,8 @@ struct xp_handle {
   int last_batch = -1;         // batch of the last refine (verify state)
   bool state_valid = false;
   bool state_k0 = false;       // last refine ran K = 0 passes (q = softmax(s))
-  bool state_temp = false;     // last refine was given per-row temperatures
+  bool state_temp = false;     // last refine was given sampling flags
+  bool call_tempered = false;  // the current refine has sampled rows and a temperature array
   std::string err;
   xp_timing_state tm;
 };

@@ -231,7 +231,10 @@ constexpr int kSkPF = 5;               // items in flight per wave
 // of 16 rows.
 __device__ __forceinline__ int sk_slot(int row, int c) { return row * 8 + (c ^ ((row & 7) ^ (row >> 3))); }
 
-template <int PF>
+// TT: the call gives temperatures (sampled rows scale by 1/T).  Without them
+// the kernel keeps no 1/T register: it runs at its register limit, so the
+// variant with temperatures keeps one item less in flight per wave.
+template <int PF, bool TT>
 __global__ __launch_bounds__(1024) void k_lmhead_sk(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int V, int H, int M, int ntiles,
     int U, float* __restrict__ S, int Ms, uint64_t* __restrict__ keys, Stat* __restrict__ stats,
@@ -255,7 +258,6 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   // other load), then h, then the first items of W_lm
   const int p_flag = p0 + (lane & 15);
   const int tvf = load_flag(temp, (p_flag < M ? p_flag : M - 1) / B, X);
-  const float pit = invT[(p_flag < M ? p_flag : M - 1) / B];   // sampled rows: softmax(s / T)
   asm volatile("" ::: "memory");
   // h: every thread issues its (at most 8) chunk loads at once; rows past M
   // are loaded from row M-1 and zeroed
@@ -299,6 +301,7 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
   };
   // s of one finished tile, and its selection partials without branches on
   // the greedy path (every key is formed and kept or dropped by a select)
+  float pit = 1.f;                                        // set after h is in LDS (TT)
   auto finalize = [&](floatx4 acc, int t) {
     const int row0 = t * kTile + 4 * g;
     if (pact)
@@ -369,6 +372,9 @@ __global__ __launch_bounds__(1024) void k_lmhead_sk(
         p0 + pp < M ? hv[j] : u32x4{0u, 0u, 0u, 0u};
   }
   lds_barrier();                                          // h is in LDS; items stay in flight
+  // 1/T of the lane's position for the sampled rows' partials (softmax(s / T)),
+  // loaded once h's registers are free
+  if constexpr (TT) pit = invT[(p_flag < M ? p_flag : M - 1) / B];
   if (i0 < i1) {
     int i = i0;
     for (; i + PF <= i1; i += PF) {
@@ -470,10 +476,16 @@ static hipError_t launch_lmhead_t(xp_handle* h, int M, const void* hidden, const
   const bool lds = (size_t)h->H * sizeof(T) <= 16u * kHChunks;
   if constexpr (sizeof(T) == 2) {
     if (lds) {
-      hipLaunchKernelGGL((k_lmhead_sk<kSkPF>), grid, dim3(kSkWaves * kWave), 0, st,
-                         (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
-                         h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
-                         h->B, h->ws.invT);
+      if (h->call_tempered)
+        hipLaunchKernelGGL((k_lmhead_sk<kSkPF - 1, true>), grid, dim3(kSkWaves * kWave), 0, st,
+                           (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
+                           h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
+                           h->B, h->ws.invT);
+      else
+        hipLaunchKernelGGL((k_lmhead_sk<kSkPF, false>), grid, dim3(kSkWaves * kWave), 0, st,
+                           (const uint16_t*)h->W_lm, (const uint16_t*)hidden, h->V, h->H, M,
+                           h->ntiles, h->lm_chunks, h->ws.s, M, h->ws.keys, h->ws.stats, temp,
+                           h->B, h->ws.invT);
       return hipGetLastError();
     }
   }
