@@ -124,6 +124,19 @@ def test_invalid_temperature_sets_device_error_and_samples_at_one():
     assert ref.device_errors() == 0, "greedy rows ignore their temperature"
 
 
+@pytest.mark.parametrize("H,V,batch,B", [(8192, 20011, 1, 16), (8192, 20011, 2, 32),
+                                         (512, 262135, 1, 16), (512, 262135, 4, 16)])
+def test_largest_built_sizes(H, V, batch, B):
+    # the largest hidden width built (H = 8192: the stream LM head without LDS
+    # staging of h at 16 positions, the 128 x 128 GEMM at 64), and a vocabulary
+    # just under the largest built (2^18, ragged tail), with B up to 32
+    _say(f"case: largest sizes bf16 H={H} V={V} B={B} batch={batch} mixed K=4")
+    prob = custom_problem("bf16", H=H, V=V, B=B, batch=batch, K=4, sigmas=STRESS,
+                          temp="mixed", seed=51 + B + batch)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
 def test_block_of_one_and_K0():
     _say("case: B=1 and K=0")
     prob = custom_problem("bf16", H=256, V=300, B=1, batch=5, K=3, sigmas=STRESS, seed=3)
