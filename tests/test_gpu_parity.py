@@ -137,6 +137,31 @@ def test_largest_built_sizes(H, V, batch, B):
     _full_check(prob, ref, upload(prob), min_exact=0.97)
 
 
+@pytest.mark.parametrize("tau", [None, 0.7])
+def test_sampled_rows_all_accepted_take_the_bonus_token(tau):
+    """Target logits equal to the refined logits (p = q) accept every draft
+    token, so the next token is the inverse-CDF sample of p_{B+1} at u_res:
+    the bonus path of verification, rarely reached with random targets."""
+    import torch
+    _say(f"case: sampled rows with p = q (all accepted, bonus token), T={tau}")
+    prob = custom_problem("bf16", H=256, V=777, B=8, batch=4, K=4, sigmas=STRESS,
+                          temp="sample", seed=61, tau=tau)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    run = run_device(ref, prob, dev)
+    tally, finals = check_refine(prob, run)
+    assert tally.exact >= 0.97 * tally.decisions
+    tl = prob.inp.target_logits.copy()
+    tl[:, :prob.B, :] = run.logits                 # p_k = q_k for k = 1..B
+    prob.inp.target_logits = tl
+    dev["target_logits"] = torch.from_numpy(tl).cuda()
+    target_ids = prob.inp.target_ids(run.ids)
+    n, nx = _verify(ref, prob, run, dev, target_ids)
+    _say(f"  verify: n={n.tolist()} next={nx.tolist()}")
+    assert (n == prob.B).all()
+    assert check_verify(prob, run, finals, n, nx, target_ids, range(prob.batch)) == 0
+
+
 def test_block_of_one_and_K0():
     _say("case: B=1 and K=0")
     prob = custom_problem("bf16", H=256, V=300, B=1, batch=5, K=3, sigmas=STRESS, seed=3)
