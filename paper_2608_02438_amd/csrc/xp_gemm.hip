@@ -110,15 +110,19 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
   }
   // first rows of the two units of the tile being issued (cached per tile)
   int iss_tile = -1, iss_r0 = 0, iss_r1 = 0;
-  auto issue = [&](int gs) {                                       // global stage gs (clamped)
+  auto prep = [&](int gs) {                                        // first rows of stage gs
     gs = gs < nstages ? gs : nstages - 1;
-    const int ti = gs / nk, kc = gs - ti * nk;
+    const int ti = gs / nk;
     if (ti != iss_tile) {                                          // wave-uniform
       const int u = sc.unit(ti);
       iss_tile = ti;
       iss_r0 = unit_tile_lo(2 * u, ntiles, U2) * kTile;
       iss_r1 = unit_tile_lo(2 * u + 1, ntiles, U2) * kTile;
     }
+  };
+  auto issue = [&](int gs) {                                       // global stage gs (clamped)
+    gs = gs < nstages ? gs : nstages - 1;
+    const int ti = gs / nk, kc = gs - ti * nk;
     const int st = gs % NS;
 #pragma unroll
     for (int j = 0; j < WI; ++j) {
@@ -234,7 +238,10 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
   };
 
 #pragma unroll
-  for (int s = 0; s < NS; ++s) issue(s);
+  for (int s = 0; s < NS; ++s) {
+    prep(s);
+    issue(s);
+  }
   constexpr int kP0 = (WI + HI) * (NS - 1), kP = (WI + HI) * (NS - 2);
   static_assert(kP0 < 64, "vmcnt field");
   // stage 0 landed (this wave's loads), then every wave's
@@ -252,19 +259,30 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     // this wave's reads of stage gs are done) makes stage gs + 1 readable for
     // everyone and frees the slot of stage gs for stage gs + NS.  Other
     // vector-memory operations (the epilogue's stores) only make the wait
-    // stricter.
+    // stricter.  The row bookkeeping of stage gs + NS runs before the wait;
+    // its loads are issued after the barrier, between the matrix operations
+    // of k step 1 (one load per two of them), so neither stalls the matrix
+    // pipe.
     rd(gs, 1, fa[1], fb[1]);
     __builtin_amdgcn_sched_barrier(0);
     mm(fa[0], fb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    prep(gs + NS);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0x0070 | (kP & 15) | ((kP >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    issue(gs + NS);
     rd(gs + 1, 0, fa[0], fb[0]);
     __builtin_amdgcn_sched_barrier(0);
     mm(fa[1], fb[1]);
+    issue(gs + NS);
+#pragma unroll
+    for (int q = 0; q < WI + HI; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_sched_barrier(0);

@@ -289,13 +289,14 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   const bool any_sample = __ballot(any) != 0;    // wave-uniform
   // greedy rows: running maximum and its row (rows arrive in increasing order
   // in every lane, so a strict comparison keeps the lowest index of a tie;
-  // -0 == +0 as in the key order)
+  // -0 == +0 as in the key order).  Other rows start at +inf, which no value
+  // exceeds, so they keep the empty key without a mask in the loop.
   float bv[P];
   uint32_t bi[P];
   Stat st[P];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
-    bv[pb] = -INFINITY;
+    bv[pb] = act[pb] & !sample[pb] ? -INFINITY : INFINITY;
     bi[pb] = 0xFFFFFFFFu;
     st[pb] = stat_empty();
   }
@@ -378,21 +379,26 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     for (int i = 0; i < NU; ++i)
 #pragma unroll
       for (int pb = 0; pb < P; ++pb) accs[pb] = Mfma<uint16_t>::mma(a[i], zf[pb][i], accs[pb]);
+    if (last) {                                    // wave-uniform
+      // rows past V become -inf: no maximum takes them, no sum counts them
+#pragma unroll
+      for (int pb = 0; pb < P; ++pb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) accs[pb][i] = row0 + i < V ? accs[pb][i] : -INFINITY;
+    }
 #pragma unroll
     for (int pb = 0; pb < P; ++pb) {
       const floatx4 acc = accs[pb];
-      const bool gv = act[pb] & !sample[pb];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bool take = gv & (!last | (row0 + i < V)) & (acc[i] > bv[pb]);
+        const bool take = acc[i] > bv[pb];
         bv[pb] = take ? acc[i] : bv[pb];
         bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
       }
       if (any_sample) {
         float x[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          x[i] = (sample[pb] & (!last | (row0 + i < V))) ? acc[i] * pit[pb] : -INFINITY;
+        for (int i = 0; i < 4; ++i) x[i] = sample[pb] ? acc[i] * pit[pb] : -INFINITY;
         st[pb] = stat_add4(st[pb], x[0], x[1], x[2], x[3]);
       }
       if (out_logits) {
