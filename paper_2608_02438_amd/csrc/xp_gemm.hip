@@ -259,13 +259,19 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     // this wave's reads of stage gs are done) makes stage gs + 1 readable for
     // everyone and frees the slot of stage gs for stage gs + NS.  Other
     // vector-memory operations (the epilogue's stores) only make the wait
-    // stricter.  The row bookkeeping of stage gs + NS runs before the wait;
-    // its loads are issued after the barrier, between the matrix operations
-    // of k step 1 (one load per two of them), so neither stalls the matrix
-    // pipe.
+    // stricter.  In both halves the fragment reads of the next k step go
+    // one by one between the matrix operations of the current one (the
+    // scheduling groups below), so the LDS reads overlap the matrix pipe; the
+    // row bookkeeping of stage gs + NS runs before the wait and its loads are
+    // issued after the barrier, behind those reads.
     rd(gs, 1, fa[1], fb[1]);
-    __builtin_amdgcn_sched_barrier(0);
     mm(fa[0], fb[0]);
+#pragma unroll
+    for (int q = 0; q < NA + NB; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
     __builtin_amdgcn_sched_barrier(0);
     prep(gs + NS);
     __builtin_amdgcn_sched_barrier(0);
@@ -274,15 +280,16 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     rd(gs + 1, 0, fa[0], fb[0]);
-    __builtin_amdgcn_sched_barrier(0);
     mm(fa[1], fb[1]);
     issue(gs + NS);
 #pragma unroll
-    for (int q = 0; q < WI + HI; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    for (int q = 0; q < NA + NB; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_sched_barrier(0);
