@@ -99,6 +99,22 @@ typedef struct {
  */
 xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle** out);
 
+/*
+ * The Toeplitz mixer (remark after Proposition 1, section 3): when L^(d)_{k,j}
+ * depends only on the offset k - j, Mix is a causal depthwise conv1d of kernel
+ * size B with taps [1, kappa_d[1], ..., kappa_d[B-1]].  Writes the full mixer
+ *   L_out[d][k][j] = kappa[d][k - j] for j < k, 0 for j >= k
+ * ([r][B][B], element type `dtype`, row-major) from
+ *   kappa [r][B] (kappa[d][0] is never read: lag 0 is the identity of eq. mix)
+ * for use as xp_weights.L, so a handle created from it runs the conv1d form.
+ * Both are device pointers owned by the caller; L_out must not overlap kappa.
+ * Asynchronous on `stream` (NULL = the default stream); no allocation.
+ * Errors: XP_EINVAL (null pointer, r outside [1, 65536], B outside [1, 32],
+ * unknown dtype), before any HIP call; XP_EHIP if the launch fails.
+ */
+xp_status xp_toeplitz_mixer(const void* kappa, int32_t r, int32_t B, int32_t dtype, void* L_out,
+                            void* stream);
+
 /* Free the handle and its workspace.  Waits for the device first.  NULL is a no-op. */
 void xp_destroy(xp_handle* h);
 

@@ -193,6 +193,23 @@ def mix(L: np.ndarray, A: np.ndarray) -> np.ndarray:
     return C
 
 
+def toeplitz_mixer(kappa: np.ndarray) -> np.ndarray:
+    """The mixer of the Toeplitz remark (section 3): L^(d)_{k,j} = kappa[d][k-j].
+
+    kappa is [r][B]; lag 0 is the identity of eq. mix, so kappa[:, 0] is never
+    read.  Returns L [r][B][B] with L[d][k][j] = kappa[d][k - j] for j < k and 0
+    on and above the diagonal, so Mix with it is a causal depthwise conv1d of
+    kernel size B (kernel [1, kappa[d][1], ..., kappa[d][B-1]]).
+    """
+    kappa = np.asarray(kappa)
+    r, B = kappa.shape
+    L = np.zeros((r, B, B), dtype=kappa.dtype)
+    for k in range(B):
+        for j in range(k):
+            L[:, k, j] = kappa[:, k - j]
+    return L
+
+
 def trans(P: Params, C: np.ndarray) -> np.ndarray:
     """z_k = c_k + W_2 sigma(W_1 c_k), sigma = SiLU   (eq. mlp)."""
     return C + silu(C @ P.W_1.T) @ P.W_2.T

@@ -23,7 +23,7 @@ XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE = 1, 2
 
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
-           "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16")
+           "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16", "xp_toeplitz_mixer")
 STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
 
 
@@ -75,6 +75,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_probe_hbm_read.restype = i32
     L.xp_probe_mfma_bf16.argtypes = [vp, i32, i32, vp, vp]
     L.xp_probe_mfma_bf16.restype = i32
+    L.xp_toeplitz_mixer.argtypes = [vp, i32, i32, i32, vp, vp]
+    L.xp_toeplitz_mixer.restype = i32
     _lib = L
     return L
 
@@ -259,3 +261,21 @@ def probe_mfma_bf16(operands, workgroups: int, iters: int, out, stream=None):
     assert out.numel() >= workgroups * 4 * 64 * 16
     _check(L.xp_probe_mfma_bf16(_ptr(operands), workgroups, iters, _ptr(out), _stream(stream)),
            "xp_probe_mfma_bf16")
+
+
+def toeplitz_mixer(kappa, out=None, stream=None):
+    """The full mixer L [r][B][B] of the Toeplitz form of Mix from its kernel
+    taps kappa [r][B] (a device tensor, bf16 or float32; kappa[:, 0] unused),
+    written by the device into `out` (allocated when None) for use as the
+    weight "L"."""
+    import torch
+    L = load_library()
+    assert kappa.dim() == 2 and kappa.is_contiguous()
+    r, B = kappa.shape
+    dt = {torch.float32: XP_F32, torch.bfloat16: XP_BF16}[kappa.dtype]
+    if out is None:
+        out = torch.empty((r, B, B), dtype=kappa.dtype, device=kappa.device)
+    assert out.shape == (r, B, B) and out.dtype == kappa.dtype and out.is_contiguous()
+    _check(L.xp_toeplitz_mixer(_ptr(kappa), r, B, dt, _ptr(out), _stream(stream)),
+           "xp_toeplitz_mixer")
+    return out

@@ -89,3 +89,14 @@ def test_probes_reject_bad_arguments_without_a_gpu():
     assert L.xp_probe_mfma_bf16(0x1000, 0, 1, 0x1000, None) == X.XP_EINVAL
     assert L.xp_probe_mfma_bf16(0x1000, 1, -1, 0x1000, None) == X.XP_EINVAL
     assert L.xp_probe_mfma_bf16(0x1000, 1, 1, None, None) == X.XP_EINVAL
+
+
+def test_toeplitz_mixer_rejects_bad_arguments_without_a_gpu():
+    L = X.load_library()
+    p = ctypes.c_void_p(0x1000)         # never dereferenced: validation fails first
+    assert L.xp_toeplitz_mixer(None, 256, 16, X.XP_BF16, p, None) == X.XP_EINVAL
+    assert L.xp_toeplitz_mixer(p, 256, 16, X.XP_BF16, None, None) == X.XP_EINVAL
+    assert L.xp_toeplitz_mixer(p, 0, 16, X.XP_BF16, p, None) == X.XP_EINVAL
+    assert L.xp_toeplitz_mixer(p, 256, 0, X.XP_F32, p, None) == X.XP_EINVAL
+    assert L.xp_toeplitz_mixer(p, 256, 33, X.XP_F32, p, None) == X.XP_EINVAL
+    assert L.xp_toeplitz_mixer(p, 256, 16, 7, p, None) == X.XP_EINVAL

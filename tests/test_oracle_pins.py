@@ -132,22 +132,25 @@ def test_token_feeding_position_k_is_the_previous_guess():
 
 # ---------------------------------------------------------------- Mix ---------
 
-def test_toeplitz_mix_is_causal_depthwise_conv1d():
-    """Toeplitz L^(d)_{k,j} = kappa_d[k-j] makes Mix np.convolve (Toeplitz remark)."""
-    g = np.random.default_rng(7)
-    r, B = 5, 7
+@pytest.mark.parametrize("r,B", [(5, 7), (3, 1), (2, 32)])
+def test_toeplitz_mix_is_causal_depthwise_conv1d(r, B):
+    """The oracle's Toeplitz mixer makes Mix np.convolve with kernel
+    [1, kappa_d[1], ..., kappa_d[B-1]] (Toeplitz remark), whatever kappa_d[0] is."""
+    g = np.random.default_rng(7 + B)
     kappa = g.normal(size=(r, B))
-    kappa[:, 0] = 0.0       # strictly lower: no lag-0 term beyond the identity
-    L = np.zeros((r, B, B))
-    for k in range(B):
-        for j in range(k):
-            L[:, k, j] = kappa[:, k - j]
+    L = O.toeplitz_mixer(kappa)
+    assert L.shape == (r, B, B)
+    assert (L[:, np.triu(np.ones((B, B), bool))] == 0).all()          # strictly lower
     A = g.normal(size=(B, r))
     C = O.mix(L, A)
     for d in range(r):
         ker = kappa[d].copy()
         ker[0] = 1.0
         assert np.allclose(C[:, d], np.convolve(A[:, d], ker)[:B], rtol=1e-13, atol=1e-13)
+    # one hand-checked entry: position 3 of channel 0 at B = 7
+    if B == 7:
+        want = A[3, 0] + kappa[0, 1] * A[2, 0] + kappa[0, 2] * A[1, 0] + kappa[0, 3] * A[0, 0]
+        assert abs(C[3, 0] - want) < 1e-12
 
 
 def test_mix_never_reads_diagonal_or_upper_triangle():
