@@ -5,3 +5,4 @@ the CPU-baseline leg of bench.py.  The device path (paper_2608_02438_amd) never
 imports it and shares no code with it.
 """
 from .xpress_ref import *  # noqa: F401,F403
+from . import layer_ref  # noqa: F401,E402  (the context layer)
