@@ -215,6 +215,82 @@ xp_status xp_timing_read(xp_handle* h, float* ms_total, int32_t* pairs);
 xp_status xp_device_errors(xp_handle* h, uint32_t* out, void* stream);
 
 /*
+ * The context layer: one Qwen3-8B-shaped decoder layer over the positions of
+ * a drafted block, attending to each sequence's context KV.  The refiner does
+ * not read the context (Proposition 1); such layers belong to the drafter and
+ * the target (sections 3.1 and 5.1) and produce the hidden states h that the
+ * base readout s_k = W_lm h_k (section 4.1) consumes.  Pre-norm, no biases:
+ *   u  = RMSNorm(x) g_attn;  q = u Wq^T, k = u Wk^T, v = u Wv^T
+ *   q, k: RMSNorm over head_dim per head (g_q, g_k), then rotate-half RoPE at
+ *         position ctx_len[b] + i, angle pos * theta^(-2j/head_dim)
+ *   attention: query head h reads KV head h / (n_heads / n_kv); scores
+ *         q.k / sqrt(head_dim) over the context keys and the block's own keys
+ *         (block key j visible to block query i iff j <= i when causal, always
+ *         otherwise)
+ *   x1 = x + attn Wo^T;  h = x1 + (silu(u2 Wg^T) * (u2 Wu^T)) Wd^T,
+ *         u2 = RMSNorm(x1) g_mlp
+ * RMSNorm: y = x / sqrt(mean(x^2) + eps) * g.
+ *
+ * Weights: device pointers, bf16, row-major, rows as output units:
+ *   g_attn [H], Wq [n_heads*hd][H], Wk [n_kv*hd][H], Wv [n_kv*hd][H],
+ *   g_q [hd], g_k [hd], Wo [H][n_heads*hd], g_mlp [H], Wg [ffn][H],
+ *   Wu [ffn][H], Wd [H][ffn]
+ * Built: head_dim 128; n_heads / n_kv in {1, 2, 4, 8}; H, n_heads*128 and ffn
+ * multiples of 256; H <= 8192.
+ */
+typedef struct {
+  int32_t H, n_heads, n_kv, head_dim, ffn;
+  float eps;                         /* RMSNorm epsilon (1e-6 for Qwen3) */
+  float rope_theta;                  /* RoPE base (1e6 for Qwen3) */
+  const void* g_attn;
+  const void* Wq;
+  const void* Wk;
+  const void* Wv;
+  const void* g_q;
+  const void* g_k;
+  const void* Wo;
+  const void* g_mlp;
+  const void* Wg;
+  const void* Wu;
+  const void* Wd;
+} xp_layer_weights;
+
+typedef struct xp_layer xp_layer;
+
+/*
+ * Create a layer for up to max_batch blocks of up to max_B (<= 32) positions
+ * and contexts of up to max_ctx keys on the current device; allocates its
+ * workspace (freed by xp_layer_destroy).  The weights are referenced, not
+ * copied: they must stay valid while the layer is used.
+ * Errors: XP_EINVAL (null, sizes), XP_EUNSUPPORTED (shapes outside the built
+ * set), XP_ENOMEM, XP_EHIP.  *out is NULL on error.
+ */
+xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
+                          int32_t max_ctx, xp_layer** out);
+
+/*
+ * One forward of the layer over `batch` blocks of B positions, asynchronous on
+ * `stream`.  Device pointers:
+ *   x        [batch][B][H] bf16   the block's input hidden states
+ *   k_cache  [batch][C_max][n_kv][128] bf16  context keys (already normed and
+ *            rotated, as a KV cache holds them); v_cache the same for values
+ *   ctx_len  [batch] int32 in [0, C_max]: keys [0, ctx_len[b]) of sequence b
+ *            are read, the rest never (values outside are clamped)
+ *   h_f32    [batch][B][H] fp32 or NULL; h_bf16 [batch][B][H] bf16 or NULL:
+ *            the layer output (h_bf16 is the input of the base readout)
+ * causal: 1 = block key j visible to block query i iff j <= i; 0 = every block
+ * key visible (the drafter's bidirectional block).
+ * Errors: XP_EINVAL (null handle or input, batch, B or C_max outside what the
+ * layer was created for), before any launch; XP_EHIP if a launch fails.
+ */
+xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal, const void* x,
+                           const void* k_cache, const void* v_cache, int32_t C_max,
+                           const int32_t* ctx_len, float* h_f32, void* h_bf16, void* stream);
+
+/* Free the layer and its workspace (waits for the device first).  NULL is a no-op. */
+void xp_layer_destroy(xp_layer* L);
+
+/*
  * Measurement probes (not part of the method).  They give the measured peaks
  * that roofline fractions are also quoted against: the paper reports its
  * kernels' time on its own hardware (evaluation section, latency table), and a

@@ -31,8 +31,8 @@ Rounding points (the device stores these tensors in bf16 between kernels and
 feeds them to bf16 matrix products): u, the normed and rotated q and k, v,
 the normalised attention output, u2 and the SwiGLU activation are rounded to
 bf16 here too.  Everything else is fp64; the device's fp32 accumulation and
-its bf16 softmax numerators in the P.V product are covered by the parity
-tolerance.
+its softmax numerators, which enter the P.V product as two bf16 parts (about
+16 significant bits), are covered by the parity tolerance.
 """
 from __future__ import annotations
 

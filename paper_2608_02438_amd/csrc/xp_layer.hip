@@ -1,0 +1,528 @@
+// The context layer: one Qwen3-8B-shaped decoder layer over the positions of
+// a drafted block, attending to each sequence's context KV (the layer whose
+// output h the base readout s_k = W_lm h_k of section 4.1 consumes; the
+// refiner itself never reads the context, Proposition 1).
+//
+// Kernels, in launch order:
+//   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u
+//   k_linear      y = u W^T (+ residual): W streamed once from HBM, split over
+//                 the 8 waves of a workgroup along k, 16 output rows per
+//                 workgroup, 16 P positions per pass of the weight, the waves'
+//                 partial sums added in fixed order in LDS
+//   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
+//   k_attn        split-KV block attention: a workgroup takes 256 keys of one
+//                 KV head for 16 block positions, one wave per query head of
+//                 the group; S = K Q^T and O = P V on the matrix cores, the
+//                 chunk's V transposed through LDS
+//   k_attn_comb   merges the chunks of every query row in chunk order
+//   k_swiglu      silu(G) * U to bf16
+// Every reduction runs in a fixed order, so two runs give identical bits.
+#include "xp_internal.h"
+
+namespace xp {
+
+constexpr int kLinWaves = 8;        // k-split of k_linear
+constexpr int kLinChunk = 8;        // k steps (of 32) loaded before their products
+constexpr int kAttnKeys = 256;      // keys per attention workgroup
+constexpr int kAttnPad = 4;         // LDS row padding (bf16) of the transposed V
+constexpr int kHd = 128;            // head_dim (the only one built)
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm of one row per workgroup: u = bf16(x / sqrt(mean(x^2) + eps) * g).
+// The input is bf16 (xb) or fp32 (xf); x32, if given, receives the fp32 row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t* __restrict__ xb,
+                                                 const float* __restrict__ xf, int H,
+                                                 const uint16_t* __restrict__ g, float eps,
+                                                 float* __restrict__ x32,
+                                                 uint16_t* __restrict__ u) {
+  __shared__ float part[4];
+  const size_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  float ss = 0.f;
+  for (int i = tid; i < H; i += 256) {
+    const float v = xb ? bf16_to_f32(xb[row * H + i]) : xf[row * H + i];
+    ss += v * v;
+    if (x32) x32[row * H + i] = v;
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) part[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = (part[0] + part[1]) + (part[2] + part[3]);
+  const float r = 1.f / sqrtf(tot / (float)H + eps);
+  for (int i = tid; i < H; i += 256) {
+    const float v = xb ? bf16_to_f32(xb[row * H + i]) : xf[row * H + i];
+    u[row * H + i] = f32_to_bf16_rne(v * r * bf16_to_f32(g[i]));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// y[p][n] = sum_k X[p][k] W[n][k] (+ R[p][n]) for 16 rows n of W per
+// workgroup (blockIdx.x) and 16 P positions (blockIdx.y).  Wave w multiplies
+// the k range [w K/8, (w+1) K/8): 16-row x 32-k W fragments (A) against the
+// positions' X fragments (B) on v_mfma_f32_16x16x32_bf16, eight k steps of
+// loads issued before their products.  Lane l's accumulator element i is row
+// 4 (l / 16) + i of the tile for position l % 16, so one 16-byte store (or an
+// 8-byte bf16 store) per lane writes four consecutive outputs.
+// ---------------------------------------------------------------------------
+template <int P>
+__global__ __launch_bounds__(kLinWaves * kWave) void k_linear(
+    const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int K, int M, int ldx,
+    const float* __restrict__ R, int ldr, float* __restrict__ Y, uint16_t* __restrict__ Yb,
+    int ldy) {
+  __shared__ floatx4 red[kLinWaves][P][kWave];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  const int row0 = blockIdx.x * kTile, p0 = blockIdx.y * kTile * P;
+  const int kw = K / kLinWaves, nks = kw / 32;
+  const uint16_t* wp = W + (size_t)(row0 + li) * K + wave * kw + 8 * g;
+  const uint16_t* xp[P];
+  bool pv[P];
+#pragma unroll
+  for (int pb = 0; pb < P; ++pb) {
+    const int p = p0 + kTile * pb + li;
+    pv[pb] = p < M;
+    xp[pb] = X + (size_t)(pv[pb] ? p : 0) * ldx + wave * kw + 8 * g;
+  }
+  floatx4 acc[P];
+#pragma unroll
+  for (int pb = 0; pb < P; ++pb) acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const u32x4 zero{0u, 0u, 0u, 0u};
+  for (int c = 0; c < nks; c += kLinChunk) {
+    u32x4 a[kLinChunk], b[kLinChunk][P];
+#pragma unroll
+    for (int j = 0; j < kLinChunk; ++j) {
+      const int ks = c + j < nks ? c + j : nks - 1;   // past the end: re-read, not used
+      a[j] = ld16_nt(wp + 32 * ks);
+#pragma unroll
+      for (int pb = 0; pb < P; ++pb) b[j][pb] = ld16(xp[pb] + 32 * ks);
+    }
+#pragma unroll
+    for (int j = 0; j < kLinChunk; ++j)
+      if (c + j < nks)
+#pragma unroll
+        for (int pb = 0; pb < P; ++pb)
+          acc[pb] = Mfma<uint16_t>::mma(a[j], pv[pb] ? b[j][pb] : zero, acc[pb]);
+  }
+#pragma unroll
+  for (int pb = 0; pb < P; ++pb) red[wave][pb][lane] = acc[pb];
+  __syncthreads();
+  if (wave < P) {                                // wave pb adds the 8 partials of block pb
+    const int pb = wave;
+    floatx4 s = red[0][pb][lane];
+#pragma unroll
+    for (int w = 1; w < kLinWaves; ++w) s += red[w][pb][lane];
+    const int p = p0 + kTile * pb + li;
+    if (p < M) {
+      const int n = row0 + 4 * g;
+      if (R) s += *reinterpret_cast<const floatx4*>(R + (size_t)p * ldr + n);
+      if (Y) *reinterpret_cast<floatx4*>(Y + (size_t)p * ldy + n) = s;
+      if (Yb) {
+        const uint32_t lo = f32_to_bf16_rne(s[0]) | ((uint32_t)f32_to_bf16_rne(s[1]) << 16);
+        const uint32_t hi = f32_to_bf16_rne(s[2]) | ((uint32_t)f32_to_bf16_rne(s[3]) << 16);
+        *reinterpret_cast<uint2*>(Yb + (size_t)p * ldy + n) = make_uint2(lo, hi);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// QK-norm + RoPE: one wave per (position m, head slot): slots [0, nh) are the
+// q heads, [nh, nh + nkv) the k heads, [nh + nkv, nh + 2 nkv) the v heads
+// (converted only).  Lane l holds elements l and l + 64, the rotate-half pair
+// of frequency l; the angle is taken in double.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_qkrope(
+    const float* __restrict__ qkv, int ldq, int M, int B, int nh, int nkv,
+    const int32_t* __restrict__ ctx_len, int Cmax, const uint16_t* __restrict__ gq,
+    const uint16_t* __restrict__ gk, float eps, float theta, uint16_t* __restrict__ qn,
+    uint16_t* __restrict__ kb, uint16_t* __restrict__ vb) {
+  const int lane = threadIdx.x & 63;
+  const int nslots = nh + 2 * nkv;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= M * nslots) return;                   // whole wave
+  const int m = w / nslots, hs = w - m * nslots;
+  const float* src = qkv + (size_t)m * ldq + (size_t)hs * kHd;
+  float a = src[lane], b = src[lane + 64];
+  if (hs >= nh + nkv) {
+    uint16_t* dst = vb + ((size_t)m * nkv + (hs - nh - nkv)) * kHd;
+    dst[lane] = f32_to_bf16_rne(a);
+    dst[lane + 64] = f32_to_bf16_rne(b);
+    return;
+  }
+  const bool isq = hs < nh;
+  const float ss = wave_sum(a * a + b * b);
+  const float r = 1.f / sqrtf(ss / (float)kHd + eps);
+  const uint16_t* gw = isq ? gq : gk;
+  a = a * r * bf16_to_f32(gw[lane]);
+  b = b * r * bf16_to_f32(gw[lane + 64]);
+  int C = ctx_len[m / B];
+  C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
+  const double pos = (double)(C + m % B);
+  const double ang = pos * pow((double)theta, -2.0 * (double)lane / (double)kHd);
+  const float cs = (float)cos(ang), sn = (float)sin(ang);
+  uint16_t* dst = isq ? qn + ((size_t)m * nh + hs) * kHd : kb + ((size_t)m * nkv + (hs - nh)) * kHd;
+  dst[lane] = f32_to_bf16_rne(a * cs - b * sn);
+  dst[lane + 64] = f32_to_bf16_rne(b * cs + a * sn);
+}
+
+// ---------------------------------------------------------------------------
+// Split-KV block attention.  Grid (chunk s, KV head, sequence b x position
+// block pb); wave w is query head kvh * grp + w for block positions
+// 16 pb .. 16 pb + 15.  Key kk of sequence b is context key kk (kk < C) or
+// block key kk - C (C <= kk < C + B); keys from C + B on do not exist.
+//
+// S^T = K Q^T per 16-key tile (A: key rows, B: the wave's q): lane l holds
+// keys 16 t + 4 (l / 16) + i for query l % 16.  After the chunk maximum and
+// the numerators e = exp(s - m) (each as two bf16 parts), O = P V per 32
+// keys, once per part: the A operand's
+// eight k slots of lane l are its own e of tiles 2u and 2u + 1 (keys
+// 32 u + 4 (l/16) + 0..3 and 32 u + 16 + 4 (l/16) + 0..3), and the B operand
+// takes V of the same keys from the transposed LDS copy; the output lane holds
+// queries 4 (l / 16) + i for d = 16 dt + l % 16.  Written per (chunk, query):
+// O (relative to the chunk maximum m), m and l = sum of the numerators.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(512) void k_attn(
+    const uint16_t* __restrict__ qn, const uint16_t* __restrict__ kcache,
+    const uint16_t* __restrict__ vcache, const uint16_t* __restrict__ kb,
+    const uint16_t* __restrict__ vb, const int32_t* __restrict__ ctx_len, int Cmax, int B,
+    int npb, int nh, int nkv, int grp, int causal, int ns, float* __restrict__ opart,
+    float* __restrict__ mlpart) {
+  __shared__ __align__(16) uint16_t Vt[kHd][kAttnKeys + kAttnPad];
+  const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
+  const int b = z / npb, pb = z - b * npb;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  int C = ctx_len[b];
+  C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
+  const int nkeys = C + B, kbase = s * kAttnKeys;
+  const size_t pidx = (((size_t)z * nkv + kvh) * ns + s) * grp + wave;
+  float* op = opart + pidx * (kTile * kHd);
+  float* ml = mlpart + pidx * (2 * kTile);
+  if (kbase >= nkeys) {                          // whole workgroup: no key in this chunk
+    if (lane < kTile) {
+      ml[2 * lane] = -INFINITY;
+      ml[2 * lane + 1] = 0.f;
+    }
+    return;
+  }
+  // row of key kk (< nkeys) in the cache or in the block's own keys
+  auto krow = [&](int kk, const uint16_t* cache, const uint16_t* blk) -> const uint16_t* {
+    if (kk < C) return cache + (((size_t)b * Cmax + kk) * nkv + kvh) * kHd;
+    return blk + (((size_t)b * B + (kk - C)) * nkv + kvh) * kHd;
+  };
+
+  // V of the chunk, transposed: Vt[d][key]; keys past the end are zeros
+  for (int kl = threadIdx.x; kl < kAttnKeys; kl += blockDim.x) {
+    const int kk = kbase + kl;
+    const bool ok = kk < nkeys;
+    const uint16_t* src = krow(ok ? kk : nkeys - 1, vcache, vb);
+#pragma unroll
+    for (int c = 0; c < kHd / 8; ++c) {
+      const u32x4 v = ok ? ld16(src + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      Vt[8 * c + 0][kl] = (uint16_t)(v.x & 0xFFFFu);
+      Vt[8 * c + 1][kl] = (uint16_t)(v.x >> 16);
+      Vt[8 * c + 2][kl] = (uint16_t)(v.y & 0xFFFFu);
+      Vt[8 * c + 3][kl] = (uint16_t)(v.y >> 16);
+      Vt[8 * c + 4][kl] = (uint16_t)(v.z & 0xFFFFu);
+      Vt[8 * c + 5][kl] = (uint16_t)(v.z >> 16);
+      Vt[8 * c + 6][kl] = (uint16_t)(v.w & 0xFFFFu);
+      Vt[8 * c + 7][kl] = (uint16_t)(v.w >> 16);
+    }
+  }
+
+  // the wave's q (B operand): query li, head kvh * grp + wave
+  const int p = pb * kTile + li;
+  const bool qv = p < B;
+  const uint16_t* qs =
+      qn + (((size_t)b * B + (qv ? p : 0)) * nh + (size_t)kvh * grp + wave) * kHd + 8 * g;
+  u32x4 qf[kHd / 32];
+#pragma unroll
+  for (int ks = 0; ks < kHd / 32; ++ks) qf[ks] = qv ? ld16(qs + 32 * ks) : u32x4{0u, 0u, 0u, 0u};
+
+  constexpr int NT = kAttnKeys / kTile;
+  const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
+  floatx4 sc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int kk = kbase + kTile * t + li;       // A operand row
+    const uint16_t* kr = krow(kk < nkeys ? kk : nkeys - 1, kcache, kb) + 8 * g;
+    u32x4 kf[kHd / 32];
+#pragma unroll
+    for (int ks = 0; ks < kHd / 32; ++ks) kf[ks] = ld16(kr + 32 * ks);
+    floatx4 acc{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = kbase + kTile * t + 4 * g + i;
+      const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
+      sc[t][i] = vis ? acc[i] * scale : -INFINITY;
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  // numerators e as a sum of two bf16 parts (hi = bf16(e), lo = bf16(e - hi):
+  // about 16 significant bits), both multiplied into O; the sum l is taken
+  // over the same two parts
+  uint32_t eh[NT][2], el[NT][2];
+  float lsum = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    uint16_t h[4], lo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float e = mx == -INFINITY ? 0.f : __expf(sc[t][i] - mx);
+      h[i] = f32_to_bf16_rne(e);
+      lo[i] = f32_to_bf16_rne(e - bf16_to_f32(h[i]));
+      lsum += bf16_to_f32(h[i]) + bf16_to_f32(lo[i]);
+    }
+    eh[t][0] = h[0] | ((uint32_t)h[1] << 16);
+    eh[t][1] = h[2] | ((uint32_t)h[3] << 16);
+    el[t][0] = lo[0] | ((uint32_t)lo[1] << 16);
+    el[t][1] = lo[2] | ((uint32_t)lo[3] << 16);
+  }
+  lsum += __shfl_xor(lsum, 16, kWave);
+  lsum += __shfl_xor(lsum, 32, kWave);
+  __syncthreads();                               // Vt complete
+
+  floatx4 o[kHd / 16];
+#pragma unroll
+  for (int dt = 0; dt < kHd / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < NT / 2; ++u) {
+    const u32x4 ph{eh[2 * u][0], eh[2 * u][1], eh[2 * u + 1][0], eh[2 * u + 1][1]};
+    const u32x4 pl{el[2 * u][0], el[2 * u][1], el[2 * u + 1][0], el[2 * u + 1][1]};
+#pragma unroll
+    for (int dt = 0; dt < kHd / 16; ++dt) {
+      const int d = 16 * dt + li;
+      const uint2 v0 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 4 * g]);
+      const uint2 v1 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 16 + 4 * g]);
+      const u32x4 vv{v0.x, v0.y, v1.x, v1.y};
+      o[dt] = Mfma<uint16_t>::mma(pl, vv, o[dt]);
+      o[dt] = Mfma<uint16_t>::mma(ph, vv, o[dt]);
+    }
+  }
+#pragma unroll
+  for (int dt = 0; dt < kHd / 16; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) op[(4 * g + i) * kHd + 16 * dt + li] = o[dt][i];
+  if (lane < kTile) {
+    ml[2 * lane] = mx;
+    ml[2 * lane + 1] = lsum;
+  }
+}
+
+// One wave per (position m, query head h): merge the chunks in order,
+// attn = sum_s e^(m_s - M) O_s / sum_s e^(m_s - M) l_s, to bf16.
+__global__ __launch_bounds__(256) void k_attn_comb(const float* __restrict__ opart,
+                                                   const float* __restrict__ mlpart, int M, int B,
+                                                   int npb, int nh, int nkv, int grp, int ns,
+                                                   uint16_t* __restrict__ attn) {
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= M * nh) return;                       // whole wave
+  const int m = w / nh, h = w - m * nh;
+  const int b = m / B, p = m - b * B, pb = p / kTile, q = p - pb * kTile;
+  const int kvh = h / grp, wv = h - kvh * grp, z = b * npb + pb;
+  const size_t base = (((size_t)z * nkv + kvh) * ns) * grp + wv;
+  float mm = -INFINITY;
+  for (int s = 0; s < ns; ++s) {
+    const size_t pi = base + (size_t)s * grp;
+    const float ms = mlpart[pi * 2 * kTile + 2 * q], ls = mlpart[pi * 2 * kTile + 2 * q + 1];
+    if (ls > 0.f) mm = fmaxf(mm, ms);
+  }
+  float L = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const size_t pi = base + (size_t)s * grp;
+    const float ms = mlpart[pi * 2 * kTile + 2 * q], ls = mlpart[pi * 2 * kTile + 2 * q + 1];
+    if (ls > 0.f) {
+      const float f = __expf(ms - mm);
+      L += ls * f;
+      o0 += f * opart[pi * (kTile * kHd) + q * kHd + lane];
+      o1 += f * opart[pi * (kTile * kHd) + q * kHd + lane + 64];
+    }
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;     // L > 0: every query sees its own key
+  uint16_t* dst = attn + (size_t)m * nh * kHd + (size_t)h * kHd;
+  dst[lane] = f32_to_bf16_rne(o0 * inv);
+  dst[lane + 64] = f32_to_bf16_rne(o1 * inv);
+}
+
+__global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ G,
+                                                const float* __restrict__ U, size_t n,
+                                                uint16_t* __restrict__ act) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float gv = G[i];
+  act[i] = f32_to_bf16_rne(gv / (1.f + __expf(-gv)) * U[i]);
+}
+
+}  // namespace xp
+
+using namespace xp;
+
+struct xp_layer {
+  int H, nh, nkv, ffn, grp;
+  float eps, theta;
+  const uint16_t *g_attn, *Wq, *Wk, *Wv, *g_q, *g_k, *Wo, *g_mlp, *Wg, *Wu, *Wd;
+  int max_batch, max_B, max_ctx, nsmax;
+  void* ws = nullptr;
+  float* x32 = nullptr;
+  uint16_t* u = nullptr;
+  float* qkv = nullptr;
+  uint16_t *qn = nullptr, *kb = nullptr, *vb = nullptr;
+  float *opart = nullptr, *mlpart = nullptr;
+  uint16_t* attn = nullptr;
+  float *x1 = nullptr, *G = nullptr, *U = nullptr, *h32 = nullptr;
+  uint16_t* act = nullptr;
+};
+
+static int attn_chunks(int C_max, int B) { return (C_max + B + kAttnKeys - 1) / kAttnKeys; }
+
+extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
+                                     int32_t max_ctx, xp_layer** out) {
+  if (out == nullptr) return XP_EINVAL;
+  *out = nullptr;
+  if (w == nullptr || max_batch < 1 || max_batch > 4096 || max_B < 1 || max_B > 32 ||
+      max_ctx < 0 || max_ctx > (1 << 20))
+    return XP_EINVAL;
+  const void* ptrs[] = {w->g_attn, w->Wq, w->Wk, w->Wv, w->g_q, w->g_k,
+                        w->Wo,     w->g_mlp, w->Wg, w->Wu, w->Wd};
+  for (const void* p : ptrs)
+    if (p == nullptr) return XP_EINVAL;
+  if (w->H < 1 || w->n_heads < 1 || w->n_kv < 1 || w->ffn < 1 || w->head_dim < 1 ||
+      !(w->eps >= 0.f) || !(w->rope_theta > 0.f))
+    return XP_EINVAL;
+  const int grp = w->n_heads / w->n_kv;
+  if (w->head_dim != kHd || w->n_heads % w->n_kv != 0 ||
+      (grp != 1 && grp != 2 && grp != 4 && grp != 8) || w->H % 256 != 0 || w->H > 8192 ||
+      (w->n_heads * kHd) % 256 != 0 || w->ffn % 256 != 0 || w->ffn > (1 << 16))
+    return XP_EUNSUPPORTED;
+  xp_layer* L = new (std::nothrow) xp_layer();
+  if (L == nullptr) return XP_ENOMEM;
+  L->H = w->H;
+  L->nh = w->n_heads;
+  L->nkv = w->n_kv;
+  L->ffn = w->ffn;
+  L->grp = grp;
+  L->eps = w->eps;
+  L->theta = w->rope_theta;
+  L->g_attn = (const uint16_t*)w->g_attn;
+  L->Wq = (const uint16_t*)w->Wq;
+  L->Wk = (const uint16_t*)w->Wk;
+  L->Wv = (const uint16_t*)w->Wv;
+  L->g_q = (const uint16_t*)w->g_q;
+  L->g_k = (const uint16_t*)w->g_k;
+  L->Wo = (const uint16_t*)w->Wo;
+  L->g_mlp = (const uint16_t*)w->g_mlp;
+  L->Wg = (const uint16_t*)w->Wg;
+  L->Wu = (const uint16_t*)w->Wu;
+  L->Wd = (const uint16_t*)w->Wd;
+  L->max_batch = max_batch;
+  L->max_B = max_B;
+  L->max_ctx = max_ctx;
+  L->nsmax = attn_chunks(max_ctx, max_B);
+  const size_t Mx = (size_t)max_batch * max_B, H = L->H, nhd = (size_t)L->nh * kHd,
+               kvd = (size_t)L->nkv * kHd, F = L->ffn;
+  const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
+  const size_t nparts = zmax * L->nkv * L->nsmax * grp;
+  struct Slice {
+    void** p;
+    size_t bytes;
+  } sl[] = {
+      {(void**)&L->x32, Mx * H * 4},           {(void**)&L->u, Mx * H * 2},
+      {(void**)&L->qkv, Mx * (nhd + 2 * kvd) * 4}, {(void**)&L->qn, Mx * nhd * 2},
+      {(void**)&L->kb, Mx * kvd * 2},          {(void**)&L->vb, Mx * kvd * 2},
+      {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
+      {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
+      {(void**)&L->G, Mx * F * 4},             {(void**)&L->U, Mx * F * 4},
+      {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
+  };
+  size_t total = 0;
+  for (auto& s : sl) total += (s.bytes + 255) / 256 * 256;
+  if (hipMalloc(&L->ws, total) != hipSuccess) {
+    delete L;
+    return XP_ENOMEM;
+  }
+  char* p = static_cast<char*>(L->ws);
+  for (auto& s : sl) {
+    *s.p = p;
+    p += (s.bytes + 255) / 256 * 256;
+  }
+  *out = L;
+  return XP_OK;
+}
+
+extern "C" void xp_layer_destroy(xp_layer* L) {
+  if (L == nullptr) return;
+  (void)hipDeviceSynchronize();
+  if (L->ws) (void)hipFree(L->ws);
+  delete L;
+}
+
+// y [M][N] (row stride ldy) = X [M][K] W^T (+ R): P = 1, 2 or 4 position blocks per pass
+static void linear(const uint16_t* W, int N, int K, const uint16_t* X, int M, const float* R,
+                   int ldr, float* Y, uint16_t* Yb, int ldy, hipStream_t st) {
+  const int nb = (M + kTile - 1) / kTile;
+  const int P = nb >= 4 ? 4 : (nb >= 2 ? 2 : 1);
+  const dim3 grid(N / kTile, (M + kTile * P - 1) / (kTile * P)), block(kLinWaves * kWave);
+  if (P == 4)
+    hipLaunchKernelGGL(k_linear<4>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
+  else if (P == 2)
+    hipLaunchKernelGGL(k_linear<2>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
+  else
+    hipLaunchKernelGGL(k_linear<1>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
+}
+
+extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal,
+                                      const void* x, const void* k_cache, const void* v_cache,
+                                      int32_t C_max, const int32_t* ctx_len, float* h_f32,
+                                      void* h_bf16, void* stream) {
+  if (L == nullptr || x == nullptr || k_cache == nullptr || v_cache == nullptr ||
+      ctx_len == nullptr || batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B ||
+      C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1) || (causal != 0 && causal != 1))
+    return XP_EINVAL;
+  if (attn_chunks(C_max, B) > L->nsmax) return XP_EINVAL;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
+  const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
+  const int npb = (B + kTile - 1) / kTile, ns = attn_chunks(C_max, B);
+  float* hout = h_f32 ? h_f32 : L->h32;
+
+  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, st, (const uint16_t*)x, (const float*)nullptr,
+                     H, L->g_attn, L->eps, L->x32, L->u);
+  linear(L->Wq, nhd, H, L->u, M, nullptr, 0, L->qkv, nullptr, ldq, st);
+  linear(L->Wk, kvd, H, L->u, M, nullptr, 0, L->qkv + nhd, nullptr, ldq, st);
+  linear(L->Wv, kvd, H, L->u, M, nullptr, 0, L->qkv + nhd + kvd, nullptr, ldq, st);
+  const int qk_waves = M * (nh + 2 * nkv);
+  hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M, B, nh,
+                     nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn, L->kb, L->vb);
+  hipLaunchKernelGGL(k_attn, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0, st, L->qn,
+                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb, ctx_len,
+                     C_max, B, npb, nh, nkv, grp, causal, ns, L->opart, L->mlpart);
+  const int cw = M * nh;
+  hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart, L->mlpart, M, B,
+                     npb, nh, nkv, grp, ns, L->attn);
+  linear(L->Wo, H, nhd, L->attn, M, L->x32, H, L->x1, nullptr, H, st);
+  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, st, (const uint16_t*)nullptr, L->x1, H,
+                     L->g_mlp, L->eps, (float*)nullptr, L->u);
+  linear(L->Wg, F, H, L->u, M, nullptr, 0, L->G, nullptr, F, st);
+  linear(L->Wu, F, H, L->u, M, nullptr, 0, L->U, nullptr, F, st);
+  const size_t na = (size_t)M * F;
+  hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, L->G, L->U,
+                     na, L->act);
+  linear(L->Wd, H, F, L->act, M, L->x1, H, hout, (uint16_t*)h_bf16, H, st);
+  return hipGetLastError() == hipSuccess ? XP_OK : XP_EHIP;
+}

@@ -23,7 +23,9 @@ XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE = 1, 2
 
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
-           "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16", "xp_toeplitz_mixer")
+           "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16", "xp_toeplitz_mixer",
+           "xp_layer_create", "xp_layer_forward", "xp_layer_destroy")
+LAYER_WEIGHT_NAMES = ("g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp", "Wg", "Wu", "Wd")
 STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
 
 
@@ -40,6 +42,13 @@ class _Weights(ctypes.Structure):
 
 
 WEIGHT_NAMES = ("W_lm", "W_h", "W_g", "W_e", "W_in", "L", "W_1", "W_2", "W_r")
+
+class _LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("H", "n_heads", "n_kv", "head_dim", "ffn")] + [
+        ("eps", ctypes.c_float), ("rope_theta", ctypes.c_float)] + [
+        (n, ctypes.c_void_p) for n in ("g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp",
+                                       "Wg", "Wu", "Wd")]
+
 
 _lib = None
 
@@ -77,6 +86,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_probe_mfma_bf16.restype = i32
     L.xp_toeplitz_mixer.argtypes = [vp, i32, i32, i32, vp, vp]
     L.xp_toeplitz_mixer.restype = i32
+    L.xp_layer_create.argtypes = [ctypes.POINTER(_LayerWeights), i32, i32, i32, ctypes.POINTER(vp)]
+    L.xp_layer_create.restype = i32
+    L.xp_layer_forward.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
+    L.xp_layer_forward.restype = i32
+    L.xp_layer_destroy.argtypes = [vp]
+    L.xp_layer_destroy.restype = None
     _lib = L
     return L
 
@@ -279,3 +294,53 @@ def toeplitz_mixer(kappa, out=None, stream=None):
     _check(L.xp_toeplitz_mixer(_ptr(kappa), r, B, dt, _ptr(out), _stream(stream)),
            "xp_toeplitz_mixer")
     return out
+
+
+class Layer:
+    """The context layer (xp_layer_*): `weights` maps LAYER_WEIGHT_NAMES to
+    bf16 device tensors, which must outlive the layer."""
+
+    def __init__(self, weights: Dict[str, object], H: int, n_heads: int, n_kv: int, ffn: int,
+                 max_batch: int, max_B: int, max_ctx: int, eps: float = 1e-6,
+                 theta: float = 1e6, head_dim: int = 128):
+        L = load_library()
+        self._keep = dict(weights)
+        w = _LayerWeights(H=H, n_heads=n_heads, n_kv=n_kv, head_dim=head_dim, ffn=ffn, eps=eps,
+                          rope_theta=theta)
+        for n in LAYER_WEIGHT_NAMES:
+            setattr(w, n, _ptr(weights[n]))
+        h = ctypes.c_void_p(0)
+        _check(L.xp_layer_create(ctypes.byref(w), max_batch, max_B, max_ctx, ctypes.byref(h)),
+               "xp_layer_create")
+        self._h = h
+        self.H = H
+
+    def forward(self, x, k_cache, v_cache, ctx_len, causal=True, h_f32=None, h_bf16=None,
+                stream=None):
+        """x [batch][B][H] bf16; k_cache, v_cache [batch][C_max][n_kv][128] bf16;
+        ctx_len [batch] int32 (device tensors).  Returns (h_f32, h_bf16)."""
+        import torch
+        L = load_library()
+        batch, B, H = x.shape
+        C_max = k_cache.shape[1]
+        if h_f32 is None:
+            h_f32 = torch.empty((batch, B, H), dtype=torch.float32, device=x.device)
+        if h_bf16 is None:
+            h_bf16 = torch.empty((batch, B, H), dtype=torch.bfloat16, device=x.device)
+        for t in (x, k_cache, v_cache, ctx_len, h_f32, h_bf16):
+            assert t.is_contiguous()
+        _check(L.xp_layer_forward(self._h, batch, B, 1 if causal else 0, _ptr(x), _ptr(k_cache),
+                                  _ptr(v_cache), C_max, _ptr(ctx_len), _ptr(h_f32), _ptr(h_bf16),
+                                  _stream(stream)), "xp_layer_forward")
+        return h_f32, h_bf16
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load_library().xp_layer_destroy(self._h)
+            self._h = None
+
+    def __del__(self):  # pragma: no cover
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -35,6 +35,10 @@ STREAMS = {
     "W_2": 8, "W_r": 9, "h": 10, "anchor": 11, "seed_ids": 12, "u_draft": 13,
     "r_accept": 14, "u_res": 15, "coins": 16, "alts": 17, "target_logits": 18,
     "p_match": 19, "ctx_len": 20,
+    # the context layer
+    "layer.g_attn": 21, "layer.Wq": 22, "layer.Wk": 23, "layer.Wv": 24, "layer.g_q": 25,
+    "layer.g_k": 26, "layer.Wo": 27, "layer.g_mlp": 28, "layer.Wg": 29, "layer.Wu": 30,
+    "layer.Wd": 31, "layer.x": 32, "layer.k": 33, "layer.v": 34, "layer.ctx": 35,
 }
 _BLOCK = 1 << 22          # elements per independently keyed block
 _THREADS = max(1, min(16, os.cpu_count() or 1))
@@ -230,3 +234,56 @@ def normal_f32_row(w: Workload, b: int, shape, sigma: float) -> np.ndarray:
     with ThreadPoolExecutor(_THREADS) as ex:
         list(ex.map(work, enumerate(_blocks(n))))
     return out.reshape(shape)
+
+
+# --- the context layer (the configuration's decoder-layer fields) --------------
+
+LAYER_SHAPES = {
+    "g_attn": lambda w: (w.H,),
+    "Wq": lambda w: (w.n_heads * w.head_dim, w.H),
+    "Wk": lambda w: (w.n_kv_heads * w.head_dim, w.H),
+    "Wv": lambda w: (w.n_kv_heads * w.head_dim, w.H),
+    "g_q": lambda w: (w.head_dim,),
+    "g_k": lambda w: (w.head_dim,),
+    "Wo": lambda w: (w.H, w.n_heads * w.head_dim),
+    "g_mlp": lambda w: (w.H,),
+    "Wg": lambda w: (w.ffn, w.H),
+    "Wu": lambda w: (w.ffn, w.H),
+    "Wd": lambda w: (w.H, w.ffn),
+}
+
+
+def make_layer_weights(w: Workload) -> Dict[str, np.ndarray]:
+    """bf16 bit patterns: projections N(0, w_sigma^2); norm weights 1 + N(0, 0.1^2)."""
+    out = {}
+    for n, shape_fn in LAYER_SHAPES.items():
+        if n.startswith("g_"):
+            f = 1.0 + normal_f32(w, "layer." + n, shape_fn(w), 0.1)
+            out[n] = f32_to_bf16_bits(f)
+        else:
+            out[n] = normal_bf16(w, "layer." + n, shape_fn(w), w.w_sigma)
+    return out
+
+
+@dataclass
+class LayerInputs:
+    x: np.ndarray          # [batch][B][H] bf16 bits: block hidden states, N(0, h_sigma^2)
+    k_cache: np.ndarray    # [batch][C_max][n_kv][hd] bf16 bits, N(0, 1) (post-norm keys)
+    v_cache: np.ndarray    # [batch][C_max][n_kv][hd] bf16 bits, N(0, 1)
+    ctx_len: np.ndarray    # [batch] int32: ctx_len, or U{lo..hi} per sequence
+
+
+def make_layer_inputs(w: Workload, batch: Optional[int] = None,
+                      c_max: Optional[int] = None) -> LayerInputs:
+    batch = w.batch if batch is None else batch
+    if w.ctx_len_range is not None:
+        lo, hi = w.ctx_len_range
+        ctx = _rng(w, "layer.ctx").integers(lo, hi + 1, batch).astype(np.int32)
+    else:
+        ctx = np.full(batch, w.ctx_len or 0, dtype=np.int32)
+    cm = int(ctx.max()) if c_max is None else c_max
+    cm = max(cm, 1)
+    kv = (batch, cm, w.n_kv_heads, w.head_dim)
+    return LayerInputs(x=normal_bf16(w, "layer.x", (batch, w.B, w.H), w.h_sigma),
+                       k_cache=normal_bf16(w, "layer.k", kv, 1.0),
+                       v_cache=normal_bf16(w, "layer.v", kv, 1.0), ctx_len=ctx)

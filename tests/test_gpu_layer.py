@@ -1,0 +1,120 @@
+"""The context layer on the device vs the fp64 oracle, through the C ABI
+(needs an MI355X).
+
+Small shapes span several k-split chunks of every projection, several
+256-key attention chunks with ragged context lengths (0, chunk boundaries),
+every built query-group size and blocks of 1, 8, 16 and 32 positions; the
+full-size case runs the Qwen3-8B layer at batch 1 with a 2048-key context.
+
+Tolerance: h is compared in fp32 against the oracle's fp64 h with the bf16
+rounding points of the device (u, q, k, v, the attention output, u2 and the
+SwiGLU activation); what remains is fp32 accumulation order, the softmax
+numerators of P.V (two bf16 parts each) and the rare bf16 rounding that the fp32 and fp64
+values of an intermediate take to different neighbours.  The bar is the
+2e-2 absolute of bf16 logits; with the numerators in one bf16 part instead of
+two the Qwen3-shape case would reach 0.020 (measured in the oracle), with two
+it stays near 1e-3.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+from synth.configs import QWEN_B1
+
+pytestmark = pytest.mark.gpu
+
+ATOL = 2e-2
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _case(H, nh, nkv, ffn, B, batch, ctx, index, c_max=None):
+    w = synth.scaled(QWEN_B1, index=index, H=H, B=B, batch=batch, n_heads=nh, n_kv_heads=nkv,
+                     ffn=ffn, ctx_len=None, ctx_len_range=None)
+    weights = synth.make_layer_weights(w)
+    inp = synth.make_layer_inputs(w, c_max=c_max if c_max is not None else max(max(ctx), 1))
+    inp.ctx_len = np.asarray(ctx, dtype=np.int32)
+    return w, weights, inp
+
+
+def _run(w, weights, inp, causal=True, max_ctx=None, layer=None):
+    import torch
+    from paper_2608_02438_amd.xpress import LAYER_WEIGHT_NAMES, Layer, device_tensor
+    dw = {n: device_tensor(weights[n]) for n in LAYER_WEIGHT_NAMES}
+    if layer is None:
+        layer = Layer(dw, w.H, w.n_heads, w.n_kv_heads, w.ffn, max_batch=w.batch, max_B=w.B,
+                      max_ctx=max_ctx or inp.k_cache.shape[1])
+    dev = [device_tensor(a) for a in (inp.x, inp.k_cache, inp.v_cache, inp.ctx_len)]
+    h32, hb = layer.forward(*dev, causal=causal)
+    torch.cuda.synchronize()
+    hb_bits = hb.cpu().view(torch.int16).numpy().view(np.uint16)
+    return h32.cpu().numpy(), hb_bits, layer, dw
+
+
+def _check(w, weights, inp, h32, hb_bits, causal=True):
+    P = O.layer_ref.LayerParams.from_arrays(weights, w.n_heads, w.n_kv_heads, w.head_dim)
+    ref = O.layer_ref.layer_forward(P, inp.x, inp.k_cache, inp.v_cache, inp.ctx_len, causal)
+    err = np.abs(h32 - ref)
+    _say(f"  max|h|={np.abs(ref).max():.3g} max|dh|={err.max():.3g} mean|dh|={err.mean():.3g}")
+    assert np.all(np.isfinite(h32))
+    assert err.max() <= ATOL
+    # the bf16 output is the rounding of the fp32 one
+    assert np.array_equal(hb_bits, synth.f32_to_bf16_bits(h32))
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("H,nh,nkv,ffn,B,batch,ctx", [
+    (256, 4, 2, 512, 8, 3, [600, 3, 256]),          # group 2, three KV chunks, ragged
+    (512, 8, 2, 768, 16, 2, [0, 257]),              # group 4 (the Qwen3 ratio), no context
+    (256, 8, 1, 256, 32, 1, [300]),                 # group 8, two position blocks
+    (256, 2, 2, 256, 1, 2, [1, 511]),               # group 1, blocks of one position
+])
+def test_layer_matches_oracle(H, nh, nkv, ffn, B, batch, ctx, causal):
+    _say(f"case: layer H={H} heads={nh}/{nkv} ffn={ffn} B={B} batch={batch} ctx={ctx} "
+         f"causal={causal}")
+    w, weights, inp = _case(H, nh, nkv, ffn, B, batch, ctx, index=700 + H + B)
+    h32, hb, layer, _ = _run(w, weights, inp, causal)
+    _check(w, weights, inp, h32, hb, causal)
+    layer.close()
+
+
+def test_layer_run_to_run_and_cache_past_context_unread():
+    import torch
+    from paper_2608_02438_amd.xpress import device_tensor
+    _say("case: layer determinism, H=512 heads 8/2 B=16 batch=2 ctx=[100, 700]")
+    w, weights, inp = _case(512, 8, 2, 512, 16, 2, [100, 700], index=777)
+    h1, b1, layer, _ = _run(w, weights, inp)
+    h2, b2, _, _ = _run(w, weights, inp, layer=layer)
+    assert np.array_equal(h1, h2) and np.array_equal(b1, b2)
+    inp.k_cache[0, 100:] = 0x7FC0                  # NaN bit patterns past sequence 0's context
+    inp.v_cache[0, 100:] = 0x7FC0
+    h3, _, _, _ = _run(w, weights, inp, layer=layer)
+    assert np.array_equal(h3, h1)
+    layer.close()
+
+
+def test_layer_rejects_bad_calls():
+    import torch
+    from paper_2608_02438_amd.xpress import XpError
+    w, weights, inp = _case(256, 4, 2, 256, 8, 1, [10], index=790)
+    _, _, layer, _ = _run(w, weights, inp, max_ctx=10)
+    from paper_2608_02438_amd.xpress import device_tensor
+    x, k, v, c = (device_tensor(a) for a in (inp.x, inp.k_cache, inp.v_cache, inp.ctx_len))
+    big = torch.zeros((1, 64, 2, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(XpError):
+        layer.forward(x, big, big, c)              # C_max beyond the layer's max_ctx
+    x2 = torch.zeros((2, 8, 256), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(XpError):
+        layer.forward(x2, k, v, c)                 # batch beyond max_batch
+    layer.close()
+
+
+def test_layer_qwen3_shape_batch1_ctx2048():
+    _say("case: layer Qwen3-8B shape H=4096 heads 32/8 ffn=12288 B=16 batch=1 ctx=2048")
+    w, weights, inp = _case(4096, 32, 8, 12288, 16, 1, [2048], index=901)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
