@@ -225,6 +225,10 @@ def main():
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured HBM and MFMA peaks")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--layer", action="store_true",
+                    help="time the context layer (the Qwen3-8B decoder layer over the block "
+                         "and its context KV) on the workload's shapes and print that line "
+                         "instead")
     ap.add_argument("--k-sweep", action="store_true",
                     help="time refine + verify for K = 1..8 passes, fixed K and with the "
                          "per-batch early exit, and print that table as one JSON line instead")
@@ -245,6 +249,9 @@ def main():
     from paper_2608_02438_amd.xpress import device_tensor, refiner_from_arrays
 
     wl = synth.BY_NAME[args.workload]
+    if args.layer:
+        layer_bench(args, wl)
+        return
     log(f"[bench] workload {wl.name}: generating inputs")
     weights = synth.make_weights(wl)
     inp = synth.make_inputs(wl)
@@ -377,6 +384,87 @@ def main():
     else:
         line["cpu_baseline"] = None
     ref.close()
+    print(json.dumps(line), flush=True)
+
+
+LAYER_METRIC = ("context-layer forwards/sec (Qwen3-8B decoder layer over the drafted block "
+                "and its context KV); % HBM peak")
+
+
+def layer_bench(args, wl):
+    """One step = one xp_layer_forward over the workload's batch of blocks with
+    its context lengths.  The forward streams every weight once (it is
+    HBM-bound at these position counts), so the roofline is the forward's
+    algorithmic bytes (weights, the context K and V it reads, its inputs and
+    outputs) over its time, against the HBM peak."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_02438_amd.xpress import LAYER_WEIGHT_NAMES, Layer, device_tensor
+
+    log(f"[bench] context layer, workload {wl.name}: generating weights and the KV cache")
+    weights = synth.make_layer_weights(wl)
+    inp = synth.make_layer_inputs(wl)
+    dw = {n: device_tensor(weights[n]) for n in LAYER_WEIGHT_NAMES}
+    C_max = inp.k_cache.shape[1]
+    layer = Layer(dw, wl.H, wl.n_heads, wl.n_kv_heads, wl.ffn, max_batch=wl.batch, max_B=wl.B,
+                  max_ctx=C_max)
+    x, kc, vc, cl = (device_tensor(a) for a in (inp.x, inp.k_cache, inp.v_cache, inp.ctx_len))
+    M = wl.batch * wl.B
+    h32 = torch.empty((wl.batch, wl.B, wl.H), dtype=torch.float32, device="cuda")
+    hb = torch.empty((wl.batch, wl.B, wl.H), dtype=torch.bfloat16, device="cuda")
+    for _ in range(args.warmup):
+        layer.forward(x, kc, vc, cl, h_f32=h32, h_bf16=hb)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        layer.forward(x, kc, vc, cl, h_f32=h32, h_bf16=hb)
+    e1.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    wbytes = sum(int(weights[n].size) * 2 for n in LAYER_WEIGHT_NAMES)
+    kvbytes = int(np.sum(inp.ctx_len)) * wl.n_kv_heads * wl.head_dim * 2 * 2
+    iobytes = M * wl.H * (2 + 4 + 2)
+    nbytes = wbytes + kvbytes + iobytes
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    log(f"[bench] layer {ms * 1e3:.1f} us per forward, {gbs:.0f} GB/s "
+        f"({100 * gbs / HBM_PEAK_GBS:.1f}% of the HBM peak)")
+    line = {
+        "metric": LAYER_METRIC, "value": 1e3 / ms, "unit": "forwards/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded N(0,0.02^2) bf16 projections, norm weights 1+N(0,0.1^2), "
+                "N(0,1) hidden states and context K/V",
+        "config": {"workload": wl.name + "+context-layer", "batch": wl.batch, "block": wl.B,
+                   "H": wl.H, "heads": wl.n_heads, "kv_heads": wl.n_kv_heads,
+                   "head_dim": wl.head_dim, "ffn": wl.ffn,
+                   "ctx_len": [int(c) for c in inp.ctx_len[:8]]},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "xp_layer_forward (all of its kernels)",
+                     "algorithmic_bytes_per_launch": nbytes, "weight_bytes": wbytes,
+                     "kv_bytes": kvbytes, "launch_us": ms * 1e3},
+        "wall_s": elapsed,
+    }
+    if not args.no_cpu:
+        import oracle as O
+        log("[bench] CPU oracle baseline of the layer (one block, all threads)")
+        P = O.layer_ref.LayerParams.from_arrays(weights, wl.n_heads, wl.n_kv_heads, wl.head_dim)
+        t = time.perf_counter()
+        O.layer_ref.layer_forward(P, inp.x[:1], inp.k_cache[:1], inp.v_cache[:1],
+                                  inp.ctx_len[:1])
+        dt = time.perf_counter() - t
+        line["cpu_baseline"] = {"value": 1.0 / dt, "unit": "blocks/s", "kind": "oracle",
+                                "cores": os.cpu_count(),
+                                "sample": "one block of the workload through the fp64 layer "
+                                          "oracle (weights already widened)"}
+    else:
+        line["cpu_baseline"] = None
+    layer.close()
     print(json.dumps(line), flush=True)
 
 

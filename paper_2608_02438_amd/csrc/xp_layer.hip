@@ -5,17 +5,17 @@
 //
 // Kernels, in launch order:
 //   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u
-//   k_linear      y = u W^T (+ residual): W streamed once from HBM, split over
-//                 the 8 waves of a workgroup along k, 16 output rows per
+//   k_linear      y = u W^T (+ residual), or the SwiGLU product of the gate
+//                 and up projections: W streamed once from HBM, split over the
+//                 8 waves of a workgroup along k, 16 output rows per
 //                 workgroup, 16 P positions per pass of the weight, the waves'
 //                 partial sums added in fixed order in LDS
 //   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
 //   k_attn        split-KV block attention: a workgroup takes 256 keys of one
 //                 KV head for 16 block positions, one wave per query head of
-//                 the group; S = K Q^T and O = P V on the matrix cores, the
-//                 chunk's V transposed through LDS
+//                 the group; the chunk's K and V (transposed) staged in LDS in
+//                 one memory round, S = K Q^T and O = P V on the matrix cores
 //   k_attn_comb   merges the chunks of every query row in chunk order
-//   k_swiglu      silu(G) * U to bf16
 // Every reduction runs in a fixed order, so two runs give identical bits.
 #include "xp_internal.h"
 
@@ -35,98 +35,155 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // ---------------------------------------------------------------------------
 // RMSNorm of one row per workgroup: u = bf16(x / sqrt(mean(x^2) + eps) * g).
-// The input is bf16 (xb) or fp32 (xf); x32, if given, receives the fp32 row.
+// The input is bf16 or fp32 (a template parameter: a select between two
+// pointers per element would put every load under a branch); x32, if given,
+// receives the fp32 row.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t* __restrict__ xb,
-                                                 const float* __restrict__ xf, int H,
+template <typename TI>
+__global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H,
                                                  const uint16_t* __restrict__ g, float eps,
                                                  float* __restrict__ x32,
                                                  uint16_t* __restrict__ u) {
+  constexpr int kPer = 8192 / 256;               // H <= 8192: the row stays in registers
   __shared__ float part[4];
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
-  float ss = 0.f;
-  for (int i = tid; i < H; i += 256) {
-    const float v = xb ? bf16_to_f32(xb[row * H + i]) : xf[row * H + i];
-    ss += v * v;
-    if (x32) x32[row * H + i] = v;
+  float v[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {               // clamped loads: none under a branch
+    const int i = tid + 256 * j, ic = i < H ? i : H - 1;
+    const float t = to_f32<TI>(x[row * H + ic]);
+    v[j] = i < H ? t : 0.f;
   }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) ss += v[j] * v[j];
   ss = wave_sum(ss);
   if ((tid & 63) == 0) part[tid >> 6] = ss;
   __syncthreads();
   const float tot = (part[0] + part[1]) + (part[2] + part[3]);
   const float r = 1.f / sqrtf(tot / (float)H + eps);
-  for (int i = tid; i < H; i += 256) {
-    const float v = xb ? bf16_to_f32(xb[row * H + i]) : xf[row * H + i];
-    u[row * H + i] = f32_to_bf16_rne(v * r * bf16_to_f32(g[i]));
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = tid + 256 * j;
+    if (i < H) {
+      if (x32) x32[row * H + i] = v[j];
+      u[row * H + i] = f32_to_bf16_rne(v[j] * r * bf16_to_f32(g[i]));
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// y[p][n] = sum_k X[p][k] W[n][k] (+ R[p][n]) for 16 rows n of W per
-// workgroup (blockIdx.x) and 16 P positions (blockIdx.y).  Wave w multiplies
-// the k range [w K/8, (w+1) K/8): 16-row x 32-k W fragments (A) against the
-// positions' X fragments (B) on v_mfma_f32_16x16x32_bf16, eight k steps of
-// loads issued before their products.  Lane l's accumulator element i is row
-// 4 (l / 16) + i of the tile for position l % 16, so one 16-byte store (or an
-// 8-byte bf16 store) per lane writes four consecutive outputs.
+// y[p][n] = sum_k X[p][k] W[n][k] (+ R[p][n]) for 16 rows n per workgroup
+// (blockIdx.x) and 16 P positions (blockIdx.y).  Up to three weights stacked
+// by rows share a launch (rows [0, n0) of W0, [n0, n0 + n1) of W1, the rest
+// of W2: the q, k and v projections of one input).  GLU: a workgroup takes the
+// same 16 rows of W0 (gate) and W1 (up) and writes bf16(silu(gate) * up).
+// Wave w multiplies the k range [w K/8, (w+1) K/8): 16-row x 32-k W
+// fragments (A) against the positions' X fragments (B) on
+// v_mfma_f32_16x16x32_bf16, 8 / P k steps of loads issued before their
+// products; at most 128 VGPRs, so that two workgroups share a CU and one
+// streams while the other reduces.  Lane l's
+// accumulator element i is row 4 (l / 16) + i of the tile for position
+// l % 16, so one 16-byte store (or an 8-byte bf16 store) per lane writes four
+// consecutive outputs.  The waves' partial sums are added in wave order.
 // ---------------------------------------------------------------------------
-template <int P>
-__global__ __launch_bounds__(kLinWaves * kWave) void k_linear(
-    const uint16_t* __restrict__ W, const uint16_t* __restrict__ X, int K, int M, int ldx,
-    const float* __restrict__ R, int ldr, float* __restrict__ Y, uint16_t* __restrict__ Yb,
-    int ldy) {
-  __shared__ floatx4 red[kLinWaves][P][kWave];
+template <int P, int MODE>
+__global__ __launch_bounds__(kLinWaves * kWave, 2) void k_linear(
+    const uint16_t* __restrict__ W0, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W2, int n0, int n1, int K, const uint16_t* __restrict__ X,
+    int M, const float* __restrict__ R, int ldr, float* __restrict__ Y,
+    uint16_t* __restrict__ Yb, int ldy) {
+  constexpr bool GLU = MODE == 1, TWO = MODE == 2, DUAL = MODE != 0;
+  constexpr int NW = DUAL ? 2 : 1;
+  constexpr int RPW = TWO ? 2 * kTile : kTile;   // rows per workgroup
+  constexpr int CH = 8 / P;                      // k steps per round of loads
+  __shared__ floatx4 red[kLinWaves][NW * P][kWave];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, li = lane & 15;
-  const int row0 = blockIdx.x * kTile, p0 = blockIdx.y * kTile * P;
+  const int r0 = blockIdx.x * RPW, p0 = blockIdx.y * kTile * P;
   const int kw = K / kLinWaves, nks = kw / 32;
-  const uint16_t* wp = W + (size_t)(row0 + li) * K + wave * kw + 8 * g;
+  const uint16_t* Wa = W0;
+  int ra = r0;
+  if (!GLU && r0 >= n0) {                        // workgroup-uniform
+    if (r0 < n0 + n1) {
+      Wa = W1;
+      ra = r0 - n0;
+    } else {
+      Wa = W2;
+      ra = r0 - n0 - n1;
+    }
+  }
+  const uint16_t* wp0 = Wa + (size_t)(ra + li) * K + wave * kw + 8 * g;
+  const uint16_t* wp1 = GLU   ? W1 + (size_t)(r0 + li) * K + wave * kw + 8 * g
+                        : TWO ? wp0 + (size_t)kTile * K
+                              : wp0;
   const uint16_t* xp[P];
   bool pv[P];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
     const int p = p0 + kTile * pb + li;
     pv[pb] = p < M;
-    xp[pb] = X + (size_t)(pv[pb] ? p : 0) * ldx + wave * kw + 8 * g;
+    xp[pb] = X + (size_t)(pv[pb] ? p : 0) * K + wave * kw + 8 * g;
   }
-  floatx4 acc[P];
+  floatx4 acc0[P], acc1[P];
 #pragma unroll
-  for (int pb = 0; pb < P; ++pb) acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int pb = 0; pb < P; ++pb) acc0[pb] = acc1[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
   const u32x4 zero{0u, 0u, 0u, 0u};
-  for (int c = 0; c < nks; c += kLinChunk) {
-    u32x4 a[kLinChunk], b[kLinChunk][P];
+  for (int c = 0; c < nks; c += CH) {
+    u32x4 a0[CH], a1[CH], b[CH][P];
 #pragma unroll
-    for (int j = 0; j < kLinChunk; ++j) {
+    for (int j = 0; j < CH; ++j) {
       const int ks = c + j < nks ? c + j : nks - 1;   // past the end: re-read, not used
-      a[j] = ld16_nt(wp + 32 * ks);
+      a0[j] = ld16(wp0 + 32 * ks);
+      if constexpr (DUAL) a1[j] = ld16(wp1 + 32 * ks);
 #pragma unroll
       for (int pb = 0; pb < P; ++pb) b[j][pb] = ld16(xp[pb] + 32 * ks);
     }
 #pragma unroll
-    for (int j = 0; j < kLinChunk; ++j)
+    for (int j = 0; j < CH; ++j)
       if (c + j < nks)
 #pragma unroll
-        for (int pb = 0; pb < P; ++pb)
-          acc[pb] = Mfma<uint16_t>::mma(a[j], pv[pb] ? b[j][pb] : zero, acc[pb]);
+        for (int pb = 0; pb < P; ++pb) {
+          const u32x4 bx = pv[pb] ? b[j][pb] : zero;
+          acc0[pb] = Mfma<uint16_t>::mma(a0[j], bx, acc0[pb]);
+          if constexpr (DUAL) acc1[pb] = Mfma<uint16_t>::mma(a1[j], bx, acc1[pb]);
+        }
   }
 #pragma unroll
-  for (int pb = 0; pb < P; ++pb) red[wave][pb][lane] = acc[pb];
+  for (int pb = 0; pb < P; ++pb) {
+    red[wave][pb][lane] = acc0[pb];
+    if constexpr (DUAL) red[wave][P + pb][lane] = acc1[pb];
+  }
   __syncthreads();
   if (wave < P) {                                // wave pb adds the 8 partials of block pb
     const int pb = wave;
-    floatx4 s = red[0][pb][lane];
+    floatx4 s0 = red[0][pb][lane], s1{0.f, 0.f, 0.f, 0.f};
+    if constexpr (DUAL) s1 = red[0][P + pb][lane];
 #pragma unroll
-    for (int w = 1; w < kLinWaves; ++w) s += red[w][pb][lane];
+    for (int w = 1; w < kLinWaves; ++w) {
+      s0 += red[w][pb][lane];
+      if constexpr (DUAL) s1 += red[w][P + pb][lane];
+    }
     const int p = p0 + kTile * pb + li;
     if (p < M) {
-      const int n = row0 + 4 * g;
-      if (R) s += *reinterpret_cast<const floatx4*>(R + (size_t)p * ldr + n);
-      if (Y) *reinterpret_cast<floatx4*>(Y + (size_t)p * ldy + n) = s;
-      if (Yb) {
-        const uint32_t lo = f32_to_bf16_rne(s[0]) | ((uint32_t)f32_to_bf16_rne(s[1]) << 16);
-        const uint32_t hi = f32_to_bf16_rne(s[2]) | ((uint32_t)f32_to_bf16_rne(s[3]) << 16);
-        *reinterpret_cast<uint2*>(Yb + (size_t)p * ldy + n) = make_uint2(lo, hi);
+      const int n = r0 + 4 * g;
+      auto put = [&](floatx4 v, int nn) {
+        if (R) v += *reinterpret_cast<const floatx4*>(R + (size_t)p * ldr + nn);
+        if (Y) *reinterpret_cast<floatx4*>(Y + (size_t)p * ldy + nn) = v;
+        if (Yb) {
+          const uint32_t lo = f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16);
+          const uint32_t hi = f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16);
+          *reinterpret_cast<uint2*>(Yb + (size_t)p * ldy + nn) = make_uint2(lo, hi);
+        }
+      };
+      if constexpr (GLU) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s0[e] = s0[e] / (1.f + __expf(-s0[e])) * s1[e];
+        put(s0, n);
+      } else {
+        put(s0, n);
+        if constexpr (TWO) put(s1, n + kTile);
       }
     }
   }
@@ -194,6 +251,7 @@ __global__ __launch_bounds__(512) void k_attn(
     const uint16_t* __restrict__ vb, const int32_t* __restrict__ ctx_len, int Cmax, int B,
     int npb, int nh, int nkv, int grp, int causal, int ns, float* __restrict__ opart,
     float* __restrict__ mlpart) {
+  __shared__ __align__(16) uint16_t Ks[kAttnKeys][kHd + 8];        // +16 B per row
   __shared__ __align__(16) uint16_t Vt[kHd][kAttnKeys + kAttnPad];
   const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
   const int b = z / npb, pb = z - b * npb;
@@ -218,22 +276,37 @@ __global__ __launch_bounds__(512) void k_attn(
     return blk + (((size_t)b * B + (kk - C)) * nkv + kvh) * kHd;
   };
 
-  // V of the chunk, transposed: Vt[d][key]; keys past the end are zeros
-  for (int kl = threadIdx.x; kl < kAttnKeys; kl += blockDim.x) {
-    const int kk = kbase + kl;
-    const bool ok = kk < nkeys;
-    const uint16_t* src = krow(ok ? kk : nkeys - 1, vcache, vb);
+  // K and V of the chunk into LDS (K as is, V transposed: Vt[d][key]), 16
+  // bytes per item, 16 items per thread loaded before any is stored: one
+  // memory round for the whole chunk; keys past the end are zeros
+  constexpr int kItems = kAttnKeys * (kHd / 8), kStage = 16;
+  for (int r = 0; r < kItems; r += blockDim.x * kStage) {
+    u32x4 kv[kStage], vv[kStage];
 #pragma unroll
-    for (int c = 0; c < kHd / 8; ++c) {
-      const u32x4 v = ok ? ld16(src + 8 * c) : u32x4{0u, 0u, 0u, 0u};
-      Vt[8 * c + 0][kl] = (uint16_t)(v.x & 0xFFFFu);
-      Vt[8 * c + 1][kl] = (uint16_t)(v.x >> 16);
-      Vt[8 * c + 2][kl] = (uint16_t)(v.y & 0xFFFFu);
-      Vt[8 * c + 3][kl] = (uint16_t)(v.y >> 16);
-      Vt[8 * c + 4][kl] = (uint16_t)(v.z & 0xFFFFu);
-      Vt[8 * c + 5][kl] = (uint16_t)(v.z >> 16);
-      Vt[8 * c + 6][kl] = (uint16_t)(v.w & 0xFFFFu);
-      Vt[8 * c + 7][kl] = (uint16_t)(v.w >> 16);
+    for (int j = 0; j < kStage; ++j) {
+      const int it = r + threadIdx.x + blockDim.x * j;
+      const int key = (it >> 4) & (kAttnKeys - 1), c = it & 15, kk = kbase + key;
+      const bool ok = it < kItems && kk < nkeys;
+      const int kc = ok ? kk : nkeys - 1;
+      kv[j] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      vv[j] = ok ? ld16(krow(kc, vcache, vb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) {
+      const int it = r + threadIdx.x + blockDim.x * j;
+      if (it < kItems) {
+        const int key = it >> 4, c = it & 15;
+        *reinterpret_cast<u32x4*>(&Ks[key][8 * c]) = kv[j];
+        const u32x4 v = vv[j];
+        Vt[8 * c + 0][key] = (uint16_t)(v.x & 0xFFFFu);
+        Vt[8 * c + 1][key] = (uint16_t)(v.x >> 16);
+        Vt[8 * c + 2][key] = (uint16_t)(v.y & 0xFFFFu);
+        Vt[8 * c + 3][key] = (uint16_t)(v.y >> 16);
+        Vt[8 * c + 4][key] = (uint16_t)(v.z & 0xFFFFu);
+        Vt[8 * c + 5][key] = (uint16_t)(v.z >> 16);
+        Vt[8 * c + 6][key] = (uint16_t)(v.w & 0xFFFFu);
+        Vt[8 * c + 7][key] = (uint16_t)(v.w >> 16);
+      }
     }
   }
 
@@ -248,14 +321,14 @@ __global__ __launch_bounds__(512) void k_attn(
 
   constexpr int NT = kAttnKeys / kTile;
   const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
+  __syncthreads();                               // Ks and Vt complete
   floatx4 sc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    const int kk = kbase + kTile * t + li;       // A operand row
-    const uint16_t* kr = krow(kk < nkeys ? kk : nkeys - 1, kcache, kb) + 8 * g;
-    u32x4 kf[kHd / 32];
+    u32x4 kf[kHd / 32];                          // A operand: key 16 t + li
 #pragma unroll
-    for (int ks = 0; ks < kHd / 32; ++ks) kf[ks] = ld16(kr + 32 * ks);
+    for (int ks = 0; ks < kHd / 32; ++ks)
+      kf[ks] = *reinterpret_cast<const u32x4*>(&Ks[kTile * t + li][32 * ks + 8 * g]);
     floatx4 acc{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
@@ -295,7 +368,6 @@ __global__ __launch_bounds__(512) void k_attn(
   }
   lsum += __shfl_xor(lsum, 16, kWave);
   lsum += __shfl_xor(lsum, 32, kWave);
-  __syncthreads();                               // Vt complete
 
   floatx4 o[kHd / 16];
 #pragma unroll
@@ -325,7 +397,10 @@ __global__ __launch_bounds__(512) void k_attn(
 }
 
 // One wave per (position m, query head h): merge the chunks in order,
-// attn = sum_s e^(m_s - M) O_s / sum_s e^(m_s - M) l_s, to bf16.
+// attn = sum_s e^(m_s - M) O_s / sum_s e^(m_s - M) l_s, to bf16.  Lane j
+// takes the (m, l) of chunk s0 + j; the O rows are then read eight chunks at a
+// time and added in chunk order.  A chunk whose l is 0 (no visible key; its O
+// may be unwritten) contributes nothing.
 __global__ __launch_bounds__(256) void k_attn_comb(const float* __restrict__ opart,
                                                    const float* __restrict__ mlpart, int M, int B,
                                                    int npb, int nh, int nkv, int grp, int ns,
@@ -337,36 +412,54 @@ __global__ __launch_bounds__(256) void k_attn_comb(const float* __restrict__ opa
   const int b = m / B, p = m - b * B, pb = p / kTile, q = p - pb * kTile;
   const int kvh = h / grp, wv = h - kvh * grp, z = b * npb + pb;
   const size_t base = (((size_t)z * nkv + kvh) * ns) * grp + wv;
+  auto mlv = [&](int s, float& ms, float& ls) {
+    if (s < ns) {
+      const size_t pi = base + (size_t)s * grp;
+      ms = mlpart[pi * 2 * kTile + 2 * q];
+      ls = mlpart[pi * 2 * kTile + 2 * q + 1];
+    } else {
+      ms = -INFINITY;
+      ls = 0.f;
+    }
+  };
   float mm = -INFINITY;
-  for (int s = 0; s < ns; ++s) {
-    const size_t pi = base + (size_t)s * grp;
-    const float ms = mlpart[pi * 2 * kTile + 2 * q], ls = mlpart[pi * 2 * kTile + 2 * q + 1];
+  for (int s0 = 0; s0 < ns; s0 += kWave) {
+    float ms, ls;
+    mlv(s0 + lane, ms, ls);
     if (ls > 0.f) mm = fmaxf(mm, ms);
   }
-  float L = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const size_t pi = base + (size_t)s * grp;
-    const float ms = mlpart[pi * 2 * kTile + 2 * q], ls = mlpart[pi * 2 * kTile + 2 * q + 1];
-    if (ls > 0.f) {
-      const float f = __expf(ms - mm);
-      L += ls * f;
-      o0 += f * opart[pi * (kTile * kHd) + q * kHd + lane];
-      o1 += f * opart[pi * (kTile * kHd) + q * kHd + lane + 64];
+#pragma unroll
+  for (int k = 32; k >= 1; k >>= 1) mm = fmaxf(mm, __shfl_xor(mm, k, kWave));
+  float Ll = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += kWave) {
+    float ms, ls;
+    mlv(s0 + lane, ms, ls);
+    const float f = ls > 0.f ? __expf(ms - mm) : 0.f;
+    Ll += f * ls;
+    const int cnt = ns - s0 < kWave ? ns - s0 : kWave;
+    for (int j0 = 0; j0 < cnt; j0 += 8) {
+      float fj[8], v0[8], v1[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u < cnt ? j0 + u : cnt - 1;
+        fj[u] = __shfl(f, j, kWave);
+        if (j0 + u >= cnt) fj[u] = 0.f;
+        const size_t pi = base + (size_t)(s0 + j) * grp;
+        v0[u] = opart[pi * (kTile * kHd) + q * kHd + lane];
+        v1[u] = opart[pi * (kTile * kHd) + q * kHd + lane + 64];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        o0 += fj[u] != 0.f ? fj[u] * v0[u] : 0.f;
+        o1 += fj[u] != 0.f ? fj[u] * v1[u] : 0.f;
+      }
     }
   }
+  const float L = wave_sum(Ll);
   const float inv = L > 0.f ? 1.f / L : 0.f;     // L > 0: every query sees its own key
   uint16_t* dst = attn + (size_t)m * nh * kHd + (size_t)h * kHd;
   dst[lane] = f32_to_bf16_rne(o0 * inv);
   dst[lane + 64] = f32_to_bf16_rne(o1 * inv);
-}
-
-__global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ G,
-                                                const float* __restrict__ U, size_t n,
-                                                uint16_t* __restrict__ act) {
-  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  const float gv = G[i];
-  act[i] = f32_to_bf16_rne(gv / (1.f + __expf(-gv)) * U[i]);
 }
 
 }  // namespace xp
@@ -385,7 +478,7 @@ struct xp_layer {
   uint16_t *qn = nullptr, *kb = nullptr, *vb = nullptr;
   float *opart = nullptr, *mlpart = nullptr;
   uint16_t* attn = nullptr;
-  float *x1 = nullptr, *G = nullptr, *U = nullptr, *h32 = nullptr;
+  float *x1 = nullptr, *h32 = nullptr;
   uint16_t* act = nullptr;
 };
 
@@ -447,7 +540,6 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
       {(void**)&L->kb, Mx * kvd * 2},          {(void**)&L->vb, Mx * kvd * 2},
       {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
       {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
-      {(void**)&L->G, Mx * F * 4},             {(void**)&L->U, Mx * F * 4},
       {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
   };
   size_t total = 0;
@@ -472,18 +564,33 @@ extern "C" void xp_layer_destroy(xp_layer* L) {
   delete L;
 }
 
-// y [M][N] (row stride ldy) = X [M][K] W^T (+ R): P = 1, 2 or 4 position blocks per pass
-static void linear(const uint16_t* W, int N, int K, const uint16_t* X, int M, const float* R,
-                   int ldr, float* Y, uint16_t* Yb, int ldy, hipStream_t st) {
+// y [M][N] (row stride ldy) = X [M][K] W^T (+ R), W the rows of W0 | W1 | W2
+// stacked (n0, n1 rows of the first two); glu: bf16(silu(X W0^T) * (X W1^T)).
+// P = 1, 2 or 4 position blocks per pass of the weight.
+static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0, int n1,
+                   int N, int K, const uint16_t* X, int M, const float* R, int ldr, float* Y,
+                   uint16_t* Yb, int ldy, bool glu, hipStream_t st) {
   const int nb = (M + kTile - 1) / kTile;
   const int P = nb >= 4 ? 4 : (nb >= 2 ? 2 : 1);
-  const dim3 grid(N / kTile, (M + kTile * P - 1) / (kTile * P)), block(kLinWaves * kWave);
-  if (P == 4)
-    hipLaunchKernelGGL(k_linear<4>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
-  else if (P == 2)
-    hipLaunchKernelGGL(k_linear<2>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
-  else
-    hipLaunchKernelGGL(k_linear<1>, grid, block, 0, st, W, X, K, M, K, R, ldr, Y, Yb, ldy);
+  // two row tiles per workgroup (stacked row counts are multiples of 32) once
+  // several position blocks reuse each X fragment; one at a single block,
+  // where the workgroup count matters more
+  const int mode = glu ? 1 : (P > 1 ? 2 : 0);
+  const dim3 grid(N / (mode == 2 ? 2 * kTile : kTile), (M + kTile * P - 1) / (kTile * P)),
+      block(kLinWaves * kWave);
+#define XP_LIN(PP, MM)                                                                        \
+  hipLaunchKernelGGL((k_linear<PP, MM>), grid, block, 0, st, W0, W1, W2, n0, n1, K, X, M, R, \
+                     ldr, Y, Yb, ldy)
+  if (glu) {
+    if (P == 4) XP_LIN(4, 1);
+    else if (P == 2) XP_LIN(2, 1);
+    else XP_LIN(1, 1);
+  } else {
+    if (P == 4) XP_LIN(4, 2);
+    else if (P == 2) XP_LIN(2, 2);
+    else XP_LIN(1, 0);
+  }
+#undef XP_LIN
 }
 
 extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal,
@@ -501,11 +608,10 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   const int npb = (B + kTile - 1) / kTile, ns = attn_chunks(C_max, B);
   float* hout = h_f32 ? h_f32 : L->h32;
 
-  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, st, (const uint16_t*)x, (const float*)nullptr,
-                     H, L->g_attn, L->eps, L->x32, L->u);
-  linear(L->Wq, nhd, H, L->u, M, nullptr, 0, L->qkv, nullptr, ldq, st);
-  linear(L->Wk, kvd, H, L->u, M, nullptr, 0, L->qkv + nhd, nullptr, ldq, st);
-  linear(L->Wv, kvd, H, L->u, M, nullptr, 0, L->qkv + nhd + kvd, nullptr, ldq, st);
+  hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st, (const uint16_t*)x, H,
+                     L->g_attn, L->eps, L->x32, L->u);
+  linear(L->Wq, L->Wk, L->Wv, nhd, kvd, ldq, H, L->u, M, nullptr, 0, L->qkv, nullptr, ldq, false,
+         st);
   const int qk_waves = M * (nh + 2 * nkv);
   hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M, B, nh,
                      nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn, L->kb, L->vb);
@@ -515,14 +621,12 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   const int cw = M * nh;
   hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart, L->mlpart, M, B,
                      npb, nh, nkv, grp, ns, L->attn);
-  linear(L->Wo, H, nhd, L->attn, M, L->x32, H, L->x1, nullptr, H, st);
-  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, st, (const uint16_t*)nullptr, L->x1, H,
+  linear(L->Wo, nullptr, nullptr, H, 0, H, nhd, L->attn, M, L->x32, H, L->x1, nullptr, H, false,
+         st);
+  hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st, (const float*)L->x1, H,
                      L->g_mlp, L->eps, (float*)nullptr, L->u);
-  linear(L->Wg, F, H, L->u, M, nullptr, 0, L->G, nullptr, F, st);
-  linear(L->Wu, F, H, L->u, M, nullptr, 0, L->U, nullptr, F, st);
-  const size_t na = (size_t)M * F;
-  hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, L->G, L->U,
-                     na, L->act);
-  linear(L->Wd, H, F, L->act, M, L->x1, H, hout, (uint16_t*)h_bf16, H, st);
+  linear(L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F, true, st);
+  linear(L->Wd, nullptr, nullptr, H, 0, H, F, L->act, M, L->x1, H, hout, (uint16_t*)h_bf16, H,
+         false, st);
   return hipGetLastError() == hipSuccess ? XP_OK : XP_EHIP;
 }
