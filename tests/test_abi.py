@@ -100,3 +100,47 @@ def test_toeplitz_mixer_rejects_bad_arguments_without_a_gpu():
     assert L.xp_toeplitz_mixer(p, 256, 0, X.XP_F32, p, None) == X.XP_EINVAL
     assert L.xp_toeplitz_mixer(p, 256, 33, X.XP_F32, p, None) == X.XP_EINVAL
     assert L.xp_toeplitz_mixer(p, 256, 16, 7, p, None) == X.XP_EINVAL
+
+
+def _layer_weights(**kw):
+    w = X._LayerWeights(H=4096, n_heads=32, n_kv=8, head_dim=128, ffn=12288, eps=1e-6,
+                        rope_theta=1e6)
+    for n in X.LAYER_WEIGHT_NAMES:
+        setattr(w, n, 0x1000)          # never dereferenced: validation fails first
+    for k, v in kw.items():
+        setattr(w, k, v)
+    return w
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(head_dim=64), X.XP_EUNSUPPORTED),
+    (dict(n_kv=3), X.XP_EUNSUPPORTED),            # 32 heads not a multiple of 3
+    (dict(n_kv=2), X.XP_EUNSUPPORTED),            # group of 16
+    (dict(H=4000), X.XP_EUNSUPPORTED),
+    (dict(H=16384), X.XP_EUNSUPPORTED),
+    (dict(ffn=1000), X.XP_EUNSUPPORTED),
+    (dict(H=0), X.XP_EINVAL),
+    (dict(rope_theta=0.0), X.XP_EINVAL),
+    (dict(eps=-1.0), X.XP_EINVAL),
+    (dict(Wd=None), X.XP_EINVAL),
+    (dict(g_q=None), X.XP_EINVAL),
+])
+def test_layer_create_rejects_bad_arguments_without_a_gpu(change, status):
+    L = X.load_library()
+    h = ctypes.c_void_p(0)
+    w = _layer_weights(**change)
+    assert L.xp_layer_create(ctypes.byref(w), 1, 16, 2048, ctypes.byref(h)) == status
+    assert not h.value
+
+
+def test_layer_create_and_forward_reject_bad_sizes_and_null_handles():
+    L = X.load_library()
+    h = ctypes.c_void_p(0)
+    w = _layer_weights()
+    for mb, mB, mc in ((0, 16, 2048), (1, 0, 2048), (1, 33, 2048), (1, 16, -1)):
+        assert L.xp_layer_create(ctypes.byref(w), mb, mB, mc, ctypes.byref(h)) == X.XP_EINVAL
+    assert L.xp_layer_create(None, 1, 16, 2048, ctypes.byref(h)) == X.XP_EINVAL
+    assert L.xp_layer_create(ctypes.byref(w), 1, 16, 2048, None) == X.XP_EINVAL
+    p = 0x1000
+    assert L.xp_layer_forward(None, 1, 16, 1, p, p, p, 64, p, p, p, None) == X.XP_EINVAL
+    L.xp_layer_destroy(None)
