@@ -23,7 +23,8 @@ namespace xp {
 
 constexpr int kLinWaves = 8;        // k-split of k_linear
 constexpr int kLinChunk = 8;        // k steps (of 32) loaded before their products
-constexpr int kAttnKeys = 256;      // keys per attention workgroup
+constexpr int kAttnKeys = 256;      // keys per attention workgroup (64 at small batch)
+constexpr int kAttnKeysSmall = 64;
 constexpr int kAttnPad = 4;         // LDS row padding (bf16) of the transposed V
 constexpr int kHd = 128;            // head_dim (the only one built)
 
@@ -245,21 +246,22 @@ __global__ __launch_bounds__(256) void k_qkrope(
 // queries 4 (l / 16) + i for d = 16 dt + l % 16.  Written per (chunk, query):
 // O (relative to the chunk maximum m), m and l = sum of the numerators.
 // ---------------------------------------------------------------------------
+template <int KEYS>
 __global__ __launch_bounds__(512) void k_attn(
     const uint16_t* __restrict__ qn, const uint16_t* __restrict__ kcache,
     const uint16_t* __restrict__ vcache, const uint16_t* __restrict__ kb,
     const uint16_t* __restrict__ vb, const int32_t* __restrict__ ctx_len, int Cmax, int B,
     int npb, int nh, int nkv, int grp, int causal, int ns, float* __restrict__ opart,
     float* __restrict__ mlpart) {
-  __shared__ __align__(16) uint16_t Ks[kAttnKeys][kHd + 8];        // +16 B per row
-  __shared__ __align__(16) uint16_t Vt[kHd][kAttnKeys + kAttnPad];
+  __shared__ __align__(16) uint16_t Ks[KEYS][kHd + 8];        // +16 B per row
+  __shared__ __align__(16) uint16_t Vt[kHd][KEYS + kAttnPad];
   const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
   const int b = z / npb, pb = z - b * npb;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, li = lane & 15;
   int C = ctx_len[b];
   C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
-  const int nkeys = C + B, kbase = s * kAttnKeys;
+  const int nkeys = C + B, kbase = s * KEYS;
   const size_t pidx = (((size_t)z * nkv + kvh) * ns + s) * grp + wave;
   float* op = opart + pidx * (kTile * kHd);
   float* ml = mlpart + pidx * (2 * kTile);
@@ -279,13 +281,13 @@ __global__ __launch_bounds__(512) void k_attn(
   // K and V of the chunk into LDS (K as is, V transposed: Vt[d][key]), 16
   // bytes per item, 16 items per thread loaded before any is stored: one
   // memory round for the whole chunk; keys past the end are zeros
-  constexpr int kItems = kAttnKeys * (kHd / 8), kStage = 16;
+  constexpr int kItems = KEYS * (kHd / 8), kStage = 16;
   for (int r = 0; r < kItems; r += blockDim.x * kStage) {
     u32x4 kv[kStage], vv[kStage];
 #pragma unroll
     for (int j = 0; j < kStage; ++j) {
       const int it = r + threadIdx.x + blockDim.x * j;
-      const int key = (it >> 4) & (kAttnKeys - 1), c = it & 15, kk = kbase + key;
+      const int key = (it >> 4) & (KEYS - 1), c = it & 15, kk = kbase + key;
       const bool ok = it < kItems && kk < nkeys;
       const int kc = ok ? kk : nkeys - 1;
       kv[j] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
@@ -319,7 +321,7 @@ __global__ __launch_bounds__(512) void k_attn(
 #pragma unroll
   for (int ks = 0; ks < kHd / 32; ++ks) qf[ks] = qv ? ld16(qs + 32 * ks) : u32x4{0u, 0u, 0u, 0u};
 
-  constexpr int NT = kAttnKeys / kTile;
+  constexpr int NT = KEYS / kTile;
   const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
   __syncthreads();                               // Ks and Vt complete
   floatx4 sc[NT];
@@ -482,7 +484,9 @@ struct xp_layer {
   uint16_t* act = nullptr;
 };
 
-static int attn_chunks(int C_max, int B) { return (C_max + B + kAttnKeys - 1) / kAttnKeys; }
+constexpr int kSmallAttnWgs = 512;  // below this many 256-key workgroups, 64-key chunks
+
+static int attn_chunks(int C_max, int B, int keys) { return (C_max + B + keys - 1) / keys; }
 
 extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
                                      int32_t max_ctx, xp_layer** out) {
@@ -526,11 +530,13 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   L->max_batch = max_batch;
   L->max_B = max_B;
   L->max_ctx = max_ctx;
-  L->nsmax = attn_chunks(max_ctx, max_B);
+  L->nsmax = attn_chunks(max_ctx, max_B, kAttnKeys);
   const size_t Mx = (size_t)max_batch * max_B, H = L->H, nhd = (size_t)L->nh * kHd,
                kvd = (size_t)L->nkv * kHd, F = L->ffn;
   const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
-  const size_t nparts = zmax * L->nkv * L->nsmax * grp;
+  // partials of 256-key chunks at the largest call, or of the 64-key chunks
+  // that small calls (fewer than kSmallAttnWgs 256-key workgroups) use
+  const size_t nparts = std::max(zmax * L->nkv * L->nsmax, (size_t)4 * kSmallAttnWgs) * grp;
   struct Slice {
     void** p;
     size_t bytes;
@@ -601,11 +607,16 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
       ctx_len == nullptr || batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B ||
       C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1) || (causal != 0 && causal != 1))
     return XP_EINVAL;
-  if (attn_chunks(C_max, B) > L->nsmax) return XP_EINVAL;
+  if (attn_chunks(C_max, B, kAttnKeys) > L->nsmax) return XP_EINVAL;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
-  const int npb = (B + kTile - 1) / kTile, ns = attn_chunks(C_max, B);
+  const int npb = (B + kTile - 1) / kTile;
+  // 64-key chunks when 256-key ones would leave most CUs idle (their
+  // partials fit the 4 x kSmallAttnWgs reserved), 256-key ones otherwise
+  const bool small =
+      (size_t)batch * npb * nkv * attn_chunks(C_max, B, kAttnKeys) < (size_t)kSmallAttnWgs;
+  const int ns = attn_chunks(C_max, B, small ? kAttnKeysSmall : kAttnKeys);
   float* hout = h_f32 ? h_f32 : L->h32;
 
   hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st, (const uint16_t*)x, H,
@@ -615,9 +626,15 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   const int qk_waves = M * (nh + 2 * nkv);
   hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M, B, nh,
                      nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn, L->kb, L->vb);
-  hipLaunchKernelGGL(k_attn, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0, st, L->qn,
-                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb, ctx_len,
-                     C_max, B, npb, nh, nkv, grp, causal, ns, L->opart, L->mlpart);
+  if (small)
+    hipLaunchKernelGGL(k_attn<kAttnKeysSmall>, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0,
+                       st, L->qn, (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb,
+                       L->vb, ctx_len, C_max, B, npb, nh, nkv, grp, causal, ns, L->opart,
+                       L->mlpart);
+  else
+    hipLaunchKernelGGL(k_attn<kAttnKeys>, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0, st,
+                       L->qn, (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb,
+                       ctx_len, C_max, B, npb, nh, nkv, grp, causal, ns, L->opart, L->mlpart);
   const int cw = M * nh;
   hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart, L->mlpart, M, B,
                      npb, nh, nkv, grp, ns, L->attn);

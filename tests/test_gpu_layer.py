@@ -2,7 +2,8 @@
 (needs an MI355X).
 
 Small shapes span several k-split chunks of every projection, several
-256-key attention chunks with ragged context lengths (0, chunk boundaries),
+attention chunks (64-key ones for small calls, 256-key ones for large) with
+ragged context lengths (0, chunk boundaries),
 every built query-group size and blocks of 1, 8, 16 and 32 positions; the
 full-size case runs the Qwen3-8B layer at batch 1 with a 2048-key context.
 
@@ -78,6 +79,18 @@ def test_layer_matches_oracle(H, nh, nkv, ffn, B, batch, ctx, causal):
     w, weights, inp = _case(H, nh, nkv, ffn, B, batch, ctx, index=700 + H + B)
     h32, hb, layer, _ = _run(w, weights, inp, causal)
     _check(w, weights, inp, h32, hb, causal)
+    layer.close()
+
+
+def test_layer_large_call_takes_256_key_chunks():
+    """8 sequences x 8 KV heads x up to 16 chunks of 256 keys: at least 512
+    workgroups, so the forward takes the 256-key attention chunks (smaller
+    calls take 64-key ones); ragged contexts from 0 to 4095 keys."""
+    ctx = [4000, 3000, 2500, 1, 0, 257, 4095, 100]
+    _say(f"case: layer 256-key chunks H=256 heads 8/8 B=16 batch=8 ctx={ctx}")
+    w, weights, inp = _case(256, 8, 8, 256, 16, 8, ctx, index=811, c_max=4096)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
     layer.close()
 
 
