@@ -91,6 +91,11 @@ hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, cons
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
 int gemm_units(const xp_handle* h, int M);
+// the context layer's projections for many positions (xp_lgemm.hip)
+bool layer_gemm_ok(int n0, int n1, int N, int K, int M);
+hipError_t launch_layer_gemm(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
+                             int n1, int N, int K, const uint16_t* X, int M, const float* R,
+                             int ldr, float* Y, uint16_t* Yb, int ldy, hipStream_t st);
 int gemm_units_max(const xp_handle* h);
 bool lmhead_gemm_ok(const xp_handle* h, int M);
 hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,

@@ -11,7 +11,7 @@
 //                 workgroup, 16 P positions per pass of the weight, the waves'
 //                 partial sums added in fixed order in LDS
 //   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
-//   k_attn        split-KV block attention: a workgroup takes 256 keys of one
+//   k_attn        split-KV block attention: a workgroup takes 128 keys of one
 //                 KV head for 16 block positions, one wave per query head of
 //                 the group; the chunk's K and V (transposed) staged in LDS in
 //                 one memory round, S = K Q^T and O = P V on the matrix cores
@@ -22,8 +22,8 @@
 namespace xp {
 
 constexpr int kLinWaves = 8;        // k-split of k_linear
-constexpr int kLinChunk = 8;        // k steps (of 32) loaded before their products
-constexpr int kAttnKeys = 256;      // keys per attention workgroup (64 at small batch)
+constexpr int kLinMaxStream = 64;   // positions up to which the projections stream
+constexpr int kAttnKeys = 128;      // keys per attention workgroup (64 at small batch)
 constexpr int kAttnKeysSmall = 64;
 constexpr int kAttnPad = 4;         // LDS row padding (bf16) of the transposed V
 constexpr int kHd = 128;            // head_dim (the only one built)
@@ -324,6 +324,7 @@ __global__ __launch_bounds__(512) void k_attn(
   constexpr int NT = KEYS / kTile;
   const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
   __syncthreads();                               // Ks and Vt complete
+  const bool interior = kbase + KEYS <= C;       // a chunk of context keys only
   floatx4 sc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -334,11 +335,16 @@ __global__ __launch_bounds__(512) void k_attn(
     floatx4 acc{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
+    if (interior) {                              // workgroup-uniform: every key visible
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = kbase + kTile * t + 4 * g + i;
-      const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
-      sc[t][i] = vis ? acc[i] * scale : -INFINITY;
+      for (int i = 0; i < 4; ++i) sc[t][i] = qv ? acc[i] * scale : -INFINITY;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kbase + kTile * t + 4 * g + i;
+        const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
+        sc[t][i] = vis ? acc[i] * scale : -INFINITY;
+      }
     }
   }
   float mx = -INFINITY;
@@ -464,6 +470,17 @@ __global__ __launch_bounds__(256) void k_attn_comb(const float* __restrict__ opa
   dst[lane + 64] = f32_to_bf16_rne(o1 * inv);
 }
 
+// silu(gate) * up to bf16, gate and up side by side in one row of 2 F
+// (the GEMM path computes both projections in one launch)
+__global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ GU, int F, size_t n,
+                                                uint16_t* __restrict__ act) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const size_t m = i / F, j = i - m * F;
+  const float gv = GU[m * 2 * F + j], uv = GU[m * 2 * F + F + j];
+  act[i] = f32_to_bf16_rne(gv / (1.f + __expf(-gv)) * uv);
+}
+
 }  // namespace xp
 
 using namespace xp;
@@ -480,11 +497,11 @@ struct xp_layer {
   uint16_t *qn = nullptr, *kb = nullptr, *vb = nullptr;
   float *opart = nullptr, *mlpart = nullptr;
   uint16_t* attn = nullptr;
-  float *x1 = nullptr, *h32 = nullptr;
+  float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;
   uint16_t* act = nullptr;
 };
 
-constexpr int kSmallAttnWgs = 512;  // below this many 256-key workgroups, 64-key chunks
+constexpr int kSmallAttnWgs = 512;  // below this many 128-key workgroups, 64-key chunks
 
 static int attn_chunks(int C_max, int B, int keys) { return (C_max + B + keys - 1) / keys; }
 
@@ -534,9 +551,9 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   const size_t Mx = (size_t)max_batch * max_B, H = L->H, nhd = (size_t)L->nh * kHd,
                kvd = (size_t)L->nkv * kHd, F = L->ffn;
   const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
-  // partials of 256-key chunks at the largest call, or of the 64-key chunks
-  // that small calls (fewer than kSmallAttnWgs 256-key workgroups) use
-  const size_t nparts = std::max(zmax * L->nkv * L->nsmax, (size_t)4 * kSmallAttnWgs) * grp;
+  // partials of 128-key chunks at the largest call, or of the 64-key chunks
+  // that small calls (fewer than kSmallAttnWgs 128-key workgroups) use
+  const size_t nparts = std::max(zmax * L->nkv * L->nsmax, (size_t)2 * kSmallAttnWgs) * grp;
   struct Slice {
     void** p;
     size_t bytes;
@@ -547,6 +564,7 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
       {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
       {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
       {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
+      {(void**)&L->GU, (Mx > kLinMaxStream ? Mx : 0) * 2 * F * 4},
   };
   size_t total = 0;
   for (auto& s : sl) total += (s.bytes + 255) / 256 * 256;
@@ -575,7 +593,20 @@ extern "C" void xp_layer_destroy(xp_layer* L) {
 // P = 1, 2 or 4 position blocks per pass of the weight.
 static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0, int n1,
                    int N, int K, const uint16_t* X, int M, const float* R, int ldr, float* Y,
-                   uint16_t* Yb, int ldy, bool glu, hipStream_t st) {
+                   uint16_t* Yb, int ldy, bool glu, hipStream_t st, float* GU = nullptr) {
+  // above one 64-position pass of the stream: the tiled GEMM (weights read
+  // once per 128 or 256 positions); gate and up side by side, then SwiGLU
+  if (M > kLinMaxStream && (glu ? layer_gemm_ok(N, N, 2 * N, K, M) : layer_gemm_ok(n0, n1, N, K, M))) {
+    if (glu) {
+      launch_layer_gemm(W0, W1, W1, N, N, 2 * N, K, X, M, nullptr, 0, GU, nullptr, 2 * N, st);
+      const size_t na = (size_t)M * N;
+      hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
+                         na, Yb);
+    } else {
+      launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
+    }
+    return;
+  }
   const int nb = (M + kTile - 1) / kTile;
   const int P = nb >= 4 ? 4 : (nb >= 2 ? 2 : 1);
   // two row tiles per workgroup (stacked row counts are multiples of 32) once
@@ -612,8 +643,8 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
   const int npb = (B + kTile - 1) / kTile;
-  // 64-key chunks when 256-key ones would leave most CUs idle (their
-  // partials fit the 4 x kSmallAttnWgs reserved), 256-key ones otherwise
+  // 64-key chunks when 128-key ones would leave most CUs idle (their
+  // partials fit the 2 x kSmallAttnWgs reserved), 128-key ones otherwise
   const bool small =
       (size_t)batch * npb * nkv * attn_chunks(C_max, B, kAttnKeys) < (size_t)kSmallAttnWgs;
   const int ns = attn_chunks(C_max, B, small ? kAttnKeysSmall : kAttnKeys);
@@ -642,7 +673,8 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
          st);
   hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st, (const float*)L->x1, H,
                      L->g_mlp, L->eps, (float*)nullptr, L->u);
-  linear(L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F, true, st);
+  linear(L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F, true, st,
+         L->GU);
   linear(L->Wd, nullptr, nullptr, H, 0, H, F, L->act, M, L->x1, H, hout, (uint16_t*)h_bf16, H,
          false, st);
   return hipGetLastError() == hipSuccess ? XP_OK : XP_EHIP;

@@ -2,10 +2,12 @@
 (needs an MI355X).
 
 Small shapes span several k-split chunks of every projection, several
-attention chunks (64-key ones for small calls, 256-key ones for large) with
+attention chunks (64-key ones for small calls, 128-key ones for large) with
 ragged context lengths (0, chunk boundaries),
-every built query-group size and blocks of 1, 8, 16 and 32 positions; the
-full-size case runs the Qwen3-8B layer at batch 1 with a 2048-key context.
+every built query-group size, blocks of 1, 8, 16 and 32 positions, and the
+three projection paths (streaming up to 64 positions, the tiled GEMM with
+128 x 128 tiles up to 128 and 256 x 256 above); the full-size case runs the
+Qwen3-8B layer at batch 1 with a 2048-key context.
 
 Tolerance: h is compared in fp32 against the oracle's fp64 h with the bf16
 rounding points of the device (u, q, k, v, the attention output, u2 and the
@@ -82,13 +84,24 @@ def test_layer_matches_oracle(H, nh, nkv, ffn, B, batch, ctx, causal):
     layer.close()
 
 
-def test_layer_large_call_takes_256_key_chunks():
-    """8 sequences x 8 KV heads x up to 16 chunks of 256 keys: at least 512
-    workgroups, so the forward takes the 256-key attention chunks (smaller
+def test_layer_large_call_takes_128_key_chunks():
+    """8 sequences x 8 KV heads x up to 33 chunks of 128 keys: at least 512
+    workgroups, so the forward takes the 128-key attention chunks (smaller
     calls take 64-key ones); ragged contexts from 0 to 4095 keys."""
     ctx = [4000, 3000, 2500, 1, 0, 257, 4095, 100]
-    _say(f"case: layer 256-key chunks H=256 heads 8/8 B=16 batch=8 ctx={ctx}")
+    _say(f"case: layer 128-key chunks H=256 heads 8/8 B=16 batch=8 ctx={ctx}")
     w, weights, inp = _case(256, 8, 8, 256, 16, 8, ctx, index=811, c_max=4096)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
+def test_layer_projections_as_gemm_with_256_tiles():
+    """192 positions: the projections run as the tiled GEMM with 256 x 256
+    tiles (128 x 128 up to 128 positions, the streaming kernel up to 64)."""
+    ctx = [5, 700, 33, 0, 256, 1000, 64, 129, 300, 2, 511, 90]
+    _say(f"case: layer GEMM path H=512 heads 8/2 ffn=512 B=16 batch=12 ctx={ctx}")
+    w, weights, inp = _case(512, 8, 2, 512, 16, 12, ctx, index=833)
     h32, hb, layer, _ = _run(w, weights, inp)
     _check(w, weights, inp, h32, hb)
     layer.close()
