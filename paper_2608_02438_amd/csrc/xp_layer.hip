@@ -11,10 +11,11 @@
 //                 workgroup, 16 P positions per pass of the weight, the waves'
 //                 partial sums added in fixed order in LDS
 //   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
-//   k_attn        split-KV block attention: a workgroup takes 128 keys of one
-//                 KV head for 16 block positions, one wave per query head of
-//                 the group; the chunk's K and V (transposed) staged in LDS in
-//                 one memory round, S = K Q^T and O = P V on the matrix cores
+//   k_attn        split-KV block attention: a workgroup takes a chunk of
+//                 64-key sub-chunks of one KV head for 16 block positions, one
+//                 wave per query head of the group, with an online softmax;
+//                 each sub-chunk's K and V (transposed) staged in LDS while the
+//                 next one loads; S = K Q^T and O = P V on the matrix cores
 //   k_attn_comb   merges the chunks of every query row in chunk order
 // Every reduction runs in a fixed order, so two runs give identical bits.
 #include "xp_internal.h"
@@ -23,8 +24,7 @@ namespace xp {
 
 constexpr int kLinWaves = 8;        // k-split of k_linear
 constexpr int kLinMaxStream = 64;   // positions up to which the projections stream
-constexpr int kAttnKeys = 128;      // keys per attention workgroup (64 at small batch)
-constexpr int kAttnKeysSmall = 64;
+constexpr int kAttnWgs = 1024;      // attention workgroups aimed at per call
 constexpr int kAttnPad = 4;         // LDS row padding (bf16) of the transposed V
 constexpr int kHd = 128;            // head_dim (the only one built)
 
@@ -231,38 +231,47 @@ __global__ __launch_bounds__(256) void k_qkrope(
 }
 
 // ---------------------------------------------------------------------------
-// Split-KV block attention.  Grid (chunk s, KV head, sequence b x position
-// block pb); wave w is query head kvh * grp + w for block positions
-// 16 pb .. 16 pb + 15.  Key kk of sequence b is context key kk (kk < C) or
-// block key kk - C (C <= kk < C + B); keys from C + B on do not exist.
+// Split-KV block attention, flash-decoding style.  Grid (chunk s, KV head,
+// sequence b x position block pb); wave w is query head kvh * GRP + w for
+// block positions 16 pb .. 16 pb + 15; a chunk is nsub sub-chunks of 64 keys,
+// walked with an online softmax.  Key kk of sequence b is context key kk
+// (kk < C) or block key kk - C (C <= kk < C + B); keys from C + B on do not
+// exist.
 //
-// S^T = K Q^T per 16-key tile (A: key rows, B: the wave's q): lane l holds
-// keys 16 t + 4 (l / 16) + i for query l % 16.  After the chunk maximum and
-// the numerators e = exp(s - m) (each as two bf16 parts), O = P V per 32
-// keys, once per part: the A operand's
-// eight k slots of lane l are its own e of tiles 2u and 2u + 1 (keys
-// 32 u + 4 (l/16) + 0..3 and 32 u + 16 + 4 (l/16) + 0..3), and the B operand
-// takes V of the same keys from the transposed LDS copy; the output lane holds
-// queries 4 (l / 16) + i for d = 16 dt + l % 16.  Written per (chunk, query):
-// O (relative to the chunk maximum m), m and l = sum of the numerators.
+// Per sub-chunk: its K (as is) and V (transposed) go through one LDS buffer;
+// the next sub-chunk's 16-byte items are loaded into registers before the
+// current one is computed, so its latency hides behind that work.  S^T = K Q^T
+// per 16-key tile (A: key rows, B: the wave's q): lane l holds keys
+// 16 t + 4 (l / 16) + i for query l % 16.  With the running maximum m (per
+// query) the numerators e = exp(s - m) enter O = P V as two bf16 parts: the A
+// operand's eight k slots of lane l are its own e of tiles 2u and 2u + 1
+// (keys 32 u + 4 (l/16) + 0..3 and 32 u + 16 + 4 (l/16) + 0..3), the B operand
+// takes V of the same keys from the transposed copy, and the output lane holds
+// queries 4 (l / 16) + i for d = 16 dt + l % 16.  A new maximum rescales O and
+// l by exp(m_old - m_new).  Written per (chunk, query): O (relative to the
+// chunk's final maximum m), m and l.
 // ---------------------------------------------------------------------------
-template <int KEYS>
-__global__ __launch_bounds__(512) void k_attn(
+constexpr int kSub = 64;            // keys per sub-chunk (one LDS stage)
+
+template <int GRP>
+__global__ __launch_bounds__(GRP * kWave) void k_attn(
     const uint16_t* __restrict__ qn, const uint16_t* __restrict__ kcache,
     const uint16_t* __restrict__ vcache, const uint16_t* __restrict__ kb,
     const uint16_t* __restrict__ vb, const int32_t* __restrict__ ctx_len, int Cmax, int B,
-    int npb, int nh, int nkv, int grp, int causal, int ns, float* __restrict__ opart,
+    int npb, int nh, int nkv, int causal, int ns, int nsub, float* __restrict__ opart,
     float* __restrict__ mlpart) {
-  __shared__ __align__(16) uint16_t Ks[KEYS][kHd + 8];        // +16 B per row
-  __shared__ __align__(16) uint16_t Vt[kHd][KEYS + kAttnPad];
+  constexpr int kItems = kSub * (kHd / 8);       // 16-byte items of K (and of V) per sub-chunk
+  constexpr int PER = kItems / (GRP * kWave);    // items per thread
+  __shared__ __align__(16) uint16_t Ks[kSub][kHd + 8];        // +16 B per row
+  __shared__ __align__(16) uint16_t Vt[kHd][kSub + kAttnPad];
   const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
   const int b = z / npb, pb = z - b * npb;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, li = lane & 15;
   int C = ctx_len[b];
   C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
-  const int nkeys = C + B, kbase = s * KEYS;
-  const size_t pidx = (((size_t)z * nkv + kvh) * ns + s) * grp + wave;
+  const int nkeys = C + B, kbase = s * kSub * nsub;
+  const size_t pidx = (((size_t)z * nkv + kvh) * ns + s) * GRP + wave;
   float* op = opart + pidx * (kTile * kHd);
   float* ml = mlpart + pidx * (2 * kTile);
   if (kbase >= nkeys) {                          // whole workgroup: no key in this chunk
@@ -272,126 +281,139 @@ __global__ __launch_bounds__(512) void k_attn(
     }
     return;
   }
+  const int left = (nkeys - kbase + kSub - 1) / kSub;
+  const int nj = left < nsub ? left : nsub;      // sub-chunks holding keys (>= 1)
   // row of key kk (< nkeys) in the cache or in the block's own keys
   auto krow = [&](int kk, const uint16_t* cache, const uint16_t* blk) -> const uint16_t* {
     if (kk < C) return cache + (((size_t)b * Cmax + kk) * nkv + kvh) * kHd;
     return blk + (((size_t)b * B + (kk - C)) * nkv + kvh) * kHd;
   };
-
-  // K and V of the chunk into LDS (K as is, V transposed: Vt[d][key]), 16
-  // bytes per item, 16 items per thread loaded before any is stored: one
-  // memory round for the whole chunk; keys past the end are zeros
-  constexpr int kItems = KEYS * (kHd / 8), kStage = 16;
-  for (int r = 0; r < kItems; r += blockDim.x * kStage) {
-    u32x4 kv[kStage], vv[kStage];
+  // the items of sub-chunk j into registers (keys past the end are zeros)
+  auto load_sub = [&](int j, u32x4 (&kv)[PER], u32x4 (&vv)[PER]) {
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) {
-      const int it = r + threadIdx.x + blockDim.x * j;
-      const int key = (it >> 4) & (KEYS - 1), c = it & 15, kk = kbase + key;
-      const bool ok = it < kItems && kk < nkeys;
+    for (int e = 0; e < PER; ++e) {
+      const int it = threadIdx.x + GRP * kWave * e;
+      const int kk = kbase + j * kSub + (it >> 4), c = it & 15;
+      const bool ok = kk < nkeys;
       const int kc = ok ? kk : nkeys - 1;
-      kv[j] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
-      vv[j] = ok ? ld16(krow(kc, vcache, vb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      kv[e] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      vv[e] = ok ? ld16(krow(kc, vcache, vb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
     }
+  };
+  auto store_sub = [&](const u32x4 (&kv)[PER], const u32x4 (&vv)[PER]) {
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) {
-      const int it = r + threadIdx.x + blockDim.x * j;
-      if (it < kItems) {
-        const int key = it >> 4, c = it & 15;
-        *reinterpret_cast<u32x4*>(&Ks[key][8 * c]) = kv[j];
-        const u32x4 v = vv[j];
-        Vt[8 * c + 0][key] = (uint16_t)(v.x & 0xFFFFu);
-        Vt[8 * c + 1][key] = (uint16_t)(v.x >> 16);
-        Vt[8 * c + 2][key] = (uint16_t)(v.y & 0xFFFFu);
-        Vt[8 * c + 3][key] = (uint16_t)(v.y >> 16);
-        Vt[8 * c + 4][key] = (uint16_t)(v.z & 0xFFFFu);
-        Vt[8 * c + 5][key] = (uint16_t)(v.z >> 16);
-        Vt[8 * c + 6][key] = (uint16_t)(v.w & 0xFFFFu);
-        Vt[8 * c + 7][key] = (uint16_t)(v.w >> 16);
-      }
+    for (int e = 0; e < PER; ++e) {
+      const int it = threadIdx.x + GRP * kWave * e;
+      const int key = it >> 4, c = it & 15;
+      *reinterpret_cast<u32x4*>(&Ks[key][8 * c]) = kv[e];
+      const u32x4 v = vv[e];
+      Vt[8 * c + 0][key] = (uint16_t)(v.x & 0xFFFFu);
+      Vt[8 * c + 1][key] = (uint16_t)(v.x >> 16);
+      Vt[8 * c + 2][key] = (uint16_t)(v.y & 0xFFFFu);
+      Vt[8 * c + 3][key] = (uint16_t)(v.y >> 16);
+      Vt[8 * c + 4][key] = (uint16_t)(v.z & 0xFFFFu);
+      Vt[8 * c + 5][key] = (uint16_t)(v.z >> 16);
+      Vt[8 * c + 6][key] = (uint16_t)(v.w & 0xFFFFu);
+      Vt[8 * c + 7][key] = (uint16_t)(v.w >> 16);
     }
-  }
+  };
 
-  // the wave's q (B operand): query li, head kvh * grp + wave
+  // the wave's q (B operand): query li, head kvh * GRP + wave
   const int p = pb * kTile + li;
   const bool qv = p < B;
   const uint16_t* qs =
-      qn + (((size_t)b * B + (qv ? p : 0)) * nh + (size_t)kvh * grp + wave) * kHd + 8 * g;
+      qn + (((size_t)b * B + (qv ? p : 0)) * nh + (size_t)kvh * GRP + wave) * kHd + 8 * g;
   u32x4 qf[kHd / 32];
 #pragma unroll
   for (int ks = 0; ks < kHd / 32; ++ks) qf[ks] = qv ? ld16(qs + 32 * ks) : u32x4{0u, 0u, 0u, 0u};
 
-  constexpr int NT = KEYS / kTile;
+  constexpr int NT = kSub / kTile;
   const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
-  __syncthreads();                               // Ks and Vt complete
-  const bool interior = kbase + KEYS <= C;       // a chunk of context keys only
-  floatx4 sc[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    u32x4 kf[kHd / 32];                          // A operand: key 16 t + li
-#pragma unroll
-    for (int ks = 0; ks < kHd / 32; ++ks)
-      kf[ks] = *reinterpret_cast<const u32x4*>(&Ks[kTile * t + li][32 * ks + 8 * g]);
-    floatx4 acc{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
-    if (interior) {                              // workgroup-uniform: every key visible
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sc[t][i] = qv ? acc[i] * scale : -INFINITY;
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kbase + kTile * t + 4 * g + i;
-        const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
-        sc[t][i] = vis ? acc[i] * scale : -INFINITY;
-      }
-    }
-  }
-  float mx = -INFINITY;
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-  // numerators e as a sum of two bf16 parts (hi = bf16(e), lo = bf16(e - hi):
-  // about 16 significant bits), both multiplied into O; the sum l is taken
-  // over the same two parts
-  uint32_t eh[NT][2], el[NT][2];
-  float lsum = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    uint16_t h[4], lo[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float e = mx == -INFINITY ? 0.f : __expf(sc[t][i] - mx);
-      h[i] = f32_to_bf16_rne(e);
-      lo[i] = f32_to_bf16_rne(e - bf16_to_f32(h[i]));
-      lsum += bf16_to_f32(h[i]) + bf16_to_f32(lo[i]);
-    }
-    eh[t][0] = h[0] | ((uint32_t)h[1] << 16);
-    eh[t][1] = h[2] | ((uint32_t)h[3] << 16);
-    el[t][0] = lo[0] | ((uint32_t)lo[1] << 16);
-    el[t][1] = lo[2] | ((uint32_t)lo[3] << 16);
-  }
-  lsum += __shfl_xor(lsum, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
-
+  float m_run = -INFINITY, l_run = 0.f;          // per query li
   floatx4 o[kHd / 16];
 #pragma unroll
   for (int dt = 0; dt < kHd / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  u32x4 kv[PER], vv[PER];
+  load_sub(0, kv, vv);
+  for (int j = 0; j < nj; ++j) {
+    __syncthreads();                             // every wave is done with sub-chunk j - 1
+    store_sub(kv, vv);
+    __syncthreads();                             // sub-chunk j is in LDS
+    load_sub(j + 1 < nj ? j + 1 : j, kv, vv);    // next (the last re-reads itself: no branch)
+    const int kb0 = kbase + j * kSub;
+    const bool interior = kb0 + kSub <= C;       // context keys only: every key visible
+    floatx4 sc[NT];
 #pragma unroll
-  for (int u = 0; u < NT / 2; ++u) {
-    const u32x4 ph{eh[2 * u][0], eh[2 * u][1], eh[2 * u + 1][0], eh[2 * u + 1][1]};
-    const u32x4 pl{el[2 * u][0], el[2 * u][1], el[2 * u + 1][0], el[2 * u + 1][1]};
+    for (int t = 0; t < NT; ++t) {
+      u32x4 kf[kHd / 32];                        // A operand: key 16 t + li
 #pragma unroll
-    for (int dt = 0; dt < kHd / 16; ++dt) {
-      const int d = 16 * dt + li;
-      const uint2 v0 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 4 * g]);
-      const uint2 v1 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 16 + 4 * g]);
-      const u32x4 vv{v0.x, v0.y, v1.x, v1.y};
-      o[dt] = Mfma<uint16_t>::mma(pl, vv, o[dt]);
-      o[dt] = Mfma<uint16_t>::mma(ph, vv, o[dt]);
+      for (int ks = 0; ks < kHd / 32; ++ks)
+        kf[ks] = *reinterpret_cast<const u32x4*>(&Ks[kTile * t + li][32 * ks + 8 * g]);
+      floatx4 acc{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
+      if (interior) {                            // workgroup-uniform
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sc[t][i] = qv ? acc[i] * scale : -INFINITY;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kb0 + kTile * t + 4 * g + i;
+          const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
+          sc[t][i] = vis ? acc[i] * scale : -INFINITY;
+        }
+      }
+    }
+    float mx = m_run;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float alpha = m_run == -INFINITY ? 0.f : __expf(m_run - mx);
+    // numerators as two bf16 parts; the sum is taken over the same parts
+    uint32_t eh[NT][2], el[NT][2];
+    float lsum = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      uint16_t h[4], lo[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = mx == -INFINITY ? 0.f : __expf(sc[t][i] - mx);
+        h[i] = f32_to_bf16_rne(e);
+        lo[i] = f32_to_bf16_rne(e - bf16_to_f32(h[i]));
+        lsum += bf16_to_f32(h[i]) + bf16_to_f32(lo[i]);
+      }
+      eh[t][0] = h[0] | ((uint32_t)h[1] << 16);
+      eh[t][1] = h[2] | ((uint32_t)h[3] << 16);
+      el[t][0] = lo[0] | ((uint32_t)lo[1] << 16);
+      el[t][1] = lo[2] | ((uint32_t)lo[3] << 16);
+    }
+    lsum += __shfl_xor(lsum, 16, kWave);
+    lsum += __shfl_xor(lsum, 32, kWave);
+    l_run = l_run * alpha + lsum;
+    m_run = mx;
+    // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ai = __shfl(alpha, 4 * g + i, kWave);
+#pragma unroll
+      for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
+    }
+#pragma unroll
+    for (int u = 0; u < NT / 2; ++u) {
+      const u32x4 ph{eh[2 * u][0], eh[2 * u][1], eh[2 * u + 1][0], eh[2 * u + 1][1]};
+      const u32x4 pl{el[2 * u][0], el[2 * u][1], el[2 * u + 1][0], el[2 * u + 1][1]};
+#pragma unroll
+      for (int dt = 0; dt < kHd / 16; ++dt) {
+        const int d = 16 * dt + li;
+        const uint2 v0 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 4 * g]);
+        const uint2 v1 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 16 + 4 * g]);
+        const u32x4 vvv{v0.x, v0.y, v1.x, v1.y};
+        o[dt] = Mfma<uint16_t>::mma(pl, vvv, o[dt]);
+        o[dt] = Mfma<uint16_t>::mma(ph, vvv, o[dt]);
+      }
     }
   }
 #pragma unroll
@@ -399,8 +421,8 @@ __global__ __launch_bounds__(512) void k_attn(
 #pragma unroll
     for (int i = 0; i < 4; ++i) op[(4 * g + i) * kHd + 16 * dt + li] = o[dt][i];
   if (lane < kTile) {
-    ml[2 * lane] = mx;
-    ml[2 * lane + 1] = lsum;
+    ml[2 * lane] = m_run;
+    ml[2 * lane + 1] = l_run;
   }
 }
 
@@ -489,7 +511,8 @@ struct xp_layer {
   int H, nh, nkv, ffn, grp;
   float eps, theta;
   const uint16_t *g_attn, *Wq, *Wk, *Wv, *g_q, *g_k, *Wo, *g_mlp, *Wg, *Wu, *Wd;
-  int max_batch, max_B, max_ctx, nsmax;
+  int max_batch, max_B, max_ctx;
+  size_t nparts;                     // attention partials the workspace holds
   void* ws = nullptr;
   float* x32 = nullptr;
   uint16_t* u = nullptr;
@@ -500,8 +523,6 @@ struct xp_layer {
   float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;
   uint16_t* act = nullptr;
 };
-
-constexpr int kSmallAttnWgs = 512;  // below this many 128-key workgroups, 64-key chunks
 
 static int attn_chunks(int C_max, int B, int keys) { return (C_max + B + keys - 1) / keys; }
 
@@ -547,13 +568,15 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   L->max_batch = max_batch;
   L->max_B = max_B;
   L->max_ctx = max_ctx;
-  L->nsmax = attn_chunks(max_ctx, max_B, kAttnKeys);
   const size_t Mx = (size_t)max_batch * max_B, H = L->H, nhd = (size_t)L->nh * kHd,
                kvd = (size_t)L->nkv * kHd, F = L->ffn;
   const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
-  // partials of 128-key chunks at the largest call, or of the 64-key chunks
-  // that small calls (fewer than kSmallAttnWgs 128-key workgroups) use
-  const size_t nparts = std::max(zmax * L->nkv * L->nsmax, (size_t)2 * kSmallAttnWgs) * grp;
+  // attention partials: a call has at most max(2 kAttnWgs, w64 / 256) + one
+  // per (sequence, position block, KV head) chunks, w64 its 64-key sub-chunks
+  const size_t w64max = zmax * L->nkv * (size_t)attn_chunks(max_ctx, max_B, kSub);
+  const size_t nparts =
+      (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + zmax * L->nkv) * grp;
+  L->nparts = nparts;
   struct Slice {
     void** p;
     size_t bytes;
@@ -638,16 +661,17 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
       ctx_len == nullptr || batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B ||
       C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1) || (causal != 0 && causal != 1))
     return XP_EINVAL;
-  if (attn_chunks(C_max, B, kAttnKeys) > L->nsmax) return XP_EINVAL;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
   const int npb = (B + kTile - 1) / kTile;
-  // 64-key chunks when 128-key ones would leave most CUs idle (their
-  // partials fit the 2 x kSmallAttnWgs reserved), 128-key ones otherwise
-  const bool small =
-      (size_t)batch * npb * nkv * attn_chunks(C_max, B, kAttnKeys) < (size_t)kSmallAttnWgs;
-  const int ns = attn_chunks(C_max, B, small ? kAttnKeysSmall : kAttnKeys);
+  // chunks of nsub 64-key sub-chunks: about kAttnWgs workgroups in all (one
+  // sub-chunk each at small calls), so that the partials stay few
+  const size_t w64 = (size_t)batch * npb * nkv * attn_chunks(C_max, B, kSub);
+  int nsub = (int)(w64 / kAttnWgs);
+  nsub = nsub < 1 ? 1 : (nsub > 256 ? 256 : nsub);
+  const int ns = attn_chunks(C_max, B, kSub * nsub);
+  if ((size_t)batch * npb * nkv * ns * grp > L->nparts) return XP_EINVAL;   // not reached
   float* hout = h_f32 ? h_f32 : L->h32;
 
   hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st, (const uint16_t*)x, H,
@@ -657,15 +681,15 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   const int qk_waves = M * (nh + 2 * nkv);
   hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M, B, nh,
                      nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn, L->kb, L->vb);
-  if (small)
-    hipLaunchKernelGGL(k_attn<kAttnKeysSmall>, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0,
-                       st, L->qn, (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb,
-                       L->vb, ctx_len, C_max, B, npb, nh, nkv, grp, causal, ns, L->opart,
-                       L->mlpart);
-  else
-    hipLaunchKernelGGL(k_attn<kAttnKeys>, dim3(ns, nkv, batch * npb), dim3(grp * kWave), 0, st,
-                       L->qn, (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb,
-                       ctx_len, C_max, B, npb, nh, nkv, grp, causal, ns, L->opart, L->mlpart);
+#define XP_ATTN(GG)                                                                           \
+  hipLaunchKernelGGL(k_attn<GG>, dim3(ns, nkv, batch * npb), dim3(GG * kWave), 0, st, L->qn, \
+                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb, ctx_len, \
+                     C_max, B, npb, nh, nkv, causal, ns, nsub, L->opart, L->mlpart)
+  if (grp == 1) XP_ATTN(1);
+  else if (grp == 2) XP_ATTN(2);
+  else if (grp == 4) XP_ATTN(4);
+  else XP_ATTN(8);
+#undef XP_ATTN
   const int cw = M * nh;
   hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart, L->mlpart, M, B,
                      npb, nh, nkv, grp, ns, L->attn);
