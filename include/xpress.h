@@ -280,6 +280,8 @@ xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t 
  *            the layer output (h_bf16 is the input of the base readout)
  * causal: 1 = block key j visible to block query i iff j <= i; 0 = every block
  * key visible (the drafter's bidirectional block).
+ * Calls on one layer share its workspace: issue them in stream order (one
+ * stream, or streams synchronized between calls).
  * Errors: XP_EINVAL (null handle or input, batch, B or C_max outside what the
  * layer was created for), before any launch; XP_EHIP if a launch fails.
  */
