@@ -39,6 +39,8 @@ CSRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc")
 TRAFFIC = {
     "qwen3-8b-bf16-B16-b1-greedy": ("k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md", "xp_lmhead.hip"),
     "qwen3-8b-bf16-B16-b32-greedy": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b32_traffic.md", "xp_gemm.hip"),
+    "qwen3-8b-bf16-B16-b8-sample": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b8_traffic.md", "xp_gemm.hip"),
+    "qwen3-8b-bf16-B32-b64-mixed": ("k_lmhead_gemm_qwen3-8b-bf16-B32-b64_traffic.md", "xp_gemm.hip"),
 }
 
 
