@@ -5,11 +5,13 @@
 //
 // Kernels, in launch order:
 //   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u
-//   k_linear      y = u W^T (+ residual), or the SwiGLU product of the gate
-//                 and up projections: W streamed once from HBM, split over the
-//                 8 waves of a workgroup along k, 16 output rows per
-//                 workgroup, 16 P positions per pass of the weight, the waves'
-//                 partial sums added in fixed order in LDS
+//   k_linear      (up to 64 positions) y = u W^T (+ residual), or the SwiGLU
+//                 product of the gate and up projections: W streamed from HBM,
+//                 split over the 8 waves of a workgroup along k, 16 or 32
+//                 output rows per workgroup, 16 P positions per pass of the
+//                 weight, the waves' partial sums added in fixed order in LDS;
+//                 above 64 positions the tiled GEMM of xp_lgemm.hip and
+//                 k_swiglu take the projections
 //   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
 //   k_attn        split-KV block attention: a workgroup takes a chunk of
 //                 64-key sub-chunks of one KV head for 16 block positions, one
@@ -76,10 +78,12 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H
 
 // ---------------------------------------------------------------------------
 // y[p][n] = sum_k X[p][k] W[n][k] (+ R[p][n]) for 16 rows n per workgroup
-// (blockIdx.x) and 16 P positions (blockIdx.y).  Up to three weights stacked
-// by rows share a launch (rows [0, n0) of W0, [n0, n0 + n1) of W1, the rest
-// of W2: the q, k and v projections of one input).  GLU: a workgroup takes the
-// same 16 rows of W0 (gate) and W1 (up) and writes bf16(silu(gate) * up).
+// (blockIdx.x; 32 in MODE 2) and 16 P positions (blockIdx.y).  Up to three
+// weights stacked by rows share a launch (rows [0, n0) of W0, [n0, n0 + n1)
+// of W1, the rest of W2: the q, k and v projections of one input).  MODE 1
+// (GLU): a workgroup takes the same 16 rows of W0 (gate) and W1 (up) and
+// writes bf16(silu(gate) * up).  MODE 2: two consecutive 16-row tiles share
+// every X fragment (used from two position blocks on).
 // Wave w multiplies the k range [w K/8, (w+1) K/8): 16-row x 32-k W
 // fragments (A) against the positions' X fragments (B) on
 // v_mfma_f32_16x16x32_bf16, 8 / P k steps of loads issued before their
