@@ -107,6 +107,16 @@ def test_layer_projections_as_gemm_with_256_tiles():
     layer.close()
 
 
+def test_layer_largest_hidden_size():
+    """H = 8192, the largest built: 32 values per thread in the RMSNorm row,
+    K = 8192 in the q/k/v, gate and up projections."""
+    _say("case: layer H=8192 heads 4/2 ffn=256 B=8 batch=1 ctx=[50]")
+    w, weights, inp = _case(8192, 4, 2, 256, 8, 1, [50], index=871)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
 def test_layer_run_to_run_and_cache_past_context_unread():
     import torch
     from paper_2608_02438_amd.xpress import device_tensor
