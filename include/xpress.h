@@ -236,7 +236,8 @@ xp_status xp_device_errors(xp_handle* h, uint32_t* out, void* stream);
  *   g_q [hd], g_k [hd], Wo [H][n_heads*hd], g_mlp [H], Wg [ffn][H],
  *   Wu [ffn][H], Wd [H][ffn]
  * Built: head_dim 128; n_heads / n_kv in {1, 2, 4, 8}; H, n_heads*128 and ffn
- * multiples of 256; H <= 8192.
+ * multiples of 256; H <= 8192.  Every pointer 16-byte aligned (the kernels
+ * read and write 16 bytes at a time).
  */
 typedef struct {
   int32_t H, n_heads, n_kv, head_dim, ffn;
@@ -262,8 +263,8 @@ typedef struct xp_layer xp_layer;
  * and contexts of up to max_ctx keys on the current device; allocates its
  * workspace (freed by xp_layer_destroy).  The weights are referenced, not
  * copied: they must stay valid while the layer is used.
- * Errors: XP_EINVAL (null, sizes), XP_EUNSUPPORTED (shapes outside the built
- * set), XP_ENOMEM, XP_EHIP.  *out is NULL on error.
+ * Errors: XP_EINVAL (null or misaligned pointers, sizes), XP_EUNSUPPORTED
+ * (shapes outside the built set), XP_ENOMEM, XP_EHIP.  *out is NULL on error.
  */
 xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
                           int32_t max_ctx, xp_layer** out);
@@ -282,8 +283,10 @@ xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t 
  * key visible (the drafter's bidirectional block).
  * Calls on one layer share its workspace: issue them in stream order (one
  * stream, or streams synchronized between calls).
- * Errors: XP_EINVAL (null handle or input, batch, B or C_max outside what the
- * layer was created for), before any launch; XP_EHIP if a launch fails.
+ * Every pointer 16-byte aligned.
+ * Errors: XP_EINVAL (null handle or input, a misaligned pointer, batch, B or
+ * C_max outside what the layer was created for), before any launch; XP_EHIP
+ * if a launch fails.
  */
 xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal, const void* x,
                            const void* k_cache, const void* v_cache, int32_t C_max,

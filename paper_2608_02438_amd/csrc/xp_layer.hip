@@ -47,20 +47,37 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H
                                                  const uint16_t* __restrict__ g, float eps,
                                                  float* __restrict__ x32,
                                                  uint16_t* __restrict__ u) {
-  constexpr int kPer = 8192 / 256;               // H <= 8192: the row stays in registers
+  // chunks of 8 consecutive elements (16-byte bf16 loads and stores); H is a
+  // multiple of 256 up to 8192, so a thread takes at most 4 chunks
+  constexpr int kPer = 8192 / 8 / 256;
   __shared__ float part[4];
   const size_t row = blockIdx.x;
-  const int tid = threadIdx.x;
-  float v[kPer];
+  const int tid = threadIdx.x, nch = H / 8;
+  float v[kPer][8];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {               // clamped loads: none under a branch
-    const int i = tid + 256 * j, ic = i < H ? i : H - 1;
-    const float t = to_f32<TI>(x[row * H + ic]);
-    v[j] = i < H ? t : 0.f;
+    const int c = tid + 256 * j, cc = c < nch ? c : nch - 1;
+    if constexpr (sizeof(TI) == 2) {
+      const u32x4 q = ld16(x + row * H + 8 * (size_t)cc);
+      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[j][2 * e] = bf16_to_f32((uint16_t)(w[e] & 0xFFFFu));
+        v[j][2 * e + 1] = bf16_to_f32((uint16_t)(w[e] >> 16));
+      }
+    } else {
+      const float4 a = *reinterpret_cast<const float4*>(x + row * H + 8 * (size_t)cc);
+      const float4 b = *reinterpret_cast<const float4*>(x + row * H + 8 * (size_t)cc + 4);
+      v[j][0] = a.x; v[j][1] = a.y; v[j][2] = a.z; v[j][3] = a.w;
+      v[j][4] = b.x; v[j][5] = b.y; v[j][6] = b.z; v[j][7] = b.w;
+    }
   }
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) ss += v[j] * v[j];
+  for (int j = 0; j < kPer; ++j)
+    if (tid + 256 * j < nch)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[j][e] * v[j][e];
   ss = wave_sum(ss);
   if ((tid & 63) == 0) part[tid >> 6] = ss;
   __syncthreads();
@@ -68,10 +85,25 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H
   const float r = 1.f / sqrtf(tot / (float)H + eps);
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
-    const int i = tid + 256 * j;
-    if (i < H) {
-      if (x32) x32[row * H + i] = v[j];
-      u[row * H + i] = f32_to_bf16_rne(v[j] * r * bf16_to_f32(g[i]));
+    const int c = tid + 256 * j;
+    if (c < nch) {
+      const u32x4 gq = ld16(g + 8 * (size_t)c);
+      const uint32_t gw[4] = {gq.x, gq.y, gq.z, gq.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float g0 = bf16_to_f32((uint16_t)(gw[e] & 0xFFFFu));
+        const float g1 = bf16_to_f32((uint16_t)(gw[e] >> 16));
+        o[e] = f32_to_bf16_rne(v[j][2 * e] * r * g0) |
+               ((uint32_t)f32_to_bf16_rne(v[j][2 * e + 1] * r * g1) << 16);
+      }
+      *reinterpret_cast<u32x4*>(u + row * H + 8 * (size_t)c) = u32x4{o[0], o[1], o[2], o[3]};
+      if (x32) {
+        *reinterpret_cast<float4*>(x32 + row * H + 8 * (size_t)c) =
+            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+        *reinterpret_cast<float4*>(x32 + row * H + 8 * (size_t)c + 4) =
+            make_float4(v[j][4], v[j][5], v[j][6], v[j][7]);
+      }
     }
   }
 }
@@ -540,7 +572,7 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   const void* ptrs[] = {w->g_attn, w->Wq, w->Wk, w->Wv, w->g_q, w->g_k,
                         w->Wo,     w->g_mlp, w->Wg, w->Wu, w->Wd};
   for (const void* p : ptrs)
-    if (p == nullptr) return XP_EINVAL;
+    if (p == nullptr || reinterpret_cast<uintptr_t>(p) % 16 != 0) return XP_EINVAL;
   if (w->H < 1 || w->n_heads < 1 || w->n_kv < 1 || w->ffn < 1 || w->head_dim < 1 ||
       !(w->eps >= 0.f) || !(w->rope_theta > 0.f))
     return XP_EINVAL;
@@ -665,6 +697,8 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
       ctx_len == nullptr || batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B ||
       C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1) || (causal != 0 && causal != 1))
     return XP_EINVAL;
+  for (const void* q : {x, k_cache, v_cache, (const void*)h_f32, (const void*)h_bf16})
+    if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return XP_EINVAL;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;

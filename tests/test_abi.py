@@ -124,6 +124,7 @@ def _layer_weights(**kw):
     (dict(eps=-1.0), X.XP_EINVAL),
     (dict(Wd=None), X.XP_EINVAL),
     (dict(g_q=None), X.XP_EINVAL),
+    (dict(Wo=0x1008), X.XP_EINVAL),               # not 16-byte aligned
 ])
 def test_layer_create_rejects_bad_arguments_without_a_gpu(change, status):
     L = X.load_library()
