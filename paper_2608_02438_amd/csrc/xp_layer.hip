@@ -5,7 +5,11 @@
 //
 // Kernels, in launch order:
 //   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u
-//   k_linear      (up to 64 positions) y = u W^T (+ residual), or the SwiGLU
+//   k_gemv_sk     (one block of up to 16 positions, K <= 4096) y = u W^T
+//                 (+ residual) in the LM-head stream kernel's manner: x in
+//                 LDS, stream-K items with line-complete loads, per-wave LDS
+//                 transpose; gate and up side by side, then k_swiglu
+//   k_linear      (otherwise up to 64 positions) y = u W^T (+ residual), or the SwiGLU
 //                 product of the gate and up projections: W streamed from HBM,
 //                 split over the 8 waves of a workgroup along k, 16 or 32
 //                 output rows per workgroup, 16 P positions per pass of the
@@ -224,6 +228,176 @@ __global__ __launch_bounds__(kLinWaves * kWave, 2) void k_linear(
       }
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// The same projections for one block of up to 16 positions and K <= 4096, in
+// the manner of the LM-head stream kernel (A1): x (16 positions x K) sits in
+// LDS for the whole kernel; every wave takes a contiguous share of its
+// workgroup's (16-row tile, 64-k group) items, loads each item with two
+// line-complete instructions (8 rows x 128 B), transposes it through a 2 KB
+// per-wave LDS tile into operand order and keeps PF items in flight.  A tile
+// whose items straddle waves is finished at the end, its partial tiles added
+// in wave order (= k order).  Rows of up to three stacked weights (boundaries
+// multiples of 16).  Output: y[p][n] (+ R) row-major, fp32 and / or bf16.
+// ---------------------------------------------------------------------------
+constexpr int kGsWaves = 16;
+constexpr int kGsPF = 5;                // items in flight per wave
+constexpr int kGsXChunks = 512;         // 16-byte chunks of x per position (K <= 4096)
+
+__device__ __forceinline__ int gs_slot(int row, int c) { return row * 8 + (c ^ ((row & 7) ^ (row >> 3))); }
+
+__global__ __launch_bounds__(kGsWaves * kWave) void k_gemv_sk(
+    const uint16_t* __restrict__ W0, const uint16_t* __restrict__ W1,
+    const uint16_t* __restrict__ W2, int n0, int n1, int N, int K,
+    const uint16_t* __restrict__ X, int M, int U, const float* __restrict__ R, int ldr,
+    float* __restrict__ Y, uint16_t* __restrict__ Yb, int ldy) {
+  __shared__ u32x4 lds[16 * kGsXChunks + kGsWaves * 128];     // x (128 KB) + transpose tiles
+  u32x4* xl = lds;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  u32x4* tb = lds + 16 * kGsXChunks + wave * 128;
+  const int u = blockIdx.x, ntiles = N / kTile;
+  const int tlo = unit_tile_lo(u, ntiles, U), thi = unit_tile_lo(u + 1, ntiles, U);
+  const int nch = K / 8, G = K / 64;                          // chunks per row, items per tile
+  const int NI = (thi - tlo) * G;
+  auto wlo = [&](int w) { return (int)(((long)w * NI) / kGsWaves); };
+  const int i0 = wlo(wave), i1 = wlo(wave + 1);
+
+  // x: every thread issues its (at most 8) chunk loads at once; positions
+  // past M are loaded from position M - 1 and zeroed
+  constexpr int kXPer = 16 * kGsXChunks / (kGsWaves * kWave);
+  u32x4 xv[kXPer];
+#pragma unroll
+  for (int j = 0; j < kXPer; ++j) {
+    int e = threadIdx.x + kGsWaves * kWave * j;
+    e = e < 16 * nch ? e : 0;
+    const int pr = e / nch;
+    xv[j] = ld16(X + (size_t)(pr < M ? pr : M - 1) * K + (size_t)(e % nch) * 8);
+  }
+  // load role: 8 lanes per row, lane -> (row ri of 8, chunk lc of 8)
+  const int ri = lane >> 3, lc = lane & 7;
+  // MFMA role: row / position li, k-group g
+  const int li = lane & 15, g = lane >> 4;
+  const bool pact = li < M;
+  // item counters of the next load: tile (relative) and k-group; frozen at the
+  // wave's last item, so loads past the end re-read it
+  int lt = G > 0 ? i0 / G : 0, lq = i0 - lt * G, ln = i0;
+  auto load_item = [&](u32x4 (&r)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = (tlo + lt) * kTile + 8 * j + ri;
+      const uint16_t* w = row < n0 ? W0 + (size_t)row * K
+                        : row < n0 + n1 ? W1 + (size_t)(row - n0) * K
+                                        : W2 + (size_t)(row - n0 - n1) * K;
+      r[j] = ld16_nt(w + (size_t)(8 * lq + lc) * 8);
+    }
+    const int adv = ln + 1 < i1 ? 1 : 0;                  // scalar, branch-free
+    ln += adv;
+    lq += adv;
+    const int wrap = lq == G ? 1 : 0;
+    lq = wrap ? 0 : lq;
+    lt += wrap;
+  };
+  auto finalize = [&](floatx4 acc, int t) {
+    const int n = t * kTile + 4 * g;
+    if (pact) {
+      if (R) acc += *reinterpret_cast<const floatx4*>(R + (size_t)li * ldr + n);
+      if (Y) *reinterpret_cast<floatx4*>(Y + (size_t)li * ldy + n) = acc;
+      if (Yb) {
+        const uint32_t lo = f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
+        const uint32_t hi = f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
+        *reinterpret_cast<uint2*>(Yb + (size_t)li * ldy + n) = make_uint2(lo, hi);
+      }
+    }
+  };
+  const int tf = G > 0 ? i0 / G : 0;                      // first (relative) tile of the wave
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f}, part0 = acc, part1 = acc;
+  int ct = tf, cq = i0 - tf * G;                          // item being computed
+  auto step = [&](const u32x4 (&r)[2], int i) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) tb[gs_slot(8 * j + ri, lc)] = r[j];
+    wave_lds_order();
+#pragma unroll
+    for (int uu = 0; uu < 2; ++uu) {
+      const int c = 4 * uu + g;
+      const u32x4 a = tb[gs_slot(li, c)];
+      const int cc = 8 * cq + c;
+      const u32x4 b = xl[li * kGsXChunks + ((cc & ~15) | ((cc & 15) ^ li))];
+      acc = Mfma<uint16_t>::mma(a, b, acc);
+    }
+    wave_lds_order();
+    if (cq == G - 1 || i == i1 - 1) {                     // end of a tile segment
+      if (cq == G - 1 && ct * G >= i0)
+        finalize(acc, tlo + ct);
+      else if (ct == tf)
+        part0 = acc;
+      else
+        part1 = acc;
+      acc = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (++cq == G) {
+      cq = 0;
+      ++ct;
+    }
+  };
+
+  asm volatile("" ::: "memory");
+  u32x4 ring[kGsPF][2];
+  if (i0 < i1) {
+#pragma unroll
+    for (int q = 0; q < kGsPF; ++q) load_item(ring[q]);
+  }
+  asm volatile("" ::: "memory");
+  // no guard on the stores (a guarded store would sink its load): chunks past
+  // 16 * nch were loaded from chunk 0 and rewrite chunk 0's slot with its value
+#pragma unroll
+  for (int j = 0; j < kXPer; ++j) {
+    int e = threadIdx.x + kGsWaves * kWave * j;
+    e = e < 16 * nch ? e : 0;
+    const int pp = e / nch, c = e % nch;
+    xl[pp * kGsXChunks + ((c & ~15) | ((c & 15) ^ pp))] = pp < M ? xv[j] : u32x4{0u, 0u, 0u, 0u};
+  }
+  lds_barrier();                                          // x is in LDS; items stay in flight
+  if (i0 < i1) {
+    int i = i0;
+    for (; i + kGsPF <= i1; i += kGsPF) {
+#pragma unroll
+      for (int q = 0; q < kGsPF; ++q) {
+        step(ring[q], i + q);
+        load_item(ring[q]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kGsPF; ++q)
+      if (i + q < i1) step(ring[q], i + q);
+  }
+  // tiles split between waves: partial tiles through LDS (the x area is free)
+  __syncthreads();
+  floatx4* fx = reinterpret_cast<floatx4*>(lds);          // [wave][2][64]
+  fx[(wave * 2 + 0) * 64 + lane] = part0;
+  fx[(wave * 2 + 1) * 64 + lane] = part1;
+  __syncthreads();
+  if (i0 < i1) {
+    const int tl = (i1 - 1) / G;
+    int tfin = -1;
+    floatx4 a = part0;
+    if (i0 % G == 0 && i1 < (tf + 1) * G) {               // starts a tile it does not finish
+      tfin = tf;
+    } else if (tl > tf && i1 % G != 0) {                  // last tile started here, unfinished
+      tfin = tl;
+      a = part1;
+    }
+    if (tfin >= 0) {
+      for (int w = wave + 1; w < kGsWaves && wlo(w) < (tfin + 1) * G; ++w) {
+        if (wlo(w + 1) > wlo(w)) {
+          const floatx4 o = fx[(w * 2 + 0) * 64 + lane];
+          a[0] += o[0]; a[1] += o[1]; a[2] += o[2]; a[3] += o[3];
+        }
+      }
+      finalize(a, tlo + tfin);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0070);                     // the re-read loads past the end
 }
 
 // ---------------------------------------------------------------------------
@@ -623,7 +797,7 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
       {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
       {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
       {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
-      {(void**)&L->GU, (Mx > kLinMaxStream ? Mx : 0) * 2 * F * 4},
+      {(void**)&L->GU, (Mx > kLinMaxStream || max_B <= kTile ? Mx : 0) * 2 * F * 4},
   };
   size_t total = 0;
   for (auto& s : sl) total += (s.bytes + 255) / 256 * 256;
@@ -653,6 +827,25 @@ extern "C" void xp_layer_destroy(xp_layer* L) {
 static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0, int n1,
                    int N, int K, const uint16_t* X, int M, const float* R, int ldr, float* Y,
                    uint16_t* Yb, int ldy, bool glu, hipStream_t st, float* GU = nullptr) {
+  // one block of positions and x small enough for LDS: the stream-K kernel
+  // (gate and up side by side, then SwiGLU)
+  if (M <= kTile && K <= 8 * kGsXChunks && K % 64 == 0 && N % kTile == 0 && n0 % kTile == 0 &&
+      n1 % kTile == 0) {
+    const int rows = glu ? 2 * N : N, ntl = rows / kTile;
+    const int U = ntl < 256 ? ntl : 256;
+    if (glu) {
+      hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W1, N, N,
+                         2 * N, K, X, M, U, (const float*)nullptr, 0, GU, (uint16_t*)nullptr,
+                         2 * N);
+      const size_t na = (size_t)M * N;
+      hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
+                         na, Yb);
+    } else {
+      hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W2, n0, n1,
+                         N, K, X, M, U, R, ldr, Y, Yb, ldy);
+    }
+    return;
+  }
   // above one 64-position pass of the stream: the tiled GEMM (weights read
   // once per 128 or 256 positions); gate and up side by side, then SwiGLU
   if (M > kLinMaxStream && (glu ? layer_gemm_ok(N, N, 2 * N, K, M) : layer_gemm_ok(n0, n1, N, K, M))) {
