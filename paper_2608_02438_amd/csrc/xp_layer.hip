@@ -472,6 +472,7 @@ __global__ __launch_bounds__(GRP * kWave) void k_attn(
     float* __restrict__ mlpart) {
   constexpr int kItems = kSub * (kHd / 8);       // 16-byte items of K (and of V) per sub-chunk
   constexpr int PER = kItems / (GRP * kWave);    // items per thread
+  static_assert(PER % 2 == 0, "items come in key pairs");
   __shared__ __align__(16) uint16_t Ks[kSub][kHd + 8];        // +16 B per row
   __shared__ __align__(16) uint16_t Vt[kHd][kSub + kAttnPad];
   const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
@@ -502,29 +503,31 @@ __global__ __launch_bounds__(GRP * kWave) void k_attn(
   auto load_sub = [&](int j, u32x4 (&kv)[PER], u32x4 (&vv)[PER]) {
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const int it = threadIdx.x + GRP * kWave * e;
-      const int kk = kbase + j * kSub + (it >> 4), c = it & 15;
+      const int ip = threadIdx.x + GRP * kWave * (e >> 1);
+      const int kk = kbase + j * kSub + 2 * (ip >> 4) + (e & 1), c = ip & 15;
       const bool ok = kk < nkeys;
       const int kc = ok ? kk : nkeys - 1;
       kv[e] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
       vv[e] = ok ? ld16(krow(kc, vcache, vb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
     }
   };
+  // items 2e and 2e + 1 of a thread are keys 2 kq and 2 kq + 1 of one 16-byte
+  // column c: V is transposed with one 32-bit LDS store per d (both keys)
   auto store_sub = [&](const u32x4 (&kv)[PER], const u32x4 (&vv)[PER]) {
 #pragma unroll
-    for (int e = 0; e < PER; ++e) {
-      const int it = threadIdx.x + GRP * kWave * e;
-      const int key = it >> 4, c = it & 15;
+    for (int e = 0; e < PER; e += 2) {
+      const int ip = threadIdx.x + GRP * kWave * (e >> 1);
+      const int key = 2 * (ip >> 4), c = ip & 15;
       *reinterpret_cast<u32x4*>(&Ks[key][8 * c]) = kv[e];
-      const u32x4 v = vv[e];
-      Vt[8 * c + 0][key] = (uint16_t)(v.x & 0xFFFFu);
-      Vt[8 * c + 1][key] = (uint16_t)(v.x >> 16);
-      Vt[8 * c + 2][key] = (uint16_t)(v.y & 0xFFFFu);
-      Vt[8 * c + 3][key] = (uint16_t)(v.y >> 16);
-      Vt[8 * c + 4][key] = (uint16_t)(v.z & 0xFFFFu);
-      Vt[8 * c + 5][key] = (uint16_t)(v.z >> 16);
-      Vt[8 * c + 6][key] = (uint16_t)(v.w & 0xFFFFu);
-      Vt[8 * c + 7][key] = (uint16_t)(v.w >> 16);
+      *reinterpret_cast<u32x4*>(&Ks[key + 1][8 * c]) = kv[e + 1];
+      const uint32_t a[4] = {vv[e].x, vv[e].y, vv[e].z, vv[e].w};
+      const uint32_t bb[4] = {vv[e + 1].x, vv[e + 1].y, vv[e + 1].z, vv[e + 1].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        *reinterpret_cast<uint32_t*>(&Vt[8 * c + 2 * q][key]) = (a[q] & 0xFFFFu) | (bb[q] << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[8 * c + 2 * q + 1][key]) =
+            (a[q] >> 16) | (bb[q] & 0xFFFF0000u);
+      }
     }
   };
 
@@ -603,13 +606,16 @@ __global__ __launch_bounds__(GRP * kWave) void k_attn(
     lsum += __shfl_xor(lsum, 16, kWave);
     lsum += __shfl_xor(lsum, 32, kWave);
     l_run = l_run * alpha + lsum;
+    const bool moved = __ballot(mx != m_run) != 0;   // wave-uniform: else every alpha is 1
     m_run = mx;
     // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
+    if (moved) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float ai = __shfl(alpha, 4 * g + i, kWave);
+      for (int i = 0; i < 4; ++i) {
+        const float ai = __shfl(alpha, 4 * g + i, kWave);
 #pragma unroll
-      for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
+        for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
+      }
     }
 #pragma unroll
     for (int u = 0; u < NT / 2; ++u) {
