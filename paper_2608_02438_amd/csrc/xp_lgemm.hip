@@ -4,7 +4,8 @@
 //
 // Above one 64-position pass of the streaming projection kernel the weights
 // would be re-read per 64 positions; here a tile is BN weight rows x BM
-// positions (128 x 128 up to 128 positions, 256 x 256 above), so every weight
+// positions (256 x 256 where every workgroup then gets two tiles or more, else
+// 128 x 128), so every weight
 // is read once per BM positions.  Up to three weights stacked by rows share
 // the launch (the q, k and v projections of one input); BN divides each
 // one's row count, so a tile never straddles two of them.
@@ -247,15 +248,23 @@ namespace xp {
 
 // Rows of W0 | W1 | W2 stacked (n0, n1 rows of the first two; BN must divide
 // n0, n1 and N); K a multiple of 32; M >= 1.
+// Position and row tile size: 256 x 256 only when that still gives every
+// workgroup of the persistent grid two tiles or more; else 128 x 128 (four
+// times as many tiles for the same work).
+static int layer_bm(int N, int M) {
+  const long t256 = (long)(N / 256) * ((M + 255) / 256);
+  return M <= 128 || t256 < 2 * 8 * kLPerXcd ? 128 : 256;
+}
+
 bool layer_gemm_ok(int n0, int n1, int N, int K, int M) {
-  const int bn = M <= 128 ? 128 : 256;
+  const int bn = layer_bm(N, M);
   return K % kLK == 0 && N % bn == 0 && n0 % bn == 0 && n1 % bn == 0 && M >= 1;
 }
 
 hipError_t launch_layer_gemm(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
                              int n1, int N, int K, const uint16_t* X, int M, const float* R,
                              int ldr, float* Y, uint16_t* Yb, int ldy, hipStream_t st) {
-  const int bm = M <= 128 ? 128 : 256;
+  const int bm = layer_bm(N, M);
   const int nMb = (M + bm - 1) / bm;
   int per = kLPerXcd / nMb * nMb;                // workgroups per XCD: whole position tiles
   per = per > 0 ? per : nMb;

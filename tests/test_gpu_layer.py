@@ -6,7 +6,8 @@ attention chunks (64-key ones for small calls, 128-key ones for large) with
 ragged context lengths (0, chunk boundaries),
 every built query-group size, blocks of 1, 8, 16 and 32 positions, and the
 three projection paths (streaming up to 64 positions, the tiled GEMM with
-128 x 128 tiles up to 128 and 256 x 256 above); the full-size case runs the
+128 x 128 tiles, and 256 x 256 ones where a launch has 512 of them or more);
+the full-size case runs the
 Qwen3-8B layer at batch 1 with a 2048-key context.
 
 Tolerance: h is compared in fp32 against the oracle's fp64 h with the bf16
@@ -96,12 +97,25 @@ def test_layer_large_call_takes_128_key_chunks():
     layer.close()
 
 
-def test_layer_projections_as_gemm_with_256_tiles():
-    """192 positions: the projections run as the tiled GEMM with 256 x 256
-    tiles (128 x 128 up to 128 positions, the streaming kernel up to 64)."""
+def test_layer_projections_as_gemm_with_128_tiles():
+    """192 positions: the projections run as the tiled GEMM with 128 x 128
+    tiles in three position tiles, the last one ragged (the streaming kernel
+    takes up to 64 positions)."""
     ctx = [5, 700, 33, 0, 256, 1000, 64, 129, 300, 2, 511, 90]
     _say(f"case: layer GEMM path H=512 heads 8/2 ffn=512 B=16 batch=12 ctx={ctx}")
     w, weights, inp = _case(512, 8, 2, 512, 16, 12, ctx, index=833)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
+def test_layer_gate_up_as_gemm_with_256_tiles():
+    """1024 positions and ffn = 16384: the gate/up launch (32768 stacked rows)
+    has 128 x 4 tiles of 256 x 256 and takes them; the other projections
+    stay on 128 x 128 tiles."""
+    ctx = [(37 * i) % 300 for i in range(32)]
+    _say(f"case: layer 256-tile GEMM H=256 heads 2/2 ffn=16384 B=32 batch=32 ctx={ctx}")
+    w, weights, inp = _case(256, 2, 2, 16384, 32, 32, ctx, index=857)
     h32, hb, layer, _ = _run(w, weights, inp)
     _check(w, weights, inp, h32, hb)
     layer.close()
