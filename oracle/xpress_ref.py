@@ -28,8 +28,8 @@ of softmax(l_k) with one uniform u_k per position that stays fixed across
 passes; the temperature-1 seed is the same inverse-CDF rule on softmax(s_k);
 the refined distribution used for verification is the one of the pass that
 produced the final token; for bf16 workloads z is the only activation rounded
-to bf16 (before Read), everything else is exact fp64 here.  Selections are
-taken on the logits rounded to fp32, the precision the device computes them in.
+to bf16 (before Read), everything else is exact fp64 here, selections
+included (argmax and softmax on the fp64 logits).
 
 Parity status: every function below is pinned by the CPU tests
 (tests/test_oracle_*.py) except the exact logit values of a trained refiner,
@@ -254,12 +254,12 @@ def fuse_mix_folded(W_in: np.ndarray, L: np.ndarray, At: np.ndarray) -> np.ndarr
 def select_greedy(l: np.ndarray):
     """argmax_v l_v with ties to the lowest index; returns (token, margin).
 
-    The comparison is taken on the logits rounded to fp32 (np.argmax returns
-    the first maximal index and treats -0 and +0 as equal).  The margin is the
-    fp64 gap between the two largest logits.
+    The comparison is taken on the fp64 logits (np.argmax returns the first
+    maximal index and treats -0 and +0 as equal).  The margin is the gap
+    between the two largest logits.
     """
-    l32 = l.astype(np.float32)
-    y = int(np.argmax(l32))
+    l = np.asarray(l, dtype=F64)
+    y = int(np.argmax(l))
     if l.shape[0] < 2:
         return y, np.inf
     top2 = np.partition(l, -2)[-2:]
@@ -284,10 +284,10 @@ def inverse_cdf(w: np.ndarray, u: float):
 
 
 def softmax_weights(l: np.ndarray, T: float = 1.0) -> np.ndarray:
-    """exp((l_v - max l) / T) in fp64 from the fp32-rounded logits: the
-    unnormalised softmax of the logits at temperature T > 0."""
-    l32 = l.astype(np.float32).astype(F64)
-    return np.exp((l32 - l32.max()) / float(T))
+    """exp((l_v - max l) / T) in fp64: the unnormalised softmax of the
+    logits at temperature T > 0."""
+    l = np.asarray(l, dtype=F64)
+    return np.exp((l - l.max()) / float(T))
 
 
 def select_sample(l: np.ndarray, u: float, T: float = 1.0):

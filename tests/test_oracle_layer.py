@@ -55,6 +55,37 @@ def test_rope_rotation_of_one_pair():
     assert np.allclose(r, [3 * c + 2 * s, -2 * c + 3 * s], rtol=1e-14)   # (a, b) -> (a c - b s, b c + a s)
 
 
+def test_rope_frequency_schedule_by_hand():
+    # theta = 1e4, head_dim 8: pair j = (j, j + 4) turns by pos * 1e4^(-2j/8)
+    # = pos * 10^-j radians, i.e. 3, 0.3, 0.03 and 0.003 at position 3
+    for j, ang in enumerate([3.0, 0.3, 0.03, 0.003]):
+        x = np.zeros((2, 8))
+        x[0, j] = 1.0                      # first member of pair j
+        x[1, j + 4] = 1.0                  # second member
+        y = L.rope(x, np.array([3, 3]), 1e4)
+        e0 = np.zeros(8)
+        e0[j], e0[j + 4] = np.cos(ang), np.sin(ang)
+        e1 = np.zeros(8)
+        e1[j], e1[j + 4] = -np.sin(ang), np.cos(ang)
+        assert np.allclose(y[0], e0, rtol=0, atol=1e-15), j
+        assert np.allclose(y[1], e1, rtol=0, atol=1e-15), j
+
+
+def test_swiglu_applies_silu_to_the_gate_by_hand():
+    """One FFN unit with gate 2 and up -1, attention switched off (Wo = 0):
+    silu(2) * -1 = -1.76159..., which rounds to the bf16 value -1.7578125, so
+    h = x1 + (-1.7578125, 0) with x1 = x = (1, 1).  SiLU on up instead,
+    silu(-1) * 2 = -0.53788... (bf16 -0.5390625), would give 0.4609375."""
+    w = dict(g_attn=np.ones(2), Wq=np.eye(2), Wk=np.eye(2), Wv=np.eye(2), g_q=np.ones(2),
+             g_k=np.ones(2), Wo=np.zeros((2, 2)), g_mlp=np.ones(2), Wg=np.array([[2.0, 0.0]]),
+             Wu=np.array([[0.0, -1.0]]), Wd=np.array([[1.0], [0.0]]))
+    P = L.LayerParams.from_arrays(w, 1, 1, 2, eps=0.0, theta=1e4)
+    x = np.ones((1, 1, 2))
+    h = L.layer_forward(P, x, np.zeros((1, 1, 1, 2)), np.zeros((1, 1, 1, 2)), np.array([0]))
+    assert h[0, 0, 0] == 1.0 - 1.7578125
+    assert h[0, 0, 1] == 1.0
+
+
 def test_rope_preserves_pair_norms_and_depends_on_relative_position():
     g = np.random.default_rng(3)
     hd = 16

@@ -83,11 +83,38 @@ def test_zero_readout_reduces_to_library_argmax():
     assert res.iters == 1
 
 
+@pytest.mark.parametrize("V,chunk", [(20011, 8192), (50, 7)])
+def test_base_logits_across_chunk_seams_is_the_exact_integer_product(V, chunk):
+    """Small-integer weights (exact in bf16) and states make every product and
+    partial sum an integer below 2^53, so the chunked fp64 readout must equal
+    the int64 matrix product exactly in every row, on both sides of each chunk
+    seam (8192 and 16384 at V = 20011; every 7 rows at V = 50)."""
+    g = np.random.default_rng(11)
+    H = 24
+    Wi = g.integers(-8, 9, size=(V, H))
+    hi = g.integers(-8, 9, size=(3, H))
+    W_bits = (Wi.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    s = O.base_logits(W_bits, hi.astype(np.float32), chunk=chunk)
+    assert s.shape == (3, V)
+    assert np.array_equal(s, (hi @ Wi.T).astype(np.float64))
+
+
 def test_argmax_ties_go_to_lowest_index():
     l = np.array([0.5, 2.0, -1.0, 2.0, 2.0])
     assert O.select_greedy(l)[0] == 1
     assert O.select_greedy(np.array([-0.0, 0.0, -1.0]))[0] == 0
     assert O.select_greedy(np.array([-1.0, 0.0, -0.0]))[0] == 1
+
+
+def test_selection_is_taken_on_the_exact_logits():
+    """Algorithm 1's argmax and the refined distribution are defined on the
+    logits themselves: a gap of 1e-9 at 1.0 (below fp32 resolution, 6e-8)
+    still decides.  Greedy: index 1.  Sampling at u = 0.5 - 1e-10: the first
+    weight e^-1e-9 = 1 - 1e-9 is below u * Z = 1 - 7e-10, so the CDF crosses
+    at index 1 (with the logits rounded to fp32 it would stay at index 0)."""
+    l = np.array([1.0, 1.0 + 1e-9])
+    assert O.select_greedy(l)[0] == 1
+    assert O.select_sample(l, 0.5 - 1e-10)[0] == 1
 
 
 # ------------------------------------------------------------- Fuse stages ----
