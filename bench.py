@@ -4,8 +4,12 @@
 One step = one xp_refine_block (base readout through the target LM head,
 seed selection, K Jacobi passes of the refiner) plus one xp_verify_block over
 a batch of synthetic draft blocks whose inputs are already resident in HBM.
-The default workload is the Qwen3-8B shape at batch 1 (H = 4096, V = 151936,
-r = 256, block 16, greedy, K = 6).
+The default workload is the largest one that fits one GPU: the Qwen3-8B shape
+at batch 64 with blocks of 32 positions, rows alternating greedy and
+temperature-1 sampling (H = 4096, V = 151936, r = 256, K = 6).  The same run
+also measures the batch-1 (block 16, greedy) and batch-32 (block 16, greedy)
+workloads briefly, for the LM-head kernel targets: the stream kernel against
+the HBM peak at batch 1, the GEMM against the bf16 matrix peak at batch 32.
 
 Prints one JSON line.  `value` is refined draft blocks per second; `roofline`
 rates the dominant kernel, the LM-head launch (the stream kernel for one
@@ -92,8 +96,8 @@ def cpu_baseline(wl, weights, inp, min_seconds=10.0, threads=None):
     limit = threadpool_limits(limits=threads) if threads else contextlib.nullcontext()
     with limit:
         used = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        P = O.Params.from_arrays(weights)          # the fp64 widening, before the window
         t0 = time.perf_counter()
-        P = O.Params.from_arrays(weights)
         n = 0
         while True:
             b = n % wl.batch
@@ -113,8 +117,9 @@ def cpu_baseline(wl, weights, inp, min_seconds=10.0, threads=None):
                 break
     return {"value": n / dt, "unit": "blocks/s", "cores": int(used), "kind": "oracle",
             "sample": f"{n} block(s) of {wl.name} (batch rows in turn): fp64 base readout, "
-                      f"{wl.K} Jacobi passes and verification, {dt:.1f} s including the fp64 "
-                      f"weight conversion",
+                      f"{wl.K} Jacobi passes and verification, {dt:.1f} s (the refiner "
+                      f"weights widened to fp64 beforehand; the LM head is widened chunk by "
+                      f"chunk inside the readout, as the oracle does)",
             "cpu_model": _cpu_model()}
 
 
@@ -185,29 +190,141 @@ def read_per_pass(wl, breakdown):
             "frac_hbm_peak": gbs / HBM_PEAK_GBS, "TFLOP_s": flops / (us * 1e-6) / 1e12}
 
 
-def k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout):
+class Setup:
+    """A workload's inputs resident in HBM, its handle, and one step (refine +
+    verify over the batch)."""
+
+    def __init__(self, wl):
+        import torch
+
+        import synth
+        from paper_2608_02438_amd.xpress import device_tensor, refiner_from_arrays
+        self.wl = wl
+        log(f"[bench] workload {wl.name}: generating inputs")
+        self.weights = synth.make_weights(wl)
+        self.inp = inp = synth.make_inputs(wl)
+        log("[bench] uploading and creating the handle")
+        self.ref = refiner_from_arrays(self.weights, wl.H, wl.r, wl.V, wl.B, wl.batch)
+        self.hid = device_tensor(inp.h)
+        self.anchor = device_tensor(inp.anchor)
+        self.seed = device_tensor(inp.seed_ids) if inp.seed_ids is not None else None
+        sample_rows = bool(inp.temp.any())
+        self.temp = device_tensor(inp.temp) if sample_rows else None
+        self.u_draft = device_tensor(inp.u_draft) if sample_rows else None
+        self.tl = device_tensor(inp.target_logits) if sample_rows else None
+        self.r_acc = device_tensor(inp.r_accept)
+        self.u_res = device_tensor(inp.u_res)
+        self.out = self.ref.refine_block(self.hid, self.anchor, seed_ids=self.seed, temp=self.temp,
+                                         u_draft=self.u_draft, K=wl.K)
+        torch.cuda.synchronize()
+        # greedy targets are built around the refined block (fixed by the inputs)
+        self.tids = device_tensor(inp.target_ids(self.out.ids.cpu().numpy()))
+        self.vout = self.ref.verify_block(self.out.ids, self.tids, temp=self.temp,
+                                          target_logits=self.tl, r_accept=self.r_acc,
+                                          u_resample=self.u_res)
+
+    def step(self, K=None, early_exit=False):
+        self.ref.refine_block(self.hid, self.anchor, seed_ids=self.seed, temp=self.temp,
+                              u_draft=self.u_draft, K=self.wl.K if K is None else K,
+                              early_exit=early_exit, out=self.out)
+        self.ref.verify_block(self.out.ids, self.tids, temp=self.temp, target_logits=self.tl,
+                              r_accept=self.r_acc, u_resample=self.u_res, out=self.vout)
+
+    def close(self):
+        self.ref.close()
+
+
+def lm_roofline(wl, lm_us):
+    """Roofline of one LM-head launch of duration lm_us: algorithmic bytes
+    W_lm once, h once, s written once; algorithmic flops 2 M V H.  The launch
+    is HBM-bound below the ridge (peak flops / peak bytes, about 315 flop/B)
+    and MFMA-bound above it."""
+    M = wl.batch * wl.B
+    es = 2 if wl.dtype == "bf16" else 4
+    lm_bytes = wl.V * wl.H * es + M * wl.H * es + M * wl.V * 4
+    lm_flops = 2.0 * M * wl.V * wl.H
+    mfma_bound = wl.dtype == "bf16" and lm_flops / lm_bytes > MFMA_BF16_PEAK_TFS * 1e3 / HBM_PEAK_GBS
+    if mfma_bound:
+        achieved = lm_flops / (lm_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFS,
+                "kernel": "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)",
+                "algorithmic_flops_per_launch": lm_flops}
+    else:
+        achieved = lm_bytes / (lm_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS,
+                "kernel": "k_lmhead_sk (base readout s = W_lm h, stream + selection)"
+                          if M <= 16 else
+                          "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)"}
+    roof.update({"traffic": committed_traffic(wl.name), "algorithmic_bytes_per_launch": lm_bytes,
+                 "launch_us": lm_us})
+    return roof
+
+
+def timed_steps(st, steps):
+    """Time exactly `steps` steps between two synchronizations; the LM-head
+    launch carries an event pair recorded by the library on its stream.
+    Returns (elapsed s, LM-head us per launch, per-round ms per step)."""
+    import torch
+    st.ref.timing_enable(("lmhead",), capacity=max(steps, 1))
+    torch.cuda.synchronize()
+    # up to 5 rounds of equal length inside the timed steps, each bracketed by
+    # events on the stream the steps run on (the mean of the rounds and the
+    # fastest are reported beside the wall-clock figure)
+    nr = min(5, steps)
+    bounds = [steps * i // nr for i in range(nr + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nr + 1)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        if i in bounds:
+            evs[bounds.index(i)].record()
+        st.step()
+    evs[nr].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    rounds = [evs[j].elapsed_time(evs[j + 1]) / (bounds[j + 1] - bounds[j]) for j in range(nr)]
+    tm = st.ref.timing_read()
+    st.ref.timing_enable((), 1)
+    lm_ms, lm_n = tm["lmhead"]
+    return t1 - t0, lm_ms * 1e3 / max(lm_n, 1), rounds
+
+
+def secondary(wl, steps, warmup):
+    """A short measurement of another workload in the same run: blocks/s and
+    its LM-head launch against its own roofline."""
+    st = Setup(wl)
+    for _ in range(warmup):
+        st.step()
+    elapsed, lm_us, rounds = timed_steps(st, steps)
+    st.close()
+    roof = lm_roofline(wl, lm_us)
+    log(f"[bench] {wl.name}: {elapsed * 1e3 / steps:.3f} ms/step, LM head {lm_us:.1f} us "
+        f"({roof['achieved']:.0f} {roof['unit']}, {100 * roof['frac']:.1f}% of peak)")
+    return {"workload": wl.name, "steps": steps, "ms_per_step": elapsed * 1e3 / steps,
+            "blocks_per_s": wl.batch * steps / elapsed, "roofline": roof,
+            "ms_per_step_rounds_min": min(rounds)}
+
+
+def k_sweep(args, st):
     """Cost of K Jacobi passes (the latency-vs-K table of the paper's evaluation):
     ms per refine + verify at fixed K and with the early exit, the mean number of
     passes the early exit runs, and the share of sequences at a fixed point."""
     import numpy as np
     import torch
+    wl = st.wl
     rows = []
     for K in range(1, 9):
         for early in (False, True):
-            def st():
-                ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=K,
-                                 early_exit=early, out=out)
-                ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
-                                 u_resample=u_res, out=vout)
             for _ in range(max(args.warmup, 2)):
-                st()
+                st.step(K, early)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             for _ in range(args.steps):
-                st()
+                st.step(K, early)
             torch.cuda.synchronize()
             dt = (time.perf_counter() - t0) / args.steps
-            it = out.iters.cpu().numpy()
+            it = st.out.iters.cpu().numpy()
             rows.append({"K": K, "early_exit": early, "ms_per_step": dt * 1e3,
                          "blocks_per_s": wl.batch / dt, "iters_mean": float(np.mean(it)),
                          "fixed_point_before_K": float(np.mean(it < K))})
@@ -220,12 +337,14 @@ def k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3-8b-bf16-B16-b1-greedy")
+    ap.add_argument("--workload", default="qwen3-8b-bf16-B32-b64-mixed")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured HBM and MFMA peaks")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the batch-1 and batch-32 LM-head measurements")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES")
     ap.add_argument("--layer", action="store_true",
                     help="time the context layer (the Qwen3-8B decoder layer over the block "
@@ -233,7 +352,7 @@ def main():
                          "instead")
     ap.add_argument("--k-sweep", action="store_true",
                     help="time refine + verify for K = 1..8 passes, fixed K and with the "
-                         "per-batch early exit, and print that table as one JSON line instead")
+                         "early exit, and print that table as one JSON line instead")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -248,103 +367,34 @@ def main():
     import torch
 
     import synth
-    from paper_2608_02438_amd.xpress import device_tensor, refiner_from_arrays
 
     wl = synth.BY_NAME[args.workload]
     if args.layer:
         layer_bench(args, wl)
         return
-    log(f"[bench] workload {wl.name}: generating inputs")
-    weights = synth.make_weights(wl)
-    inp = synth.make_inputs(wl)
-    log("[bench] uploading and creating the handle")
-    ref = refiner_from_arrays(weights, wl.H, wl.r, wl.V, wl.B, wl.batch)
-    hid = device_tensor(inp.h)
-    anchor = device_tensor(inp.anchor)
-    seed = device_tensor(inp.seed_ids) if inp.seed_ids is not None else None
-    sample_rows = bool(inp.temp.any())
-    temp = device_tensor(inp.temp) if sample_rows else None
-    u_draft = device_tensor(inp.u_draft) if sample_rows else None
-    tl = device_tensor(inp.target_logits) if sample_rows else None
-    r_acc = device_tensor(inp.r_accept)
-    u_res = device_tensor(inp.u_res)
-
-    out = ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=wl.K)
-    torch.cuda.synchronize()
-    # greedy targets are built around the refined block (fixed by the inputs)
-    tids = device_tensor(inp.target_ids(out.ids.cpu().numpy()))
-    vout = ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
-                            u_resample=u_res)
-
-    def step():
-        ref.refine_block(hid, anchor, seed_ids=seed, temp=temp, u_draft=u_draft, K=wl.K, out=out)
-        ref.verify_block(out.ids, tids, temp=temp, target_logits=tl, r_accept=r_acc,
-                         u_resample=u_res, out=vout)
-
+    st = Setup(wl)
     if args.k_sweep:
-        k_sweep(args, wl, ref, hid, anchor, seed, temp, u_draft, tids, tl, r_acc, u_res, out, vout)
-        ref.close()
+        k_sweep(args, st)
+        st.close()
         return
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
-        step()
+        st.step()
     torch.cuda.synchronize()
 
     # per-stage breakdown (all stages timed), outside the measured region
-    ref.timing_enable(("prep", "lmhead", "select", "rspace", "read", "verify"), capacity=4096)
+    st.ref.timing_enable(("prep", "lmhead", "select", "rspace", "read", "verify"), capacity=4096)
     for _ in range(3):
-        step()
-    breakdown = ref.timing_read()
+        st.step()
+    breakdown = st.ref.timing_read()
 
-    # the measured region: only the LM-head launch carries an event pair
-    ref.timing_enable(("lmhead",), capacity=max(args.steps, 1))
-    torch.cuda.synchronize()
     log(f"[bench] timing {args.steps} steps")
-    # up to 5 rounds of equal length inside the timed steps, each bracketed by
-    # events on the stream the steps run on (the mean of the rounds and the
-    # fastest are reported beside the wall-clock figure)
-    nr = min(5, args.steps)
-    bounds = [args.steps * i // nr for i in range(nr + 1)]
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(nr + 1)]
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        if i in bounds:
-            evs[bounds.index(i)].record()
-        step()
-    evs[nr].record()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    rounds = [evs[j].elapsed_time(evs[j + 1]) / (bounds[j + 1] - bounds[j]) for j in range(nr)]
-    tm = ref.timing_read()
-    ref.timing_enable((), 1)
-    elapsed = t1 - t0
+    elapsed, lm_us, rounds = timed_steps(st, args.steps)
     ms_step = elapsed * 1e3 / args.steps
     blocks_s = wl.batch * args.steps / elapsed
-    lm_ms, lm_n = tm["lmhead"]
-    lm_us = lm_ms * 1e3 / max(lm_n, 1)
-    M = wl.batch * wl.B
-    es = 2 if wl.dtype == "bf16" else 4
-    # algorithmic bytes of one LM-head launch: W_lm once, h once, s written once;
-    # algorithmic flops 2 M V H.  The launch is HBM-bound below the ridge
-    # (peak flops / peak bytes, about 315 flop/B) and MFMA-bound above it.
-    lm_bytes = wl.V * wl.H * es + M * wl.H * es + M * wl.V * 4
-    lm_flops = 2.0 * M * wl.V * wl.H
-    mfma_bound = wl.dtype == "bf16" and lm_flops / lm_bytes > MFMA_BF16_PEAK_TFS * 1e3 / HBM_PEAK_GBS
-    if mfma_bound:
-        achieved = lm_flops / (lm_us * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFS,
-                "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFS,
-                "kernel": "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)",
-                "algorithmic_flops_per_launch": lm_flops}
-    else:
-        achieved = lm_bytes / (lm_us * 1e-6) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS,
-                "kernel": "k_lmhead (base readout s = W_lm h)" if M <= 16 else
-                          "k_lmhead_gemm (base readout s = W_lm h, GEMM + selection)"}
-    roof.update({"traffic": committed_traffic(wl.name), "algorithmic_bytes_per_launch": lm_bytes,
-                 "launch_us": lm_us})
+    roof = lm_roofline(wl, lm_us)
+    achieved = roof["achieved"]
     if not args.no_peaks:
         from paper_2608_02438_amd.xpress import probe_hbm_read, probe_mfma_bf16
         log("[bench] measured peaks (HBM read stream, MFMA loop)")
@@ -352,9 +402,10 @@ def main():
         peak = mp["mfma_bf16_TFs"] if roof["bound"] == "mfma" else mp["hbm_read_GBs"]
         roof.update({"measured_peak": peak, "frac_of_measured": achieved / peak,
                      "measured_peaks": mp})
-    n_acc = vout[0].cpu().numpy()
+    n_acc = st.vout[0].cpu().numpy()
     log(f"[bench] {ms_step:.3f} ms/step, LM head {lm_us:.1f} us "
         f"({achieved:.0f} {roof['unit']}, {100 * roof['frac']:.1f}% of peak)")
+    st.close()
 
     line = {
         "metric": METRIC, "value": blocks_s, "unit": "blocks/s", "n_gpus": 1,
@@ -367,7 +418,7 @@ def main():
                    "H": wl.H, "V": wl.V, "r": wl.r, "temperature": wl.temp},
         "roofline": roof,
         "refined_tokens_per_s": blocks_s * wl.B,
-        "stage_ms_per_step": {k: v[0] / max(1, 3) for k, v in breakdown.items()},
+        "stage_ms_per_step": {k: v[0] / 3 for k, v in breakdown.items()},
         "read_per_pass": read_per_pass(wl, breakdown),
         "rounds_ms_per_step": rounds,
         "ms_per_step_rounds_mean": sum(rounds) / len(rounds),
@@ -378,14 +429,23 @@ def main():
         # synthetic targets fix the acceptance
         "committed_tokens_per_s": float(np.sum(n_acc + 1)) * args.steps / elapsed,
     }
+    if not args.no_secondary and args.workload == "qwen3-8b-bf16-B32-b64-mixed":
+        # the two kernel targets: the LM-head stream at batch 1 against HBM,
+        # the LM-head GEMM at batch 32 against the bf16 matrix peak
+        sec = {}
+        for name in ("qwen3-8b-bf16-B16-b1-greedy", "qwen3-8b-bf16-B16-b32-greedy"):
+            sec[name] = secondary(synth.BY_NAME[name], 20, 5)
+        line["secondary"] = sec
+        line["lmhead_hbm_frac_batch1"] = sec["qwen3-8b-bf16-B16-b1-greedy"]["roofline"]["frac"]
+        line["lmhead_mfma_frac_batch32"] = sec["qwen3-8b-bf16-B16-b32-greedy"]["roofline"]["frac"]
     if not args.no_cpu:
         log("[bench] CPU oracle baseline (all threads)")
-        line["cpu_baseline"] = cpu_baseline(wl, weights, inp)
+        line["cpu_baseline"] = cpu_baseline(wl, st.weights, st.inp)
         log("[bench] CPU oracle baseline (one thread)")
-        line["cpu_baseline_1thread"] = cpu_baseline(wl, weights, inp, min_seconds=0.0, threads=1)
+        line["cpu_baseline_1thread"] = cpu_baseline(wl, st.weights, st.inp, min_seconds=0.0,
+                                                    threads=1)
     else:
         line["cpu_baseline"] = None
-    ref.close()
     print(json.dumps(line), flush=True)
 
 

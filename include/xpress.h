@@ -70,8 +70,10 @@ typedef struct xp_handle xp_handle;
  *   L    [r][B][B] per-channel mixer; entry [d][k][i] is read only for i < k
  *   W_1  [2r][r], W_2 [r][2r]   r-space MLP of eq. mlp
  *   W_r  [V][r]   readout head
- * r must be 256 (the paper's rank); H a multiple of 256 up to 8192; 1 <= B <= 32;
- * 16 <= V < 2^31.
+ * Built: r = 256 (the paper's rank); H a multiple of 256, up to 8192 for bf16
+ * and up to 4096 for fp32; 1 <= B <= 32; 16 <= V <= 262144 (the temperature
+ * sampler scans at most 4096 vocabulary units of at most 8 tiles of 16 rows
+ * on 256 CUs).  xp_create returns XP_EUNSUPPORTED outside these.
  */
 typedef struct {
   int32_t H, r, V, B;
@@ -259,12 +261,16 @@ typedef struct {
 typedef struct xp_layer xp_layer;
 
 /*
- * Create a layer for up to max_batch blocks of up to max_B (<= 32) positions
- * and contexts of up to max_ctx keys on the current device; allocates its
- * workspace (freed by xp_layer_destroy).  The weights are referenced, not
- * copied: they must stay valid while the layer is used.
+ * Create a layer for up to max_batch (<= 4096) blocks of up to max_B (<= 32)
+ * positions and contexts of up to max_ctx (<= 2^20) keys on the current
+ * device; allocates its workspace (freed by xp_layer_destroy).  Any later call
+ * with batch <= max_batch and B <= max_B is served by that workspace.  The
+ * weights are referenced, not copied: they must stay valid while the layer is
+ * used.
  * Errors: XP_EINVAL (null or misaligned pointers, sizes), XP_EUNSUPPORTED
- * (shapes outside the built set), XP_ENOMEM, XP_EHIP.  *out is NULL on error.
+ * (shapes outside the built set, or max_batch * max_B * max(H, n_heads*128,
+ * ffn) >= 2^31), XP_ENOMEM, XP_EHIP.  *out is NULL on error;
+ * xp_layer_last_error(NULL) names the problem.
  */
 xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
                           int32_t max_ctx, xp_layer** out);
@@ -286,7 +292,8 @@ xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t 
  * Every pointer 16-byte aligned.
  * Errors: XP_EINVAL (null handle or input, a misaligned pointer, batch, B or
  * C_max outside what the layer was created for), before any launch; XP_EHIP
- * if a launch fails.
+ * if a launch fails (kernels already enqueued stay enqueued; h is then
+ * unspecified).  xp_layer_last_error(L) names the problem.
  */
 xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal, const void* x,
                            const void* k_cache, const void* v_cache, int32_t C_max,
@@ -294,6 +301,10 @@ xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal
 
 /* Free the layer and its workspace (waits for the device first).  NULL is a no-op. */
 void xp_layer_destroy(xp_layer* L);
+
+/* Message for the last failed call on `L` (of the last failed
+ * xp_layer_create on this thread when L is NULL); "" if none failed. */
+const char* xp_layer_last_error(const xp_layer* L);
 
 /*
  * Measurement probes (not part of the method).  They give the measured peaks

@@ -26,19 +26,41 @@ def sources():
     return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libxpress.so; returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), *sources(), "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _run(cmd):
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = (r.stdout + r.stderr).strip()
-    lines = [l for l in out.splitlines() if "packed-fp32-ops" not in l]
-    if r.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(lines))
-    if verbose and lines:
-        print("\n".join(lines))
+    return r.returncode, [l for l in out.splitlines() if "packed-fp32-ops" not in l]
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every HIP source (one hipcc process per file, in parallel) and
+    link them into libxpress.so; returns its path."""
+    from concurrent.futures import ThreadPoolExecutor
+    objdir = os.path.join(ROOT, "_build", "obj")
+    os.makedirs(objdir, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include")]
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    jobs = []
+    for src in sources():
+        obj = os.path.join(objdir, os.path.basename(src) + ".o")
+        jobs.append((src, obj, [HIPCC, *compile_flags, *inc, "-c", src, "-o", obj]))
+    if verbose:
+        for _, _, cmd in jobs:
+            print(" ".join(cmd), flush=True)
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        results = list(ex.map(lambda j: _run(j[2]), jobs))
+    errs = [(j[0], lines) for j, (rc, lines) in zip(jobs, results) if rc != 0]
+    if errs:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(
+            f"{src}:\n" + "\n".join(lines) for src, lines in errs))
+    if verbose:
+        for (src, _, _), (_, lines) in zip(jobs, results):
+            if lines:
+                print("\n".join(lines))
+    tmp = LIB + ".tmp"
+    rc, lines = _run([HIPCC, *FLAGS, *[j[1] for j in jobs], "-o", tmp])
+    if rc != 0:
+        raise RuntimeError("link failed:\n" + "\n".join(lines))
     os.replace(tmp, LIB)
     return LIB
 

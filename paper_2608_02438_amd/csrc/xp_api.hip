@@ -71,6 +71,7 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
     return fail(nullptr, XP_EINVAL, "sizes must be positive (H=%d r=%d V=%d B=%d)", w->H, w->r,
                 w->V, w->B);
   if (w->r != 256) return fail(nullptr, XP_EUNSUPPORTED, "r=%d: only r=256 is built", w->r);
+  if (w->V < 16) return fail(nullptr, XP_EUNSUPPORTED, "V=%d: vocabularies below 16 are not built", w->V);
   if (w->B > 32) return fail(nullptr, XP_EUNSUPPORTED, "B=%d: blocks up to 32 are built", w->B);
   if (w->H % 256 != 0 || !lm_split_ok(w->H, w->dtype) ||
       (w->dtype == XP_F32 ? w->H > 4096 : w->H > 8192))

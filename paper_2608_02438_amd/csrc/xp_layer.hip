@@ -24,6 +24,11 @@
 //                 next one loads; S = K Q^T and O = P V on the matrix cores
 //   k_attn_comb   merges the chunks of every query row in chunk order
 // Every reduction runs in a fixed order, so two runs give identical bits.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+
 #include "xp_internal.h"
 
 namespace xp {
@@ -737,32 +742,70 @@ struct xp_layer {
   float *opart = nullptr, *mlpart = nullptr;
   uint16_t* attn = nullptr;
   float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;
+  size_t gu_rows = 0;                // positions the gate/up buffer GU holds
   uint16_t* act = nullptr;
+  std::string err;                   // message of the last failed call
 };
+
+static thread_local std::string g_layer_create_err;
+
+static xp_status layer_fail(xp_layer* L, xp_status s, const char* fmt, ...)
+    __attribute__((format(printf, 3, 4)));
+static xp_status layer_fail(xp_layer* L, xp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  (L ? L->err : g_layer_create_err) = buf;
+  return s;
+}
+
+extern "C" const char* xp_layer_last_error(const xp_layer* L) {
+  return L ? L->err.c_str() : g_layer_create_err.c_str();
+}
 
 static int attn_chunks(int C_max, int B, int keys) { return (C_max + B + keys - 1) / keys; }
 
 extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
                                      int32_t max_ctx, xp_layer** out) {
-  if (out == nullptr) return XP_EINVAL;
+  g_layer_create_err.clear();
+  if (out == nullptr) return layer_fail(nullptr, XP_EINVAL, "out is NULL");
   *out = nullptr;
-  if (w == nullptr || max_batch < 1 || max_batch > 4096 || max_B < 1 || max_B > 32 ||
-      max_ctx < 0 || max_ctx > (1 << 20))
-    return XP_EINVAL;
+  if (w == nullptr) return layer_fail(nullptr, XP_EINVAL, "weights is NULL");
+  if (max_batch < 1 || max_batch > 4096 || max_B < 1 || max_B > 32 || max_ctx < 0 ||
+      max_ctx > (1 << 20))
+    return layer_fail(nullptr, XP_EINVAL,
+                      "max_batch=%d (1..4096), max_B=%d (1..32) or max_ctx=%d (0..2^20) out of range",
+                      max_batch, max_B, max_ctx);
   const void* ptrs[] = {w->g_attn, w->Wq, w->Wk, w->Wv, w->g_q, w->g_k,
                         w->Wo,     w->g_mlp, w->Wg, w->Wu, w->Wd};
-  for (const void* p : ptrs)
-    if (p == nullptr || reinterpret_cast<uintptr_t>(p) % 16 != 0) return XP_EINVAL;
+  const char* names[] = {"g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp", "Wg", "Wu", "Wd"};
+  for (int i = 0; i < 11; ++i)
+    if (ptrs[i] == nullptr || reinterpret_cast<uintptr_t>(ptrs[i]) % 16 != 0)
+      return layer_fail(nullptr, XP_EINVAL, "weight %s is NULL or not 16-byte aligned", names[i]);
   if (w->H < 1 || w->n_heads < 1 || w->n_kv < 1 || w->ffn < 1 || w->head_dim < 1 ||
       !(w->eps >= 0.f) || !(w->rope_theta > 0.f))
-    return XP_EINVAL;
+    return layer_fail(nullptr, XP_EINVAL,
+                      "sizes must be positive, eps >= 0 and rope_theta > 0 (H=%d heads=%d kv=%d "
+                      "head_dim=%d ffn=%d)", w->H, w->n_heads, w->n_kv, w->head_dim, w->ffn);
   const int grp = w->n_heads / w->n_kv;
   if (w->head_dim != kHd || w->n_heads % w->n_kv != 0 ||
       (grp != 1 && grp != 2 && grp != 4 && grp != 8) || w->H % 256 != 0 || w->H > 8192 ||
       (w->n_heads * kHd) % 256 != 0 || w->ffn % 256 != 0 || w->ffn > (1 << 16))
-    return XP_EUNSUPPORTED;
+    return layer_fail(nullptr, XP_EUNSUPPORTED,
+                      "shape not built: head_dim %d (128), heads/kv %d/%d (group 1, 2, 4 or 8), "
+                      "H %d and heads*128 multiples of 256 with H <= 8192, ffn %d a multiple of 256 "
+                      "up to 65536", w->head_dim, w->n_heads, w->n_kv, w->H, w->ffn);
+  // every projection addresses rows of its input as (position * K) in 32 bits
+  const int64_t widest = std::max<int64_t>({(int64_t)w->H, (int64_t)w->n_heads * kHd,
+                                            (int64_t)w->ffn});
+  if ((int64_t)max_batch * max_B * widest >= ((int64_t)1 << 31))
+    return layer_fail(nullptr, XP_EUNSUPPORTED,
+                      "max_batch*max_B*max(H, heads*128, ffn) = %lld reaches 2^31",
+                      (long long)max_batch * max_B * widest);
   xp_layer* L = new (std::nothrow) xp_layer();
-  if (L == nullptr) return XP_ENOMEM;
+  if (L == nullptr) return layer_fail(nullptr, XP_ENOMEM, "host allocation failed");
   L->H = w->H;
   L->nh = w->n_heads;
   L->nkv = w->n_kv;
@@ -793,6 +836,15 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   const size_t nparts =
       (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + zmax * L->nkv) * grp;
   L->nparts = nparts;
+  // The gate/up projections write fp32 [M][2 F] to GU on two paths: the
+  // stream kernel (calls of at most one 16-position block, H within its LDS
+  // copy of x) and the tiled GEMM (calls above kLinMaxStream positions).  Any
+  // call up to the created maxima may take either, so GU holds the largest M
+  // of the two.
+  size_t gu = 0;
+  if (H <= 8 * (size_t)kGsXChunks) gu = std::min(Mx, (size_t)kTile);
+  if (Mx > (size_t)kLinMaxStream) gu = Mx;
+  L->gu_rows = gu;
   struct Slice {
     void** p;
     size_t bytes;
@@ -803,13 +855,16 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
       {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
       {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
       {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
-      {(void**)&L->GU, (Mx > kLinMaxStream || max_B <= kTile ? Mx : 0) * 2 * F * 4},
+      {(void**)&L->GU, (gu ? gu : 1) * 2 * F * 4},
   };
   size_t total = 0;
   for (auto& s : sl) total += (s.bytes + 255) / 256 * 256;
-  if (hipMalloc(&L->ws, total) != hipSuccess) {
+  const hipError_t e = hipMalloc(&L->ws, total);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
     delete L;
-    return XP_ENOMEM;
+    return layer_fail(nullptr, XP_ENOMEM, "workspace of %zu bytes: %s", total,
+                      hipGetErrorString(e));
   }
   char* p = static_cast<char*>(L->ws);
   for (auto& s : sl) {
@@ -828,11 +883,13 @@ extern "C" void xp_layer_destroy(xp_layer* L) {
 }
 
 // y [M][N] (row stride ldy) = X [M][K] W^T (+ R), W the rows of W0 | W1 | W2
-// stacked (n0, n1 rows of the first two); glu: bf16(silu(X W0^T) * (X W1^T)).
-// P = 1, 2 or 4 position blocks per pass of the weight.
-static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0, int n1,
-                   int N, int K, const uint16_t* X, int M, const float* R, int ldr, float* Y,
-                   uint16_t* Yb, int ldy, bool glu, hipStream_t st, float* GU = nullptr) {
+// stacked (n0, n1 rows of the first two); glu: bf16(silu(X W0^T) * (X W1^T)),
+// through GU (fp32 [M][2 N], gu_rows positions).  Returns the first failed
+// launch's error; hipErrorInvalidValue if GU is too small for the path taken.
+static hipError_t linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
+                         int n1, int N, int K, const uint16_t* X, int M, const float* R, int ldr,
+                         float* Y, uint16_t* Yb, int ldy, bool glu, hipStream_t st,
+                         float* GU = nullptr, size_t gu_rows = 0) {
   // one block of positions and x small enough for LDS: the stream-K kernel
   // (gate and up side by side, then SwiGLU)
   if (M <= kTile && K <= 8 * kGsXChunks && K % 64 == 0 && N % kTile == 0 && n0 % kTile == 0 &&
@@ -840,9 +897,12 @@ static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, i
     const int rows = glu ? 2 * N : N, ntl = rows / kTile;
     const int U = ntl < 256 ? ntl : 256;
     if (glu) {
+      if ((size_t)M > gu_rows) return hipErrorInvalidValue;
       hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W1, N, N,
                          2 * N, K, X, M, U, (const float*)nullptr, 0, GU, (uint16_t*)nullptr,
                          2 * N);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
       const size_t na = (size_t)M * N;
       hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
                          na, Yb);
@@ -850,20 +910,22 @@ static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, i
       hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W2, n0, n1,
                          N, K, X, M, U, R, ldr, Y, Yb, ldy);
     }
-    return;
+    return hipGetLastError();
   }
   // above one 64-position pass of the stream: the tiled GEMM (weights read
   // once per 128 or 256 positions); gate and up side by side, then SwiGLU
   if (M > kLinMaxStream && (glu ? layer_gemm_ok(N, N, 2 * N, K, M) : layer_gemm_ok(n0, n1, N, K, M))) {
     if (glu) {
-      launch_layer_gemm(W0, W1, W1, N, N, 2 * N, K, X, M, nullptr, 0, GU, nullptr, 2 * N, st);
+      if ((size_t)M > gu_rows) return hipErrorInvalidValue;
+      hipError_t e = launch_layer_gemm(W0, W1, W1, N, N, 2 * N, K, X, M, nullptr, 0, GU, nullptr,
+                                       2 * N, st);
+      if (e != hipSuccess) return e;
       const size_t na = (size_t)M * N;
       hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
                          na, Yb);
-    } else {
-      launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
+      return hipGetLastError();
     }
-    return;
+    return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
   }
   const int nb = (M + kTile - 1) / kTile;
   const int P = nb >= 4 ? 4 : (nb >= 2 ? 2 : 1);
@@ -886,18 +948,28 @@ static void linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, i
     else XP_LIN(1, 0);
   }
 #undef XP_LIN
+  return hipGetLastError();
 }
 
 extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal,
                                       const void* x, const void* k_cache, const void* v_cache,
                                       int32_t C_max, const int32_t* ctx_len, float* h_f32,
                                       void* h_bf16, void* stream) {
-  if (L == nullptr || x == nullptr || k_cache == nullptr || v_cache == nullptr ||
-      ctx_len == nullptr || batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B ||
-      C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1) || (causal != 0 && causal != 1))
-    return XP_EINVAL;
-  for (const void* q : {x, k_cache, v_cache, (const void*)h_f32, (const void*)h_bf16})
-    if (reinterpret_cast<uintptr_t>(q) % 16 != 0) return XP_EINVAL;
+  if (L == nullptr) return XP_EINVAL;
+  if (x == nullptr || k_cache == nullptr || v_cache == nullptr || ctx_len == nullptr)
+    return layer_fail(L, XP_EINVAL, "x, k_cache, v_cache and ctx_len are required");
+  if (batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B)
+    return layer_fail(L, XP_EINVAL, "batch=%d (1..%d) or B=%d (1..%d) outside the created maxima",
+                      batch, L->max_batch, B, L->max_B);
+  if (C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1))
+    return layer_fail(L, XP_EINVAL, "C_max=%d out of range 1..%d", C_max,
+                      L->max_ctx > 0 ? L->max_ctx : 1);
+  if (causal != 0 && causal != 1) return layer_fail(L, XP_EINVAL, "causal=%d is not 0 or 1", causal);
+  const char* pn[] = {"x", "k_cache", "v_cache", "h_f32", "h_bf16"};
+  const void* pv[] = {x, k_cache, v_cache, (const void*)h_f32, (const void*)h_bf16};
+  for (int i = 0; i < 5; ++i)
+    if (reinterpret_cast<uintptr_t>(pv[i]) % 16 != 0)
+      return layer_fail(L, XP_EINVAL, "%s is not 16-byte aligned", pn[i]);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
@@ -908,35 +980,55 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
   int nsub = (int)(w64 / kAttnWgs);
   nsub = nsub < 1 ? 1 : (nsub > 256 ? 256 : nsub);
   const int ns = attn_chunks(C_max, B, kSub * nsub);
-  if ((size_t)batch * npb * nkv * ns * grp > L->nparts) return XP_EINVAL;   // not reached
+  if ((size_t)batch * npb * nkv * ns * grp > L->nparts)
+    return layer_fail(L, XP_EINVAL, "attention partials exceed the workspace");   // not reached
   float* hout = h_f32 ? h_f32 : L->h32;
+  hipError_t e;
+#define XP_STEP(what, call)                                                                  \
+  do {                                                                                       \
+    call;                                                                                    \
+    if ((e = hipGetLastError()) != hipSuccess)                                               \
+      return layer_fail(L, XP_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));     \
+  } while (0)
+#define XP_LINEAR(what, ...)                                                                 \
+  do {                                                                                       \
+    if ((e = linear(__VA_ARGS__)) != hipSuccess)                                             \
+      return layer_fail(L, e == hipErrorInvalidValue ? XP_EINVAL : XP_EHIP,                  \
+                        "%s projection failed: %s", what, hipGetErrorString(e));             \
+  } while (0)
 
-  hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st, (const uint16_t*)x, H,
-                     L->g_attn, L->eps, L->x32, L->u);
-  linear(L->Wq, L->Wk, L->Wv, nhd, kvd, ldq, H, L->u, M, nullptr, 0, L->qkv, nullptr, ldq, false,
-         st);
+  XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st,
+                                        (const uint16_t*)x, H, L->g_attn, L->eps, L->x32, L->u));
+  XP_LINEAR("q/k/v", L->Wq, L->Wk, L->Wv, nhd, kvd, ldq, H, L->u, M, nullptr, 0, L->qkv, nullptr,
+            ldq, false, st);
   const int qk_waves = M * (nh + 2 * nkv);
-  hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M, B, nh,
-                     nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn, L->kb, L->vb);
+  XP_STEP("qk-norm/rope",
+          hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M,
+                             B, nh, nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn,
+                             L->kb, L->vb));
 #define XP_ATTN(GG)                                                                           \
   hipLaunchKernelGGL(k_attn<GG>, dim3(ns, nkv, batch * npb), dim3(GG * kWave), 0, st, L->qn, \
                      (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb, ctx_len, \
                      C_max, B, npb, nh, nkv, causal, ns, nsub, L->opart, L->mlpart)
-  if (grp == 1) XP_ATTN(1);
-  else if (grp == 2) XP_ATTN(2);
-  else if (grp == 4) XP_ATTN(4);
-  else XP_ATTN(8);
+  if (grp == 1) XP_STEP("attention", XP_ATTN(1));
+  else if (grp == 2) XP_STEP("attention", XP_ATTN(2));
+  else if (grp == 4) XP_STEP("attention", XP_ATTN(4));
+  else XP_STEP("attention", XP_ATTN(8));
 #undef XP_ATTN
   const int cw = M * nh;
-  hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart, L->mlpart, M, B,
-                     npb, nh, nkv, grp, ns, L->attn);
-  linear(L->Wo, nullptr, nullptr, H, 0, H, nhd, L->attn, M, L->x32, H, L->x1, nullptr, H, false,
-         st);
-  hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st, (const float*)L->x1, H,
-                     L->g_mlp, L->eps, (float*)nullptr, L->u);
-  linear(L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F, true, st,
-         L->GU);
-  linear(L->Wd, nullptr, nullptr, H, 0, H, F, L->act, M, L->x1, H, hout, (uint16_t*)h_bf16, H,
-         false, st);
-  return hipGetLastError() == hipSuccess ? XP_OK : XP_EHIP;
+  XP_STEP("attention combine",
+          hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart,
+                             L->mlpart, M, B, npb, nh, nkv, grp, ns, L->attn));
+  XP_LINEAR("output", L->Wo, nullptr, nullptr, H, 0, H, nhd, L->attn, M, L->x32, H, L->x1,
+            nullptr, H, false, st);
+  XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st,
+                                        (const float*)L->x1, H, L->g_mlp, L->eps, (float*)nullptr,
+                                        L->u));
+  XP_LINEAR("gate/up", L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F,
+            true, st, L->GU, L->gu_rows);
+  XP_LINEAR("down", L->Wd, nullptr, nullptr, H, 0, H, F, L->act, M, L->x1, H, hout,
+            (uint16_t*)h_bf16, H, false, st);
+#undef XP_STEP
+#undef XP_LINEAR
+  return XP_OK;
 }

@@ -296,7 +296,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   Stat st[P];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
-    bv[pb] = act[pb] & !sample[pb] ? -INFINITY : INFINITY;
+    bv[pb] = (act[pb] && !sample[pb]) ? -INFINITY : INFINITY;
     bi[pb] = 0xFFFFFFFFu;
     st[pb] = stat_empty();
   }

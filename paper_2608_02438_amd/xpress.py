@@ -24,7 +24,7 @@ XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE = 1, 2
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
            "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16", "xp_toeplitz_mixer",
-           "xp_layer_create", "xp_layer_forward", "xp_layer_destroy")
+           "xp_layer_create", "xp_layer_forward", "xp_layer_destroy", "xp_layer_last_error")
 LAYER_WEIGHT_NAMES = ("g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp", "Wg", "Wu", "Wd")
 STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
 
@@ -92,6 +92,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_layer_forward.restype = i32
     L.xp_layer_destroy.argtypes = [vp]
     L.xp_layer_destroy.restype = None
+    L.xp_layer_last_error.argtypes = [vp]
+    L.xp_layer_last_error.restype = ctypes.c_char_p
     _lib = L
     return L
 
@@ -310,8 +312,9 @@ class Layer:
         for n in LAYER_WEIGHT_NAMES:
             setattr(w, n, _ptr(weights[n]))
         h = ctypes.c_void_p(0)
-        _check(L.xp_layer_create(ctypes.byref(w), max_batch, max_B, max_ctx, ctypes.byref(h)),
-               "xp_layer_create")
+        st = L.xp_layer_create(ctypes.byref(w), max_batch, max_B, max_ctx, ctypes.byref(h))
+        if st != XP_OK:
+            raise XpError(st, "xp_layer_create: " + L.xp_layer_last_error(None).decode())
         self._h = h
         self.H = H
 
@@ -329,9 +332,11 @@ class Layer:
             h_bf16 = torch.empty((batch, B, H), dtype=torch.bfloat16, device=x.device)
         for t in (x, k_cache, v_cache, ctx_len, h_f32, h_bf16):
             assert t.is_contiguous()
-        _check(L.xp_layer_forward(self._h, batch, B, 1 if causal else 0, _ptr(x), _ptr(k_cache),
-                                  _ptr(v_cache), C_max, _ptr(ctx_len), _ptr(h_f32), _ptr(h_bf16),
-                                  _stream(stream)), "xp_layer_forward")
+        st = L.xp_layer_forward(self._h, batch, B, 1 if causal else 0, _ptr(x), _ptr(k_cache),
+                                _ptr(v_cache), C_max, _ptr(ctx_len), _ptr(h_f32), _ptr(h_bf16),
+                                _stream(stream))
+        if st != XP_OK:
+            raise XpError(st, "xp_layer_forward: " + L.xp_layer_last_error(self._h).decode())
         return h_f32, h_bf16
 
     def close(self):

@@ -226,8 +226,13 @@ def _decision_ok(l, E, y_dev, sample, u, T=1.0):
     return "excused" if ok else "wrong"
 
 
-def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits, T=1.0):
-    """Validate one sequence's device trajectory; returns (Tally, final logits, final E)."""
+def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits, T=1.0,
+                   abs_bar=None):
+    """Validate one sequence's device trajectory; returns (Tally, final logits, final E).
+
+    The final logits must lie within E of the oracle's element by element and,
+    when ``abs_bar`` is given, within that absolute bar as well (the workloads'
+    tolerance: 1e-5 for fp32, 2e-2 for bf16)."""
     B = s_b.shape[0]
     t = Tally(seqs=1)
     ref = O.refine_block(P, s_b, h_b, anchor, seed=seed, sample=sample, u=u, K=K,
@@ -264,11 +269,15 @@ def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits,
         assert (err <= E_final).all(), (
             f"logit error {t.max_logit_err} exceeds its bound at "
             f"{np.unravel_index(np.argmax(err / E_final), err.shape)}")
+        if abs_bar is not None:
+            assert t.max_logit_err <= abs_bar, (
+                f"logit error {t.max_logit_err} exceeds the absolute bar {abs_bar}")
     return t, l_final, E_final
 
 
-def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None):
-    """Check the chosen sequences of a device run; returns (Tally, final logits per seq)."""
+def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None, abs_bar=None):
+    """Check the chosen sequences of a device run; returns (Tally, final logits per seq).
+    ``s`` (optional) holds the oracle's base logits of those sequences, in order."""
     P = P or O.Params.from_arrays(prob.weights, round_z=prob.dtype == "bf16")
     seqs = list(range(prob.batch)) if seqs is None else list(seqs)
     i = prob.inp
@@ -281,7 +290,7 @@ def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None):
         t, lf, Ef = check_sequence(P, s[n], i.h[b], int(i.anchor[b]), seed, bool(i.temp[b]),
                                    i.u_draft[b], run.traj.shape[0] - 1, run.traj[:, b],
                                    run.iters[b], None if run.logits is None else run.logits[b],
-                                   prob.T(b))
+                                   prob.T(b), abs_bar=abs_bar)
         tot.add(t)
         finals[b] = (lf, Ef)
     return tot, finals

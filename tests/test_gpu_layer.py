@@ -44,13 +44,13 @@ def _case(H, nh, nkv, ffn, B, batch, ctx, index, c_max=None):
     return w, weights, inp
 
 
-def _run(w, weights, inp, causal=True, max_ctx=None, layer=None):
+def _run(w, weights, inp, causal=True, max_ctx=None, layer=None, max_batch=None, max_B=None):
     import torch
     from paper_2608_02438_amd.xpress import LAYER_WEIGHT_NAMES, Layer, device_tensor
     dw = {n: device_tensor(weights[n]) for n in LAYER_WEIGHT_NAMES}
     if layer is None:
-        layer = Layer(dw, w.H, w.n_heads, w.n_kv_heads, w.ffn, max_batch=w.batch, max_B=w.B,
-                      max_ctx=max_ctx or inp.k_cache.shape[1])
+        layer = Layer(dw, w.H, w.n_heads, w.n_kv_heads, w.ffn, max_batch=max_batch or w.batch,
+                      max_B=max_B or w.B, max_ctx=max_ctx or inp.k_cache.shape[1])
     dev = [device_tensor(a) for a in (inp.x, inp.k_cache, inp.v_cache, inp.ctx_len)]
     h32, hb = layer.forward(*dev, causal=causal)
     torch.cuda.synchronize()
@@ -58,10 +58,15 @@ def _run(w, weights, inp, causal=True, max_ctx=None, layer=None):
     return h32.cpu().numpy(), hb_bits, layer, dw
 
 
-def _check(w, weights, inp, h32, hb_bits, causal=True):
+def _check(w, weights, inp, h32, hb_bits, causal=True, seqs=None):
+    """h of the chosen sequences (default all) against the oracle run on just
+    those sequences (each sequence's layer output depends only on its own
+    inputs and context)."""
     P = O.layer_ref.LayerParams.from_arrays(weights, w.n_heads, w.n_kv_heads, w.head_dim)
-    ref = O.layer_ref.layer_forward(P, inp.x, inp.k_cache, inp.v_cache, inp.ctx_len, causal)
-    err = np.abs(h32 - ref)
+    sl = slice(None) if seqs is None else list(seqs)
+    ref = O.layer_ref.layer_forward(P, inp.x[sl], inp.k_cache[sl], inp.v_cache[sl],
+                                    inp.ctx_len[sl], causal)
+    err = np.abs(h32[sl] - ref)
     _say(f"  max|h|={np.abs(ref).max():.3g} max|dh|={err.max():.3g} mean|dh|={err.mean():.3g}")
     assert np.all(np.isfinite(h32))
     assert err.max() <= ATOL
@@ -167,4 +172,46 @@ def test_layer_qwen3_shape_batch1_ctx2048():
     w, weights, inp = _case(4096, 32, 8, 12288, 16, 1, [2048], index=901)
     h32, hb, layer, _ = _run(w, weights, inp)
     _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
+@pytest.mark.parametrize("max_batch,max_B,batch,B", [(2, 32, 1, 16), (2, 32, 2, 8),
+                                                     (8, 16, 1, 16), (8, 16, 3, 16)])
+def test_layer_called_below_its_created_maxima(max_batch, max_B, batch, B):
+    """A layer serves any call up to the sizes it was created for, whichever
+    projection path that call takes: created for 64 or 128 positions and
+    called with one block of 16 (the stream kernel, gate and up through the
+    fp32 gate/up buffer), two blocks of 8, or 48 positions (the k-split
+    kernel)."""
+    ctx = [(97 * i + 40) % 500 for i in range(batch)]
+    _say(f"case: layer created max_batch={max_batch} max_B={max_B}, called batch={batch} B={B} "
+         f"ctx={ctx}")
+    w, weights, inp = _case(512, 8, 2, 768, B, batch, ctx, index=950 + 10 * max_B + batch)
+    h32, hb, layer, _ = _run(w, weights, inp, max_batch=max_batch, max_B=max_B, max_ctx=512)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
+# The Qwen3-8B layer at the shapes of the three larger workloads (batch 8 with
+# 4096 context keys, batch 32 with 8192, batch 64 of 32 positions with ragged
+# contexts U{512..16384}); the device runs the whole batch, and the oracle
+# checks a few sequences of it (the longest and the shortest context among them).
+@pytest.mark.parametrize("batch,B,ctx_len,ctx_range,seqs", [
+    (8, 16, 4096, None, [0, 7]),
+    (32, 16, 8192, None, [0, 13, 31]),
+    (64, 32, None, (512, 16384), None),
+])
+def test_layer_qwen3_shape_at_workload_sizes(batch, B, ctx_len, ctx_range, seqs):
+    w = synth.scaled(QWEN_B1, index=905 + batch, B=B, batch=batch, ctx_len=ctx_len,
+                     ctx_len_range=ctx_range)
+    weights = synth.make_layer_weights(w)
+    inp = synth.make_layer_inputs(w)
+    if seqs is None:
+        order = np.argsort(inp.ctx_len)
+        seqs = sorted({int(order[0]), int(order[-1]), 5, 40})
+    _say(f"case: layer Qwen3-8B shape batch={batch} B={B} ctx max {int(inp.ctx_len.max())} "
+         f"min {int(inp.ctx_len.min())}; oracle checks sequences {seqs} "
+         f"(ctx {[int(inp.ctx_len[q]) for q in seqs]})")
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb, seqs=seqs)
     layer.close()

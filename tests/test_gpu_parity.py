@@ -11,7 +11,7 @@ import oracle as O
 import synth
 from synth.configs import TINY_F32, QWEN_B1, QWEN_B8_T1, QWEN_B32, QWEN_B64_MIXED
 
-from _parity import (check_refine, check_verify, custom_problem, make_refiner,
+from _parity import (Tally, check_refine, check_verify, custom_problem, make_refiner,
                      run_device, upload, workload_problem)
 
 pytestmark = pytest.mark.gpu
@@ -46,22 +46,6 @@ def _full_check(prob, ref, dev, seqs=None, K=None, min_exact=1.0):
     exc = check_verify(prob, run, finals, n, nx, target_ids, seqs)
     _say(f"  verify: n={n[seqs].tolist()[:8]} excused={exc}")
     return run, tally
-
-
-# ---------------------------------------------------------------- tiny ------
-
-def test_tiny_f32_workload_matches_oracle_and_sequential_decode():
-    _say("case: tiny fp32 workload H=256 V=1024 B=8 K=8, seeded ids")
-    prob = workload_problem(TINY_F32)
-    ref = make_refiner(prob)
-    dev = upload(prob)
-    run, tally = _full_check(prob, ref, dev)
-    assert tally.seq_exact == tally.seqs
-    # Theorem 1: with K = B passes the block is the sequential decode
-    P = O.Params.from_arrays(prob.weights)
-    s = O.base_logits(P.W_lm, prob.inp.h[0])
-    ystar = O.sequential_decode(P, s, prob.inp.h[0], int(prob.inp.anchor[0]))
-    assert np.array_equal(run.ids[0], ystar)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -265,44 +249,122 @@ def test_out_of_range_token_sets_device_error():
 
 
 # ------------------------------------------------------------- full size -----
+#
+# The five workloads at their own shapes and launch configuration.  Every
+# sequence is checked: ids and pass counts decision by decision, the final
+# logits within E element by element and within the absolute bar (1e-5 fp32,
+# 2e-2 bf16), verification exactly (greedy) or up to a near-tie (sampled).
+# A workload's device run and its oracle base logits are made once per module
+# (FullSize) and checked in groups of 16 sequences, one test per group.
+# MAX_EXCUSED is the number of near-tie decisions each workload's check
+# excused on MI355X (the inputs and the device arithmetic are deterministic,
+# so the count is fixed); more than that fails.
+
+ABS_BAR = {"f32": 1e-5, "bf16": 2e-2}
+GROUP = 16
+
+
+class FullSize:
+    def __init__(self, wl, tau=None):
+        import time
+        t0 = time.time()
+        self.prob = prob = workload_problem(wl, tau=tau)
+        self.ref = make_refiner(prob)
+        self.dev = upload(prob)
+        self.run = run_device(self.ref, prob, self.dev)
+        self.target_ids = prob.inp.target_ids(self.run.ids)
+        self.n, self.nx = _verify(self.ref, prob, self.run, self.dev, self.target_ids)
+        self.P = O.Params.from_arrays(prob.weights, round_z=prob.dtype == "bf16")
+        h = prob.inp.h.reshape(prob.batch * prob.B, prob.H)
+        self.s = O.base_logits(self.P.W_lm, h).reshape(prob.batch, prob.B, -1)
+        self.tally = Tally()
+        self.excused_verify = 0
+        _say(f"  {wl.name}: device run and oracle base logits in {time.time() - t0:.1f} s")
+
+    def check(self, seqs):
+        prob = self.prob
+        tally, finals = check_refine(prob, self.run, seqs=seqs, P=self.P, s=self.s[seqs],
+                                     abs_bar=ABS_BAR[prob.dtype])
+        exc = check_verify(prob, self.run, finals, self.n, self.nx, self.target_ids, seqs)
+        self.tally.add(tally)
+        self.excused_verify += exc
+        _say(f"  sequences {seqs[0]}..{seqs[-1]}: decisions={tally.decisions} "
+             f"exact={tally.exact} excused={tally.excused} seq_exact={tally.seq_exact}/"
+             f"{tally.seqs} max|dl|={tally.max_logit_err:.3g} "
+             f"max|dl|/E={tally.max_err_over_bound:.3g} verify n={self.n[seqs].tolist()} "
+             f"excused={exc}")
+        return tally, exc
+
+
+def _groups(batch):
+    return [list(range(g, min(batch, g + GROUP))) for g in range(0, batch, GROUP)]
+
 
 @pytest.fixture(scope="module")
-def qwen_b1():
-    prob = workload_problem(QWEN_B1)
-    return prob, make_refiner(prob), upload(prob)
+def full_sizes():
+    made = {}
+
+    def get(wl, tau=None):
+        key = (wl.name, tau)
+        if key not in made:
+            for k in list(made):                 # one workload's buffers at a time
+                made.pop(k).ref.close()
+            made[key] = FullSize(wl, tau)
+        return made[key]
+    yield get
+    for v in made.values():
+        v.ref.close()
 
 
-def test_qwen3_shape_batch1_greedy(qwen_b1):
-    _say("case: Qwen3-8B shape, batch 1, B=16, greedy, K=6 (bench workload)")
-    prob, ref, dev = qwen_b1
-    run, tally = _full_check(prob, ref, dev, min_exact=0.99)
+# excused near-tie decisions observed per workload (refine decisions, verify)
+MAX_EXCUSED = {
+    "tiny-f32-H256-V1024-B8-b1": (0, 0),
+    "qwen3-8b-bf16-B16-b1-greedy": (0, 0),
+    "qwen3-8b-bf16-B16-b8-sample": (2, 0),
+    "qwen3-8b-bf16-B16-b1-sample": (0, 0),
+    "qwen3-8b-bf16-B16-b32-greedy": (0, 0),
+    "qwen3-8b-bf16-B32-b64-mixed": (3, 0),
+}
 
 
-def test_qwen3_shape_batch8_sampled():
-    _say("case: Qwen3-8B shape, batch 8, B=16, temperature 1, K=6")
-    prob = workload_problem(QWEN_B8_T1)
-    ref = make_refiner(prob)
-    _full_check(prob, ref, upload(prob), min_exact=0.8)
+def _full_size_groups(wl, full_sizes, seqs, tau=None, name=None):
+    _say(f"case: {wl.name} T={tau} sequences {seqs[0]}..{seqs[-1]} of {wl.batch}")
+    fs = full_sizes(wl, tau)
+    fs.check(seqs)
+    ex_ref, ex_ver = MAX_EXCUSED[name or wl.name]
+    assert fs.tally.excused <= ex_ref, f"{fs.tally.excused} near-tie decisions excused"
+    assert fs.excused_verify <= ex_ver, f"{fs.excused_verify} verifications excused"
+    return fs
 
 
-def test_qwen3_shape_batch1_sampled_at_temperature():
+def test_tiny_f32_workload_matches_oracle_and_sequential_decode(full_sizes):
+    fs = _full_size_groups(TINY_F32, full_sizes, [0])
+    assert fs.tally.seq_exact == fs.tally.seqs
+    # Theorem 1: with K = B passes the block is the sequential decode
+    prob = fs.prob
+    ystar = O.sequential_decode(fs.P, fs.s[0], prob.inp.h[0], int(prob.inp.anchor[0]))
+    assert np.array_equal(fs.run.ids[0], ystar)
+
+
+def test_qwen3_shape_batch1_greedy(full_sizes):
+    _full_size_groups(QWEN_B1, full_sizes, [0])
+
+
+def test_qwen3_shape_batch8_sampled(full_sizes):
+    _full_size_groups(QWEN_B8_T1, full_sizes, list(range(8)))
+
+
+def test_qwen3_shape_batch1_sampled_at_temperature(full_sizes):
     from synth.configs import scaled
-    _say("case: Qwen3-8B shape, batch 1, B=16, sampled at T=0.6, K=6 (LM-head and Read streams)")
     wl = scaled(QWEN_B1, name="qwen3-8b-bf16-B16-b1-sample", temp="sample", h_sigma=1.5625)
-    prob = workload_problem(wl, tau=0.6)
-    ref = make_refiner(prob)
-    _full_check(prob, ref, upload(prob), min_exact=0.8)
+    _full_size_groups(wl, full_sizes, [0], tau=0.6)
 
 
-def test_qwen3_shape_batch32_greedy_sampled_sequences():
-    _say("case: Qwen3-8B shape, batch 32, B=16, greedy (4 sequences checked)")
-    prob = workload_problem(QWEN_B32)
-    ref = make_refiner(prob)
-    _full_check(prob, ref, upload(prob), seqs=[0, 9, 22, 31], min_exact=0.99)
+@pytest.mark.parametrize("seqs", _groups(QWEN_B32.batch))
+def test_qwen3_shape_batch32_greedy(full_sizes, seqs):
+    _full_size_groups(QWEN_B32, full_sizes, seqs)
 
 
-def test_qwen3_shape_batch64_block32_mixed_sampled_sequences():
-    _say("case: Qwen3-8B shape, batch 64, B=32, mixed rows (4 sequences checked)")
-    prob = workload_problem(QWEN_B64_MIXED)
-    ref = make_refiner(prob)
-    _full_check(prob, ref, upload(prob), seqs=[0, 1, 36, 63], min_exact=0.8)
+@pytest.mark.parametrize("seqs", _groups(QWEN_B64_MIXED.batch))
+def test_qwen3_shape_batch64_block32_mixed(full_sizes, seqs):
+    _full_size_groups(QWEN_B64_MIXED, full_sizes, seqs)
