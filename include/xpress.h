@@ -302,9 +302,41 @@ xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal
 /* Free the layer and its workspace (waits for the device first).  NULL is a no-op. */
 void xp_layer_destroy(xp_layer* L);
 
-/* Message for the last failed call on `L` (of the last failed
- * xp_layer_create on this thread when L is NULL); "" if none failed. */
+/* Message for the last failed call on `L` (when L is NULL: of the last failed
+ * xp_layer_create or xp_layer_forward_noalloc on this thread); "" if none
+ * failed. */
 const char* xp_layer_last_error(const xp_layer* L);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * forward as xp_layer_forward, without a layer handle and without any
+ * allocation.  `w` is the weight set (as for xp_layer_create; only read
+ * during the call); every other argument is as for xp_layer_forward.
+ *
+ * The intermediates live in a static device array of 64 MiB that every GPU
+ * the library runs on holds until the process ends; its address is looked up
+ * on the first call on each device.  Calls on one GPU share that array and it
+ * keeps the last call's contents: calls that overlap in time on one GPU (two
+ * streams, or two host threads) race and give undefined results; calls
+ * ordered on one stream are safe.  Output equals xp_layer_forward's bit for
+ * bit when the call's attention partials fit beside its other buffers at the
+ * default chunking; otherwise the context is read in longer chunks (fewer
+ * partials), which changes only the fp32 summation order.
+ *
+ * Limits: batch * B positions whose buffers (about 124 KB per position at
+ * the Qwen3-8B shape, plus 1.5 MB of gate/up rows) fit in the array with at
+ * least one attention partial per (sequence, position block, KV head, query
+ * head); calls beyond that return XP_EINVAL before any HIP call.
+ * Errors: XP_EINVAL (weights or arguments as for xp_layer_create and
+ * xp_layer_forward, sizes beyond the array), XP_EUNSUPPORTED (shapes outside
+ * the built set), before any HIP call; XP_EHIP if the address lookup or a
+ * launch fails.  xp_layer_last_error(NULL) names the problem.
+ */
+xp_status xp_layer_forward_noalloc(const xp_layer_weights* w, int32_t batch, int32_t B,
+                                   int32_t causal, const void* x, const void* k_cache,
+                                   const void* v_cache, int32_t C_max, const int32_t* ctx_len,
+                                   float* h_f32, void* h_bf16, void* stream);
 
 /*
  * Measurement probes (not part of the method).  They give the measured peaks

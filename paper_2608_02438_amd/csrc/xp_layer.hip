@@ -28,6 +28,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "xp_internal.h"
 
@@ -728,26 +729,34 @@ __global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ GU, in
 
 using namespace xp;
 
+// Device buffers of one forward (a layer's workspace, or the static scratch
+// of the allocation-free entry point).
+struct LayerBufs {
+  float* x32 = nullptr;              // [M][H]    x in fp32 (residual of Wo)
+  uint16_t* u = nullptr;             // [M][H]    RMSNorm(x) g_attn, then RMSNorm(x1) g_mlp
+  float* qkv = nullptr;              // [M][nhd + 2 kvd]
+  uint16_t *qn = nullptr, *kb = nullptr, *vb = nullptr;   // normed, rotated q, k; v
+  float *opart = nullptr, *mlpart = nullptr;              // attention chunk partials
+  uint16_t* attn = nullptr;          // [M][nhd]
+  float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;     // GU: [gu_rows][2 F] gate | up
+  uint16_t* act = nullptr;           // [M][F]    SwiGLU activation
+  size_t nparts = 0;                 // attention partials the buffers hold
+  size_t gu_rows = 0;                // positions GU holds
+};
+
 struct xp_layer {
   int H, nh, nkv, ffn, grp;
   float eps, theta;
   const uint16_t *g_attn, *Wq, *Wk, *Wv, *g_q, *g_k, *Wo, *g_mlp, *Wg, *Wu, *Wd;
-  int max_batch, max_B, max_ctx;
-  size_t nparts;                     // attention partials the workspace holds
-  void* ws = nullptr;
-  float* x32 = nullptr;
-  uint16_t* u = nullptr;
-  float* qkv = nullptr;
-  uint16_t *qn = nullptr, *kb = nullptr, *vb = nullptr;
-  float *opart = nullptr, *mlpart = nullptr;
-  uint16_t* attn = nullptr;
-  float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;
-  size_t gu_rows = 0;                // positions the gate/up buffer GU holds
-  uint16_t* act = nullptr;
+  int max_batch = 0, max_B = 0, max_ctx = 0;
+  void* ws = nullptr;                // the workspace allocation (NULL: static scratch)
+  LayerBufs b;
   std::string err;                   // message of the last failed call
 };
 
-static thread_local std::string g_layer_create_err;
+// Message of the last failed xp_layer_create or xp_layer_forward_noalloc of
+// this thread (calls without a layer to hold it).
+static thread_local std::string g_layer_err;
 
 static xp_status layer_fail(xp_layer* L, xp_status s, const char* fmt, ...)
     __attribute__((format(printf, 3, 4)));
@@ -757,27 +766,20 @@ static xp_status layer_fail(xp_layer* L, xp_status s, const char* fmt, ...) {
   va_start(ap, fmt);
   vsnprintf(buf, sizeof buf, fmt, ap);
   va_end(ap);
-  (L ? L->err : g_layer_create_err) = buf;
+  (L ? L->err : g_layer_err) = buf;
   return s;
 }
 
 extern "C" const char* xp_layer_last_error(const xp_layer* L) {
-  return L ? L->err.c_str() : g_layer_create_err.c_str();
+  return L ? L->err.c_str() : g_layer_err.c_str();
 }
 
 static int attn_chunks(int C_max, int B, int keys) { return (C_max + B + keys - 1) / keys; }
 
-extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
-                                     int32_t max_ctx, xp_layer** out) {
-  g_layer_create_err.clear();
-  if (out == nullptr) return layer_fail(nullptr, XP_EINVAL, "out is NULL");
-  *out = nullptr;
+// Checks the weight set and copies it into *L (shapes and pointers only).
+// Errors are reported through layer_fail(nullptr, ...).
+static xp_status layer_weights(const xp_layer_weights* w, xp_layer* L) {
   if (w == nullptr) return layer_fail(nullptr, XP_EINVAL, "weights is NULL");
-  if (max_batch < 1 || max_batch > 4096 || max_B < 1 || max_B > 32 || max_ctx < 0 ||
-      max_ctx > (1 << 20))
-    return layer_fail(nullptr, XP_EINVAL,
-                      "max_batch=%d (1..4096), max_B=%d (1..32) or max_ctx=%d (0..2^20) out of range",
-                      max_batch, max_B, max_ctx);
   const void* ptrs[] = {w->g_attn, w->Wq, w->Wk, w->Wv, w->g_q, w->g_k,
                         w->Wo,     w->g_mlp, w->Wg, w->Wu, w->Wd};
   const char* names[] = {"g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp", "Wg", "Wu", "Wd"};
@@ -797,15 +799,6 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
                       "shape not built: head_dim %d (128), heads/kv %d/%d (group 1, 2, 4 or 8), "
                       "H %d and heads*128 multiples of 256 with H <= 8192, ffn %d a multiple of 256 "
                       "up to 65536", w->head_dim, w->n_heads, w->n_kv, w->H, w->ffn);
-  // every projection addresses rows of its input as (position * K) in 32 bits
-  const int64_t widest = std::max<int64_t>({(int64_t)w->H, (int64_t)w->n_heads * kHd,
-                                            (int64_t)w->ffn});
-  if ((int64_t)max_batch * max_B * widest >= ((int64_t)1 << 31))
-    return layer_fail(nullptr, XP_EUNSUPPORTED,
-                      "max_batch*max_B*max(H, heads*128, ffn) = %lld reaches 2^31",
-                      (long long)max_batch * max_B * widest);
-  xp_layer* L = new (std::nothrow) xp_layer();
-  if (L == nullptr) return layer_fail(nullptr, XP_ENOMEM, "host allocation failed");
   L->H = w->H;
   L->nh = w->n_heads;
   L->nkv = w->n_kv;
@@ -824,41 +817,107 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   L->Wg = (const uint16_t*)w->Wg;
   L->Wu = (const uint16_t*)w->Wu;
   L->Wd = (const uint16_t*)w->Wd;
+  return XP_OK;
+}
+
+// Every projection addresses rows of its input as (position * K) in 32 bits.
+static bool rows_fit_int32(const xp_layer& L, int64_t positions) {
+  const int64_t widest = std::max<int64_t>({(int64_t)L.H, (int64_t)L.nh * kHd, (int64_t)L.ffn});
+  return positions * widest < ((int64_t)1 << 31);
+}
+
+// The gate/up projections write fp32 [M][2 F] to GU on two paths: the stream
+// kernel (calls of at most one 16-position block, H within its LDS copy of
+// x) and the tiled GEMM (calls above kLinMaxStream positions).  For calls of
+// up to Mx positions GU must hold the largest M of the two.
+static size_t gu_rows_for(const xp_layer& L, size_t Mx) {
+  size_t gu = 0;
+  if ((size_t)L.H <= 8 * (size_t)kGsXChunks) gu = std::min(Mx, (size_t)kTile);
+  if (Mx > (size_t)kLinMaxStream) gu = Mx;
+  return gu;
+}
+
+// Lays out the buffers for up to Mx positions and nparts attention partials
+// from `base` (256-byte aligned slices); returns the bytes used.  With
+// base == nullptr only the size is computed.
+static size_t carve(const xp_layer& L, size_t Mx, size_t nparts, size_t gu_rows, char* base,
+                    LayerBufs* b) {
+  const size_t H = L.H, nhd = (size_t)L.nh * kHd, kvd = (size_t)L.nkv * kHd, F = L.ffn;
+  LayerBufs t;
+  t.nparts = nparts;
+  t.gu_rows = gu_rows;
+  struct Slice {
+    void** p;
+    size_t bytes;
+  } sl[] = {
+      {(void**)&t.x32, Mx * H * 4},           {(void**)&t.u, Mx * H * 2},
+      {(void**)&t.qkv, Mx * (nhd + 2 * kvd) * 4}, {(void**)&t.qn, Mx * nhd * 2},
+      {(void**)&t.kb, Mx * kvd * 2},          {(void**)&t.vb, Mx * kvd * 2},
+      {(void**)&t.opart, nparts * kTile * kHd * 4}, {(void**)&t.mlpart, nparts * 2 * kTile * 4},
+      {(void**)&t.attn, Mx * nhd * 2},        {(void**)&t.x1, Mx * H * 4},
+      {(void**)&t.act, Mx * F * 2},           {(void**)&t.h32, Mx * H * 4},
+      {(void**)&t.GU, (gu_rows ? gu_rows : 1) * 2 * F * 4},
+  };
+  size_t off = 0;
+  for (auto& q : sl) {
+    if (base) *q.p = base + off;
+    off += (q.bytes + 255) / 256 * 256;
+  }
+  if (base && b) *b = t;
+  return off;
+}
+
+// Attention chunking of one call: chunks of nsub 64-key sub-chunks, about
+// kAttnWgs workgroups in all (one sub-chunk each at small calls), so that the
+// partials stay few.  Returns the partial count batch * npb * nkv * ns * grp.
+struct AttnPlan {
+  int nsub, ns;
+  size_t parts;
+};
+static AttnPlan attn_plan(const xp_layer& L, int batch, int B, int C_max, int nsub) {
+  const int npb = (B + kTile - 1) / kTile;
+  const int ns = attn_chunks(C_max, B, kSub * nsub);
+  return {nsub, ns, (size_t)batch * npb * L.nkv * ns * L.grp};
+}
+static AttnPlan attn_plan_default(const xp_layer& L, int batch, int B, int C_max) {
+  const int npb = (B + kTile - 1) / kTile;
+  const size_t w64 = (size_t)batch * npb * L.nkv * attn_chunks(C_max, B, kSub);
+  int nsub = (int)(w64 / kAttnWgs);
+  nsub = nsub < 1 ? 1 : (nsub > 256 ? 256 : nsub);
+  return attn_plan(L, batch, B, C_max, nsub);
+}
+
+extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batch, int32_t max_B,
+                                     int32_t max_ctx, xp_layer** out) {
+  g_layer_err.clear();
+  if (out == nullptr) return layer_fail(nullptr, XP_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (max_batch < 1 || max_batch > 4096 || max_B < 1 || max_B > 32 || max_ctx < 0 ||
+      max_ctx > (1 << 20))
+    return layer_fail(nullptr, XP_EINVAL,
+                      "max_batch=%d (1..4096), max_B=%d (1..32) or max_ctx=%d (0..2^20) out of range",
+                      max_batch, max_B, max_ctx);
+  xp_layer tmp;
+  const xp_status ws = layer_weights(w, &tmp);
+  if (ws != XP_OK) return ws;
+  if (!rows_fit_int32(tmp, (int64_t)max_batch * max_B))
+    return layer_fail(nullptr, XP_EUNSUPPORTED,
+                      "max_batch*max_B*max(H, heads*128, ffn) reaches 2^31 (max_batch=%d max_B=%d)",
+                      max_batch, max_B);
+  xp_layer* L = new (std::nothrow) xp_layer(tmp);
+  if (L == nullptr) return layer_fail(nullptr, XP_ENOMEM, "host allocation failed");
   L->max_batch = max_batch;
   L->max_B = max_B;
   L->max_ctx = max_ctx;
-  const size_t Mx = (size_t)max_batch * max_B, H = L->H, nhd = (size_t)L->nh * kHd,
-               kvd = (size_t)L->nkv * kHd, F = L->ffn;
+  const size_t Mx = (size_t)max_batch * max_B;
   const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
   // attention partials: a call has at most max(2 kAttnWgs, w64 / 256) + one
   // per (sequence, position block, KV head) chunks, w64 its 64-key sub-chunks
   const size_t w64max = zmax * L->nkv * (size_t)attn_chunks(max_ctx, max_B, kSub);
   const size_t nparts =
-      (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + zmax * L->nkv) * grp;
-  L->nparts = nparts;
-  // The gate/up projections write fp32 [M][2 F] to GU on two paths: the
-  // stream kernel (calls of at most one 16-position block, H within its LDS
-  // copy of x) and the tiled GEMM (calls above kLinMaxStream positions).  Any
-  // call up to the created maxima may take either, so GU holds the largest M
-  // of the two.
-  size_t gu = 0;
-  if (H <= 8 * (size_t)kGsXChunks) gu = std::min(Mx, (size_t)kTile);
-  if (Mx > (size_t)kLinMaxStream) gu = Mx;
-  L->gu_rows = gu;
-  struct Slice {
-    void** p;
-    size_t bytes;
-  } sl[] = {
-      {(void**)&L->x32, Mx * H * 4},           {(void**)&L->u, Mx * H * 2},
-      {(void**)&L->qkv, Mx * (nhd + 2 * kvd) * 4}, {(void**)&L->qn, Mx * nhd * 2},
-      {(void**)&L->kb, Mx * kvd * 2},          {(void**)&L->vb, Mx * kvd * 2},
-      {(void**)&L->opart, nparts * kTile * kHd * 4}, {(void**)&L->mlpart, nparts * 2 * kTile * 4},
-      {(void**)&L->attn, Mx * nhd * 2},        {(void**)&L->x1, Mx * H * 4},
-      {(void**)&L->act, Mx * F * 2},           {(void**)&L->h32, Mx * H * 4},
-      {(void**)&L->GU, (gu ? gu : 1) * 2 * F * 4},
-  };
-  size_t total = 0;
-  for (auto& s : sl) total += (s.bytes + 255) / 256 * 256;
+      (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + zmax * L->nkv) * L->grp;
+  const size_t gu = gu_rows_for(*L, Mx);
+  const size_t total = carve(*L, Mx, nparts, gu, nullptr, nullptr);
   const hipError_t e = hipMalloc(&L->ws, total);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -866,11 +925,7 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
     return layer_fail(nullptr, XP_ENOMEM, "workspace of %zu bytes: %s", total,
                       hipGetErrorString(e));
   }
-  char* p = static_cast<char*>(L->ws);
-  for (auto& s : sl) {
-    *s.p = p;
-    p += (s.bytes + 255) / 256 * 256;
-  }
+  carve(*L, Mx, nparts, gu, static_cast<char*>(L->ws), &L->b);
   *out = L;
   return XP_OK;
 }
@@ -951,65 +1006,67 @@ static hipError_t linear(const uint16_t* W0, const uint16_t* W1, const uint16_t*
   return hipGetLastError();
 }
 
-extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal,
-                                      const void* x, const void* k_cache, const void* v_cache,
-                                      int32_t C_max, const int32_t* ctx_len, float* h_f32,
-                                      void* h_bf16, void* stream) {
-  if (L == nullptr) return XP_EINVAL;
+// Argument checks of a forward call, shared by both entry points.
+static xp_status check_call(xp_layer* Lerr, int32_t batch, int32_t B, int32_t causal,
+                            const void* x, const void* k_cache, const void* v_cache,
+                            int32_t C_max, const int32_t* ctx_len, const float* h_f32,
+                            const void* h_bf16) {
   if (x == nullptr || k_cache == nullptr || v_cache == nullptr || ctx_len == nullptr)
-    return layer_fail(L, XP_EINVAL, "x, k_cache, v_cache and ctx_len are required");
-  if (batch < 1 || batch > L->max_batch || B < 1 || B > L->max_B)
-    return layer_fail(L, XP_EINVAL, "batch=%d (1..%d) or B=%d (1..%d) outside the created maxima",
-                      batch, L->max_batch, B, L->max_B);
-  if (C_max < 1 || C_max > (L->max_ctx > 0 ? L->max_ctx : 1))
-    return layer_fail(L, XP_EINVAL, "C_max=%d out of range 1..%d", C_max,
-                      L->max_ctx > 0 ? L->max_ctx : 1);
-  if (causal != 0 && causal != 1) return layer_fail(L, XP_EINVAL, "causal=%d is not 0 or 1", causal);
+    return layer_fail(Lerr, XP_EINVAL, "x, k_cache, v_cache and ctx_len are required");
+  if (causal != 0 && causal != 1) return layer_fail(Lerr, XP_EINVAL, "causal=%d is not 0 or 1", causal);
+  if (batch < 1 || B < 1 || B > 32 || C_max < 1 || C_max > (1 << 20))
+    return layer_fail(Lerr, XP_EINVAL, "batch=%d, B=%d (1..32) or C_max=%d (1..2^20) out of range",
+                      batch, B, C_max);
   const char* pn[] = {"x", "k_cache", "v_cache", "h_f32", "h_bf16"};
-  const void* pv[] = {x, k_cache, v_cache, (const void*)h_f32, (const void*)h_bf16};
+  const void* pv[] = {x, k_cache, v_cache, (const void*)h_f32, h_bf16};
   for (int i = 0; i < 5; ++i)
     if (reinterpret_cast<uintptr_t>(pv[i]) % 16 != 0)
-      return layer_fail(L, XP_EINVAL, "%s is not 16-byte aligned", pn[i]);
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int M = batch * B, H = L->H, nh = L->nh, nkv = L->nkv, F = L->ffn, grp = L->grp;
+      return layer_fail(Lerr, XP_EINVAL, "%s is not 16-byte aligned", pn[i]);
+  return XP_OK;
+}
+
+// The launch sequence of one forward over `batch` blocks of B positions with
+// the attention chunking `ap`, on the buffers `b` (which hold at least the
+// call's positions and ap.parts partials).  Errors go to Lerr (NULL: the
+// thread's message).
+static xp_status forward(const xp_layer& L, const LayerBufs& b, const AttnPlan& ap,
+                         xp_layer* Lerr, int32_t batch, int32_t B, int32_t causal, const void* x,
+                         const void* k_cache, const void* v_cache, int32_t C_max,
+                         const int32_t* ctx_len, float* h_f32, void* h_bf16, hipStream_t st) {
+  const int M = batch * B, H = L.H, nh = L.nh, nkv = L.nkv, F = L.ffn, grp = L.grp;
   const int nhd = nh * kHd, kvd = nkv * kHd, ldq = nhd + 2 * kvd;
   const int npb = (B + kTile - 1) / kTile;
-  // chunks of nsub 64-key sub-chunks: about kAttnWgs workgroups in all (one
-  // sub-chunk each at small calls), so that the partials stay few
-  const size_t w64 = (size_t)batch * npb * nkv * attn_chunks(C_max, B, kSub);
-  int nsub = (int)(w64 / kAttnWgs);
-  nsub = nsub < 1 ? 1 : (nsub > 256 ? 256 : nsub);
-  const int ns = attn_chunks(C_max, B, kSub * nsub);
-  if ((size_t)batch * npb * nkv * ns * grp > L->nparts)
-    return layer_fail(L, XP_EINVAL, "attention partials exceed the workspace");   // not reached
-  float* hout = h_f32 ? h_f32 : L->h32;
+  const int ns = ap.ns, nsub = ap.nsub;
+  if (ap.parts > b.nparts)
+    return layer_fail(Lerr, XP_EINVAL, "attention partials exceed the buffers");   // not reached
+  float* hout = h_f32 ? h_f32 : b.h32;
   hipError_t e;
 #define XP_STEP(what, call)                                                                  \
   do {                                                                                       \
     call;                                                                                    \
     if ((e = hipGetLastError()) != hipSuccess)                                               \
-      return layer_fail(L, XP_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));     \
+      return layer_fail(Lerr, XP_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));  \
   } while (0)
 #define XP_LINEAR(what, ...)                                                                 \
   do {                                                                                       \
     if ((e = linear(__VA_ARGS__)) != hipSuccess)                                             \
-      return layer_fail(L, e == hipErrorInvalidValue ? XP_EINVAL : XP_EHIP,                  \
+      return layer_fail(Lerr, e == hipErrorInvalidValue ? XP_EINVAL : XP_EHIP,               \
                         "%s projection failed: %s", what, hipGetErrorString(e));             \
   } while (0)
 
   XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st,
-                                        (const uint16_t*)x, H, L->g_attn, L->eps, L->x32, L->u));
-  XP_LINEAR("q/k/v", L->Wq, L->Wk, L->Wv, nhd, kvd, ldq, H, L->u, M, nullptr, 0, L->qkv, nullptr,
-            ldq, false, st);
+                                        (const uint16_t*)x, H, L.g_attn, L.eps, b.x32, b.u));
+  XP_LINEAR("q/k/v", L.Wq, L.Wk, L.Wv, nhd, kvd, ldq, H, b.u, M, nullptr, 0, b.qkv, nullptr, ldq,
+            false, st);
   const int qk_waves = M * (nh + 2 * nkv);
   XP_STEP("qk-norm/rope",
-          hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, L->qkv, ldq, M,
-                             B, nh, nkv, ctx_len, C_max, L->g_q, L->g_k, L->eps, L->theta, L->qn,
-                             L->kb, L->vb));
+          hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, b.qkv, ldq, M,
+                             B, nh, nkv, ctx_len, C_max, L.g_q, L.g_k, L.eps, L.theta, b.qn, b.kb,
+                             b.vb));
 #define XP_ATTN(GG)                                                                           \
-  hipLaunchKernelGGL(k_attn<GG>, dim3(ns, nkv, batch * npb), dim3(GG * kWave), 0, st, L->qn, \
-                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, L->kb, L->vb, ctx_len, \
-                     C_max, B, npb, nh, nkv, causal, ns, nsub, L->opart, L->mlpart)
+  hipLaunchKernelGGL(k_attn<GG>, dim3(ns, nkv, batch * npb), dim3(GG * kWave), 0, st, b.qn,  \
+                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, b.kb, b.vb, ctx_len, \
+                     C_max, B, npb, nh, nkv, causal, ns, nsub, b.opart, b.mlpart)
   if (grp == 1) XP_STEP("attention", XP_ATTN(1));
   else if (grp == 2) XP_STEP("attention", XP_ATTN(2));
   else if (grp == 4) XP_STEP("attention", XP_ATTN(4));
@@ -1017,18 +1074,119 @@ extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int
 #undef XP_ATTN
   const int cw = M * nh;
   XP_STEP("attention combine",
-          hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, L->opart,
-                             L->mlpart, M, B, npb, nh, nkv, grp, ns, L->attn));
-  XP_LINEAR("output", L->Wo, nullptr, nullptr, H, 0, H, nhd, L->attn, M, L->x32, H, L->x1,
-            nullptr, H, false, st);
+          hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, b.opart,
+                             b.mlpart, M, B, npb, nh, nkv, grp, ns, b.attn));
+  XP_LINEAR("output", L.Wo, nullptr, nullptr, H, 0, H, nhd, b.attn, M, b.x32, H, b.x1, nullptr, H,
+            false, st);
   XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st,
-                                        (const float*)L->x1, H, L->g_mlp, L->eps, (float*)nullptr,
-                                        L->u));
-  XP_LINEAR("gate/up", L->Wg, L->Wu, nullptr, F, 0, F, H, L->u, M, nullptr, 0, nullptr, L->act, F,
-            true, st, L->GU, L->gu_rows);
-  XP_LINEAR("down", L->Wd, nullptr, nullptr, H, 0, H, F, L->act, M, L->x1, H, hout,
+                                        (const float*)b.x1, H, L.g_mlp, L.eps, (float*)nullptr,
+                                        b.u));
+  XP_LINEAR("gate/up", L.Wg, L.Wu, nullptr, F, 0, F, H, b.u, M, nullptr, 0, nullptr, b.act, F,
+            true, st, b.GU, b.gu_rows);
+  XP_LINEAR("down", L.Wd, nullptr, nullptr, H, 0, H, F, b.act, M, b.x1, H, hout,
             (uint16_t*)h_bf16, H, false, st);
 #undef XP_STEP
 #undef XP_LINEAR
   return XP_OK;
+}
+
+extern "C" xp_status xp_layer_forward(xp_layer* L, int32_t batch, int32_t B, int32_t causal,
+                                      const void* x, const void* k_cache, const void* v_cache,
+                                      int32_t C_max, const int32_t* ctx_len, float* h_f32,
+                                      void* h_bf16, void* stream) {
+  if (L == nullptr) return XP_EINVAL;
+  const xp_status cs =
+      check_call(L, batch, B, causal, x, k_cache, v_cache, C_max, ctx_len, h_f32, h_bf16);
+  if (cs != XP_OK) return cs;
+  if (batch > L->max_batch || B > L->max_B)
+    return layer_fail(L, XP_EINVAL, "batch=%d (1..%d) or B=%d (1..%d) outside the created maxima",
+                      batch, L->max_batch, B, L->max_B);
+  if (C_max > (L->max_ctx > 0 ? L->max_ctx : 1))
+    return layer_fail(L, XP_EINVAL, "C_max=%d out of range 1..%d", C_max,
+                      L->max_ctx > 0 ? L->max_ctx : 1);
+  return forward(*L, L->b, attn_plan_default(*L, batch, B, C_max), L, batch, B, causal, x,
+                 k_cache, v_cache, C_max, ctx_len, h_f32, h_bf16, (hipStream_t)stream);
+}
+
+// ---------------------------------------------------------------------------
+// The allocation-free forward.  Its buffers live in `scratch`, a static
+// device array (every GPU the library runs on holds its own copy until the
+// process ends).  Host code never uses the array's name as an address: the
+// device address is looked up once per device with hipGetSymbolAddress and
+// kept in g_scratch.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up on the first
+// call there.
+static hipError_t scratch_ptr(char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = p;
+  }
+  *out = static_cast<char*>(g_scratch[dev]);
+  return hipSuccess;
+}
+
+extern "C" xp_status xp_layer_forward_noalloc(const xp_layer_weights* w, int32_t batch, int32_t B,
+                                              int32_t causal, const void* x, const void* k_cache,
+                                              const void* v_cache, int32_t C_max,
+                                              const int32_t* ctx_len, float* h_f32, void* h_bf16,
+                                              void* stream) {
+  g_layer_err.clear();
+  xp_layer L;
+  xp_status s = layer_weights(w, &L);
+  if (s != XP_OK) return s;
+  s = check_call(nullptr, batch, B, causal, x, k_cache, v_cache, C_max, ctx_len, h_f32, h_bf16);
+  if (s != XP_OK) return s;
+  const size_t M = (size_t)batch * B;
+  if (!rows_fit_int32(L, (int64_t)M))
+    return layer_fail(nullptr, XP_EINVAL, "batch*B*max(H, heads*128, ffn) reaches 2^31");
+  // The buffers the call needs, its partials at the default chunking; if
+  // those do not fit, chunks of more 64-key sub-chunks (fewer partials).
+  const size_t gu = gu_rows_for(L, M);
+  const size_t fixed = carve(L, M, 0, gu, nullptr, nullptr);
+  const size_t per_part = (size_t)kTile * kHd * 4 + (size_t)2 * kTile * 4;   // opart + mlpart
+  if (fixed + 2 * 256 + per_part > kScratchBytes)
+    return layer_fail(nullptr, XP_EINVAL,
+                      "%zu positions need %zu bytes of buffers; the static scratch holds %zu",
+                      M, fixed + per_part, kScratchBytes);
+  const size_t max_parts = (kScratchBytes - fixed - 2 * 256) / per_part;
+  AttnPlan ap = attn_plan_default(L, batch, B, C_max);
+  if (ap.parts > max_parts) {
+    const int chunks64 = attn_chunks(C_max, B, kSub);
+    int lo = ap.nsub, hi = chunks64;             // ap at nsub = chunks64 has ns = 1
+    if (attn_plan(L, batch, B, C_max, hi).parts > max_parts)
+      return layer_fail(nullptr, XP_EINVAL,
+                        "%d sequences x %d KV heads need more attention partials than the static "
+                        "scratch holds beside %zu positions", batch, L.nkv, M);
+    while (lo + 1 < hi) {                        // smallest nsub whose partials fit
+      const int mid = lo + (hi - lo) / 2;
+      if (attn_plan(L, batch, B, C_max, mid).parts > max_parts) lo = mid;
+      else hi = mid;
+    }
+    ap = attn_plan(L, batch, B, C_max, hi);
+  }
+  char* base = nullptr;
+  const hipError_t e = scratch_ptr(&base);
+  if (e != hipSuccess)
+    return layer_fail(nullptr, XP_EHIP, "static scratch address: %s", hipGetErrorString(e));
+  LayerBufs b;
+  const size_t used = carve(L, M, ap.parts, gu, base, &b);
+  if (used > kScratchBytes)                      // not reached: sized above
+    return layer_fail(nullptr, XP_EINVAL, "buffers of %zu bytes exceed the static scratch", used);
+  return forward(L, b, ap, nullptr, batch, B, causal, x, k_cache, v_cache, C_max, ctx_len, h_f32,
+                 h_bf16, (hipStream_t)stream);
 }

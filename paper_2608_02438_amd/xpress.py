@@ -24,7 +24,8 @@ XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE = 1, 2
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
            "xp_timing_read", "xp_probe_hbm_read", "xp_probe_mfma_bf16", "xp_toeplitz_mixer",
-           "xp_layer_create", "xp_layer_forward", "xp_layer_destroy", "xp_layer_last_error")
+           "xp_layer_create", "xp_layer_forward", "xp_layer_destroy", "xp_layer_last_error",
+           "xp_layer_forward_noalloc")
 LAYER_WEIGHT_NAMES = ("g_attn", "Wq", "Wk", "Wv", "g_q", "g_k", "Wo", "g_mlp", "Wg", "Wu", "Wd")
 STAGES = ("prep", "lmhead", "select", "rspace", "read", "verify")
 
@@ -94,6 +95,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_layer_destroy.restype = None
     L.xp_layer_last_error.argtypes = [vp]
     L.xp_layer_last_error.restype = ctypes.c_char_p
+    L.xp_layer_forward_noalloc.argtypes = [ctypes.POINTER(_LayerWeights), i32, i32, i32, vp, vp,
+                                           vp, i32, vp, vp, vp, vp]
+    L.xp_layer_forward_noalloc.restype = i32
     _lib = L
     return L
 
@@ -296,6 +300,33 @@ def toeplitz_mixer(kappa, out=None, stream=None):
     _check(L.xp_toeplitz_mixer(_ptr(kappa), r, B, dt, _ptr(out), _stream(stream)),
            "xp_toeplitz_mixer")
     return out
+
+
+def layer_weights_struct(weights: Dict[str, object], H: int, n_heads: int, n_kv: int, ffn: int,
+                         eps: float = 1e-6, theta: float = 1e6, head_dim: int = 128):
+    """The xp_layer_weights record of a weight dict (LAYER_WEIGHT_NAMES to bf16
+    device tensors)."""
+    w = _LayerWeights(H=H, n_heads=n_heads, n_kv=n_kv, head_dim=head_dim, ffn=ffn, eps=eps,
+                      rope_theta=theta)
+    for n in LAYER_WEIGHT_NAMES:
+        setattr(w, n, _ptr(weights[n]))
+    return w
+
+
+def layer_forward_noalloc(w, x, k_cache, v_cache, ctx_len, h_f32, h_bf16, causal=True,
+                          stream=None):
+    """xp_layer_forward_noalloc: one forward with the library's static
+    scratch; `w` from layer_weights_struct, outputs preallocated by the
+    caller (no allocation happens here or in the library)."""
+    L = load_library()
+    batch, B, _ = x.shape
+    for t in (x, k_cache, v_cache, ctx_len, h_f32, h_bf16):
+        assert t.is_contiguous()
+    st = L.xp_layer_forward_noalloc(ctypes.byref(w), batch, B, 1 if causal else 0, _ptr(x),
+                                    _ptr(k_cache), _ptr(v_cache), k_cache.shape[1],
+                                    _ptr(ctx_len), _ptr(h_f32), _ptr(h_bf16), _stream(stream))
+    if st != XP_OK:
+        raise XpError(st, "xp_layer_forward_noalloc: " + L.xp_layer_last_error(None).decode())
 
 
 class Layer:

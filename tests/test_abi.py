@@ -145,3 +145,37 @@ def test_layer_create_and_forward_reject_bad_sizes_and_null_handles():
     p = 0x1000
     assert L.xp_layer_forward(None, 1, 16, 1, p, p, p, 64, p, p, p, None) == X.XP_EINVAL
     L.xp_layer_destroy(None)
+
+
+def _layer_weights(**kw):
+    w = X._LayerWeights(H=4096, n_heads=32, n_kv=8, head_dim=128, ffn=12288, eps=1e-6,
+                        rope_theta=1e6)
+    for n in X.LAYER_WEIGHT_NAMES:
+        setattr(w, n, 0x1000)          # never dereferenced: validation fails first
+    for k, v in kw.items():
+        setattr(w, k, v)
+    return w
+
+
+@pytest.mark.parametrize("change,call,status", [
+    ({}, dict(batch=64, B=32), X.XP_EINVAL),              # 2048 positions: beyond the scratch
+    ({}, dict(batch=1, B=33), X.XP_EINVAL),
+    ({}, dict(batch=0, B=16), X.XP_EINVAL),
+    ({}, dict(C_max=0), X.XP_EINVAL),
+    ({}, dict(causal=2), X.XP_EINVAL),
+    ({}, dict(x=0x1008), X.XP_EINVAL),                    # not 16-byte aligned
+    (dict(Wd=None), {}, X.XP_EINVAL),
+    (dict(head_dim=64), {}, X.XP_EUNSUPPORTED),
+    (dict(n_heads=24), {}, X.XP_EUNSUPPORTED),            # group 3
+])
+def test_layer_forward_noalloc_rejects_without_a_gpu(change, call, status):
+    """The allocation-free forward checks the weights, the call and whether
+    the call's buffers fit its static scratch before any HIP call."""
+    L = X.load_library()
+    w = _layer_weights(**change)
+    a = dict(batch=1, B=16, causal=1, x=0x1000, C_max=100)
+    a.update(call)
+    st = L.xp_layer_forward_noalloc(ctypes.byref(w), a["batch"], a["B"], a["causal"], a["x"],
+                                    0x1000, 0x1000, a["C_max"], 0x1000, 0x1000, 0x1000, None)
+    assert st == status
+    assert L.xp_layer_last_error(None)
