@@ -290,17 +290,52 @@ def softmax_weights(l: np.ndarray, T: float = 1.0) -> np.ndarray:
     return np.exp((l - l.max()) / float(T))
 
 
-def select_sample(l: np.ndarray, u: float, T: float = 1.0):
-    """Inverse-CDF sample of softmax(l / T) at the uniform u; returns (token, margin)."""
-    return inverse_cdf(softmax_weights(l, T), u)
+def filtered_weights(l: np.ndarray, T: float = 1.0, top_k: int = 0,
+                     top_p: float = 1.0) -> np.ndarray:
+    """softmax_weights(l, T) restricted to the tokens the top-k and top-p
+    truncations keep (zero elsewhere); top_k = 0 (or >= V) and top_p >= 1
+    keep every token.
 
-
-def select(l: np.ndarray, sample: bool, u: float, T: float = 1.0):
-    return select_sample(l, u, T) if sample else select_greedy(l)
-
-
-def softmax(l: np.ndarray, T: float = 1.0) -> np.ndarray:
+    Truncated sampling at temperature T (the filtered form of the sampling
+    that verification keeps lossless, section 3.1), in this order:
+    * top-k keeps every token whose scaled logit x = l / T is at least the
+      k-th largest of them (counted with multiplicity, so ties with it stay);
+    * top-p then orders the kept tokens by x descending, ties by lower index
+      first, and keeps each token whose preceding mass in that order is
+      below p times the total mass of the top-k set, i.e. the shortest
+      prefix whose mass reaches p of it.
+    """
     w = softmax_weights(l, T)
+    V = w.shape[0]
+    keep = np.ones(V, dtype=bool)
+    x = np.asarray(l, dtype=F64) / float(T)
+    if 0 < top_k < V:
+        kth = np.sort(x)[V - top_k]
+        keep &= x >= kth
+    if top_p < 1.0:
+        idx = np.nonzero(keep)[0]
+        order = idx[np.lexsort((idx, -x[idx]))]          # x descending, then index ascending
+        before = np.concatenate([[0.0], np.cumsum(w[order])[:-1]])
+        keep_p = np.zeros(V, dtype=bool)
+        keep_p[order[before < top_p * w[idx].sum()]] = True
+        keep &= keep_p
+    return np.where(keep, w, 0.0)
+
+
+def select_sample(l: np.ndarray, u: float, T: float = 1.0, top_k: int = 0, top_p: float = 1.0):
+    """Inverse-CDF sample of the (filtered) softmax(l / T) at the uniform u;
+    returns (token, margin)."""
+    return inverse_cdf(filtered_weights(l, T, top_k, top_p), u)
+
+
+def select(l: np.ndarray, sample: bool, u: float, T: float = 1.0, top_k: int = 0,
+           top_p: float = 1.0):
+    return select_sample(l, u, T, top_k, top_p) if sample else select_greedy(l)
+
+
+def softmax(l: np.ndarray, T: float = 1.0, top_k: int = 0, top_p: float = 1.0) -> np.ndarray:
+    """The (filtered) softmax(l / T), normalised."""
+    w = filtered_weights(l, T, top_k, top_p)
     return w / w.sum()
 
 
@@ -325,7 +360,8 @@ class Refined:
 
 def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
                  sample: bool = False, u=None, K: int = 6,
-                 early_exit: bool = True, T: float = 1.0) -> Refined:
+                 early_exit: bool = True, T: float = 1.0, top_k: int = 0,
+                 top_p: float = 1.0) -> Refined:
     """Algorithm 1 for one sequence.
 
     Y^(0) is ``seed`` when given, otherwise each position's selection from the
@@ -333,7 +369,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
     x_{k-1} = y^(j)_{k-1}), re-selects every position from s_k + delta_k in
     parallel, and stops once Y^(j+1) = Y^(j).  With ``early_exit`` False the
     loop always runs K passes, which must not change the result.  Sampled
-    sequences draw from softmax(l / T).
+    sequences draw from softmax(l / T), truncated by top_k / top_p.
     """
     B = s_b.shape[0]
     u = np.zeros(B) if u is None else np.asarray(u, dtype=F64)
@@ -342,7 +378,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
         Y = np.asarray(seed, dtype=np.int64).copy()
         mg = np.full(B, np.inf)
     else:
-        sel = [select(s_b[k], sample, u[k], T) for k in range(B)]
+        sel = [select(s_b[k], sample, u[k], T, top_k, top_p) for k in range(B)]
         Y = np.array([t for t, _ in sel], dtype=np.int64)
         mg = np.array([m for _, m in sel])
     traj, margins = [Y.copy()], [mg]
@@ -351,7 +387,7 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
         x_prev = np.concatenate([[anchor], Y[:-1]])
         delta, Z = refiner(P, st, x_prev)
         l = s_b + delta
-        sel = [select(l[k], sample, u[k], T) for k in range(B)]
+        sel = [select(l[k], sample, u[k], T, top_k, top_p) for k in range(B)]
         Yn = np.array([t for t, _ in sel], dtype=np.int64)
         traj.append(Yn.copy())
         margins.append(np.array([m for _, m in sel]))
@@ -368,7 +404,8 @@ def refine_block(P: Params, s_b: np.ndarray, h_b, anchor: int, seed=None,
 
 
 def sequential_decode(P: Params, s_b: np.ndarray, h_b, anchor: int,
-                      sample: bool = False, u=None, T: float = 1.0) -> np.ndarray:
+                      sample: bool = False, u=None, T: float = 1.0, top_k: int = 0,
+                      top_p: float = 1.0) -> np.ndarray:
     """y*_k = select(s_k + delta_k(x_0, y*_1..y*_{k-1})) for k = 1..B, in order.
 
     Positions after k are filled with token 0; by the causal structure of the
@@ -381,11 +418,12 @@ def sequential_decode(P: Params, s_b: np.ndarray, h_b, anchor: int,
     for k in range(B):
         x_prev = np.concatenate([[anchor], Y[:-1]])
         delta, _ = refiner(P, st, x_prev)
-        Y[k], _ = select(s_b[k] + delta[k], sample, u[k], T)
+        Y[k], _ = select(s_b[k] + delta[k], sample, u[k], T, top_k, top_p)
     return Y
 
 
-def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u, T: float = 1.0):
+def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u, T: float = 1.0,
+              top_k: int = 0, top_p: float = 1.0):
     """One Jacobi pass from a given iterate: (new ids, margins, logits).
 
     Used to check a device trajectory decision by decision.
@@ -396,7 +434,7 @@ def pass_from(P: Params, s_b, h_b, anchor: int, Y_prev, sample: bool, u, T: floa
     x_prev = np.concatenate([[anchor], np.asarray(Y_prev, dtype=np.int64)[:-1]])
     delta, _ = refiner(P, st, x_prev)
     l = s_b + delta
-    sel = [select(l[k], sample, u[k], T) for k in range(B)]
+    sel = [select(l[k], sample, u[k], T, top_k, top_p) for k in range(B)]
     return (np.array([t for t, _ in sel], dtype=np.int64),
             np.array([m for _, m in sel]), l)
 
@@ -426,12 +464,15 @@ class Verified:
     resample_margin: float
 
 
-def verify_sample(q_logits, ids, p_logits, r_accept, u_res, T: float = 1.0) -> Verified:
+def verify_sample(q_logits, ids, p_logits, r_accept, u_res, T: float = 1.0, top_k: int = 0,
+                  top_p: float = 1.0) -> Verified:
     """Speculative accept / reject of a sampled block (section 3.1).
 
     For k = 1..B: accept y_k iff r_k * q_k(y_k) <= p_k(y_k), where q_k is the
     refined distribution the draft token was sampled from and p_k the target
-    distribution after the same prefix, both at temperature T.  At the first
+    distribution after the same prefix, both at temperature T and truncated by
+    the same top_k / top_p (so the emitted tokens follow the truncated target
+    distribution).  At the first
     rejection the next token is an inverse-CDF sample (at u_res) of
     max(0, p_k - q_k), or of p_k if that residual has no mass.  If all B are
     accepted the bonus token is sampled from p_{B+1}.
@@ -439,18 +480,19 @@ def verify_sample(q_logits, ids, p_logits, r_accept, u_res, T: float = 1.0) -> V
     B = len(ids)
     am = []
     for k in range(B):
-        q = softmax(q_logits[k], T)
-        p = softmax(p_logits[k], T)
+        q = softmax(q_logits[k], T, top_k, top_p)
+        p = softmax(p_logits[k], T, top_k, top_p)
         y = int(ids[k])
         rq = float(r_accept[k]) * q[y]
-        am.append(abs(rq - p[y]) / max(p[y], rq))
+        den = max(p[y], rq)
+        am.append(abs(rq - p[y]) / den if den > 0 else 0.0)   # 0 = 0: an exact tie
         if not rq <= p[y]:
             res = np.maximum(p - q, 0.0)
             if not res.sum() > 0:
                 res = p
             t, m = inverse_cdf(res, u_res)
             return Verified(n=k, next=t, accept_margins=np.array(am), resample_margin=m)
-    t, m = inverse_cdf(softmax(p_logits[B], T), u_res)
+    t, m = inverse_cdf(softmax(p_logits[B], T, top_k, top_p), u_res)
     return Verified(n=B, next=t, accept_margins=np.array(am), resample_margin=m)
 
 
@@ -466,9 +508,11 @@ class BatchResult:
 
 
 def refine_batch(P: Params, h, anchor, temp, u_draft, K: int, seed_ids=None,
-                 seqs=None, early_exit: bool = True, temperature=None) -> BatchResult:
+                 seqs=None, early_exit: bool = True, temperature=None, top_k=None,
+                 top_p=None) -> BatchResult:
     """Run Algorithm 1 on the chosen sequences of a batch (default: all);
-    sampled sequences use temperature[b] (1 when None)."""
+    sampled sequences use temperature[b] (1 when None) and the truncations
+    top_k[b], top_p[b] (none when None)."""
     bsz, B, H = h.shape
     seqs = list(range(bsz)) if seqs is None else list(seqs)
     s = base_logits(P.W_lm, h[seqs].reshape(len(seqs) * B, H)).reshape(len(seqs), B, -1)
@@ -478,5 +522,7 @@ def refine_batch(P: Params, h, anchor, temp, u_draft, K: int, seed_ids=None,
             P, s[i], h[b], int(anchor[b]),
             seed=None if seed_ids is None else seed_ids[b],
             sample=bool(temp[b]), u=u_draft[b], K=K, early_exit=early_exit,
-            T=1.0 if temperature is None else float(temperature[b])))
+            T=1.0 if temperature is None else float(temperature[b]),
+            top_k=0 if top_k is None else int(top_k[b]),
+            top_p=1.0 if top_p is None else float(top_p[b])))
     return out

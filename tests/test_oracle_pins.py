@@ -392,14 +392,17 @@ def _cells(probs):
     return [(c[v], c[v + 1]) for v in range(len(probs)) if c[v + 1] > c[v]]
 
 
-def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0):
+def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0, top_k=0, top_p=1.0, target=None):
     """Law of the first m emitted tokens of one SD round + target continuation.
 
     Enumerates every cell of (u_draft, r_accept, u_res) exactly and evaluates
-    the oracle at the cell's midpoint.  ``table[prefix]`` are target logits.
+    the oracle at the cell's midpoint.  ``table[prefix]`` are target logits;
+    ``target(logits)`` is the target distribution (default softmax(l / T)).
     """
     law = {}
-    p_of = lambda pre: scipy.special.softmax(table[tuple(pre)] / T)
+    if target is None:
+        target = lambda l: scipy.special.softmax(l / T)
+    p_of = lambda pre: target(table[tuple(pre)])
 
     def cont(prefix, prob):
         if len(prefix) >= m:
@@ -416,13 +419,15 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0):
             yield np.array(u_pre), prob
             return
         u_try = np.array(u_pre + [0.5] + [0.5] * (B - k - 1))
-        res = O.refine_block(P, s, h, anchor, sample=True, u=u_try, K=B, T=T)
-        q = O.softmax(res.logits[k], T)
+        res = O.refine_block(P, s, h, anchor, sample=True, u=u_try, K=B, T=T, top_k=top_k,
+                             top_p=top_p)
+        q = O.softmax(res.logits[k], T, top_k, top_p)
         for lo, hi in _cells(q):
             yield from draft_cells(k + 1, u_pre + [(lo + hi) / 2], prob * (hi - lo))
 
     for u, pu in draft_cells(0, [], 1.0):
-        res = O.refine_block(P, s, h, anchor, sample=True, u=u, K=B, T=T)
+        res = O.refine_block(P, s, h, anchor, sample=True, u=u, K=B, T=T, top_k=top_k,
+                             top_p=top_p)
         y = [int(t) for t in res.ids]
         plog = np.stack([table[tuple(y[:k])] for k in range(B + 1)])
 
@@ -431,10 +436,11 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0):
             if k == B:
                 pb = p_of(y)
                 for lo, hi in _cells(pb):
-                    v = O.verify_sample(res.logits, y, plog, r_pre + [0.5] * (B - k), (lo + hi) / 2, T)
+                    v = O.verify_sample(res.logits, y, plog, r_pre + [0.5] * (B - k), (lo + hi) / 2, T,
+                                        top_k, top_p)
                     cont(y[:v.n] + [v.next], prob * (hi - lo))
                 return
-            q = O.softmax(res.logits[k], T)
+            q = O.softmax(res.logits[k], T, top_k, top_p)
             p = p_of(y[:k])
             a = min(1.0, p[y[k]] / q[y[k]])
             branch(k + 1, r_pre + [a / 2], prob * a)                  # accept cell
@@ -443,7 +449,7 @@ def _exact_sd_law(P, h, s, anchor, table, B, V, m, T=1.0):
                 resid = np.maximum(p - q, 0.0)
                 resid = resid / resid.sum()
                 for lo, hi in _cells(resid):
-                    v = O.verify_sample(res.logits, y, plog, rr, (lo + hi) / 2, T)
+                    v = O.verify_sample(res.logits, y, plog, rr, (lo + hi) / 2, T, top_k, top_p)
                     assert v.n == k
                     cont(y[:k] + [v.next], prob * (1 - a) * (hi - lo))
 
