@@ -56,6 +56,7 @@ typedef enum { XP_F32 = 0, XP_BF16 = 1 } xp_dtype;
 /* bits of the device error word */
 #define XP_DEVERR_TOKEN 1u  /* a token id outside [0, V) was read and replaced by 0 */
 #define XP_DEVERR_TEMPERATURE 2u  /* a sampled row's temperature was not finite and > 0; 1 was used */
+#define XP_DEVERR_FILTER 4u       /* a sampled row's top_k < 0 or top_p <= 0 (or NaN); not applied */
 
 typedef struct xp_handle xp_handle;
 
@@ -139,6 +140,18 @@ const char* xp_status_string(xp_status s);
  *              sequence: it samples softmax(l / T) (greedy rows ignore it);
  *              NULL = 1 for every sampled row.  A value that is not finite and
  *              positive is replaced by 1 and sets XP_DEVERR_TEMPERATURE.
+ *   top_k      [batch] int32 or NULL; top_p [batch] float or NULL: truncated
+ *              sampling of each sampled sequence (seed, every pass, and the
+ *              verification that follows): top-k keeps the tokens whose
+ *              scaled logit l / T is at least the k-th largest (ties with it
+ *              stay); top-p then keeps, of those ordered by logit descending
+ *              (ties: lower index first), the shortest prefix whose softmax
+ *              mass reaches p of theirs; sampling is from the kept tokens,
+ *              renormalised.  k = 0 or k >= V and p >= 1 mean none; k < 0,
+ *              p <= 0 or NaN set XP_DEVERR_FILTER and mean none.  Greedy rows
+ *              ignore both.  Requires temp.  With either array given, every
+ *              pass also writes its logits [batch][B][V] to the workspace
+ *              (the truncation needs the whole row).
  *   u_draft    [batch][B] float in [0,1), required iff temp != NULL: the uniform of
  *              each position; a sampled position takes the smallest v whose
  *              cumulative softmax mass exceeds u (fixed across passes)
@@ -157,6 +170,7 @@ xp_status xp_refine_block(xp_handle* h, int32_t batch,
                           const void* hidden, const int32_t* anchor,
                           const int32_t* seed_ids, const uint8_t* temp,
                           const float* temperature,
+                          const int32_t* top_k, const float* top_p,
                           const float* u_draft, int32_t K, uint32_t flags,
                           int32_t* out_ids, int32_t* out_iters,
                           float* out_logits, int32_t* out_traj, void* stream);
@@ -180,7 +194,9 @@ xp_status xp_refine_block(xp_handle* h, int32_t batch,
  * Greedy rows: n = longest prefix with y_i = t_i, next = t_{n+1}.
  * Sampled rows: accept y_k iff r_k q_k(y_k) <= p_k(y_k), q_k the refined
  * distribution of refine's last pass and p_k = softmax(target logits k / T),
- * T the row's temperature given to that refine (section 3.1 at T > 0); at the
+ * T the row's temperature given to that refine (section 3.1 at T > 0), both
+ * truncated by that refine's top_k / top_p (so the emitted tokens follow the
+ * truncated target distribution); at the
  * first rejection next is the inverse-CDF sample at u_resample of max(0, p_k - q_k)
  * (of p_k if that has no mass); if all are accepted next samples p_{B+1}.
  */

@@ -161,6 +161,13 @@ extern "C" xp_status xp_create(const xp_weights* w, int32_t max_batch, xp_handle
       {(void**)&ws.vmass, (size_t)h->read_units * max_batch * 16},
       {(void**)&ws.vpart,
        (size_t)max_batch * (w->B + 1) * ((w->V + kVChunk - 1) / kVChunk) * 16},
+      {(void**)&ws.lf, Mmax * w->V * 4},
+      {(void**)&ws.fst, Mmax * sizeof(FState)},
+      {(void**)&ws.tst, (size_t)max_batch * (w->B + 1) * sizeof(FState)},
+      {(void**)&ws.filt, (size_t)max_batch},
+      {(void**)&ws.temp_nf, (size_t)max_batch},
+      {(void**)&ws.fk, (size_t)max_batch * 4},
+      {(void**)&ws.fp, (size_t)max_batch * 4},
   };
   size_t total = 0;
   for (auto& s : sl) total += align_up(s.bytes, 256);
@@ -284,6 +291,7 @@ extern "C" xp_status xp_timing_read(xp_handle* h, float* ms_total, int32_t* pair
 extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hidden,
                                      const int32_t* anchor, const int32_t* seed_ids,
                                      const uint8_t* temp, const float* temperature,
+                                     const int32_t* top_k, const float* top_p,
                                      const float* u_draft, int32_t K,
                                      uint32_t flags, int32_t* out_ids, int32_t* out_iters,
                                      float* out_logits, int32_t* out_traj, void* stream) {
@@ -296,6 +304,8 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
   if (flags & ~(XP_EARLY_EXIT | XP_WRITE_LOGITS))
     return fail(h, XP_EINVAL, "unknown flag bits 0x%x", flags);
   if (temp && !u_draft) return fail(h, XP_EINVAL, "u_draft is required when temp is given");
+  if ((top_k || top_p) && !temp)
+    return fail(h, XP_EINVAL, "top_k / top_p apply to sampled rows: temp is required");
   if ((flags & XP_WRITE_LOGITS) && !out_logits)
     return fail(h, XP_EINVAL, "XP_WRITE_LOGITS needs out_logits");
   if (!(flags & XP_WRITE_LOGITS) && out_logits)
@@ -303,30 +313,35 @@ extern "C" xp_status xp_refine_block(xp_handle* h, int32_t batch, const void* hi
   hipStream_t st = (hipStream_t)stream;
   h->state_valid = false;
   h->call_tempered = temp != nullptr && temperature != nullptr;
+  const bool filtering = temp != nullptr && (top_k != nullptr || top_p != nullptr);
   // All-greedy batches run the selection of pass j-1, Fuse, Mix and the first
   // Trans product of pass j as one kernel; the others use separate kernels.
   XP_TIMED(XP_STAGE_PREP, launch_prep(h, batch, hidden, temp, temperature, st));
+  if (filtering) XP_TIMED(XP_STAGE_PREP, launch_filter_params(h, batch, temp, top_k, top_p, st));
   XP_TIMED(XP_STAGE_LMHEAD, launch_lmhead(h, batch * h->B, hidden, temp, st));
   const bool fused = K > 0 && pass_fused_ok(h, temp);
   if (!fused)
     XP_TIMED(XP_STAGE_SELECT,
              launch_select(h, batch, -1, K, flags, seed_ids, temp, u_draft, out_traj,
-                           K == 0 ? out_ids : nullptr, K == 0 ? out_iters : nullptr, st));
+                           K == 0 ? out_ids : nullptr, K == 0 ? out_iters : nullptr, st,
+                           filtering));
   for (int j = 0; j < K; ++j) {
     if (fused) XP_TIMED(XP_STAGE_RSPACE, launch_pass(h, batch, j, flags, seed_ids, anchor, out_traj, st));
     XP_TIMED(XP_STAGE_RSPACE, launch_rspace(h, batch, j, flags, anchor, !fused, st));
-    XP_TIMED(XP_STAGE_READ, launch_read(h, batch, j, flags, temp,
-                                        (flags & XP_WRITE_LOGITS) ? out_logits : nullptr, st));
+    float* lout = filtering ? h->ws.lf : ((flags & XP_WRITE_LOGITS) ? out_logits : nullptr);
+    XP_TIMED(XP_STAGE_READ, launch_read(h, batch, j, flags, temp, lout, st));
     const bool lastp = j == K - 1;
     if (!fused || lastp)
       XP_TIMED(XP_STAGE_SELECT,
                launch_select(h, batch, j, K, flags, nullptr, temp, u_draft, out_traj,
-                             lastp ? out_ids : nullptr, lastp ? out_iters : nullptr, st));
+                             lastp ? out_ids : nullptr, lastp ? out_iters : nullptr, st,
+                             filtering));
   }
-  XP_LAUNCH(launch_finish(h, batch, K, flags, out_ids, out_iters, out_logits, st));
+  XP_LAUNCH(launch_finish(h, batch, K, flags, out_ids, out_iters, out_logits, st, filtering));
   h->last_batch = batch;
   h->state_k0 = (K == 0);
   h->state_temp = temp != nullptr;
+  h->state_filtered = filtering;
   h->state_valid = true;
   return XP_OK;
 }

@@ -17,6 +17,16 @@ constexpr int kLmWaves = 16;    // A1: waves per workgroup, each owning H/16 of 
 constexpr int kReadWaves = 8;   // A7: waves per workgroup, each streaming its own tiles
 constexpr int kMaxK = 64;
 
+// Truncation state of one row (xp_filter.hip): token v is kept iff
+// key(x_v) >= tk and (key(x_v) > tp or (key(x_v) == tp and v <= pidx)), key()
+// the order-preserving image of the scaled logit; m = max x, Z = kept mass.
+struct FState {
+  float m;
+  uint32_t tk, tp;
+  int32_t pidx;
+  double Z;
+};
+
 struct Workspace {
   float* s = nullptr;         // base logits s_k, tile-major (s_index), Mmax x ldS floats
   float* T = nullptr;         // [V][r]        token table W_e W_in[:, 2r:3r]^T
@@ -41,6 +51,14 @@ struct Workspace {
   int32_t* vpos = nullptr;    // [max_batch][2] rejected position (or B), state
   double* vmass = nullptr;    // [max units][max_batch] residual / bonus mass per unit
   double* vpart = nullptr;    // [max_batch][B+1][vchunks][2] target row (max, sum) per chunk
+  // truncated sampling (top-k / top-p)
+  float* lf = nullptr;        // [Mmax][V]     logits of the current pass, row-major
+  FState* fst = nullptr;      // [Mmax]        truncation state of each draft row (last pass)
+  FState* tst = nullptr;      // [max_batch][B+1] truncation state of each target row
+  uint8_t* filt = nullptr;    // [max_batch]   the row samples with truncation
+  uint8_t* temp_nf = nullptr; // [max_batch]   the row samples without truncation
+  int32_t* fk = nullptr;      // [max_batch]   effective top-k (0: none)
+  float* fp = nullptr;        // [max_batch]   effective top-p (1: none)
 };
 
 // Target rows are reduced in chunks of kVChunk entries (16 per thread).
@@ -72,6 +90,7 @@ struct xp_handle {
   bool state_k0 = false;       // last refine ran K = 0 passes (q = softmax(s))
   bool state_temp = false;     // last refine was given sampling flags
   bool call_tempered = false;  // the current refine has sampled rows and a temperature array
+  bool state_filtered = false; // last refine was given top-k / top-p arrays
   std::string err;
   xp_timing_state tm;
 };
@@ -86,7 +105,15 @@ hipError_t launch_lmhead(xp_handle* h, int M, const void* hidden, const uint8_t*
 hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
                          const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
                          int32_t* out_traj, int32_t* out_ids, int32_t* out_iters,
-                         hipStream_t st);
+                         hipStream_t st, bool filtering);
+// truncated sampling (xp_filter.hip)
+hipError_t launch_filter_params(xp_handle* h, int batch, const uint8_t* temp, const int32_t* top_k,
+                                const float* top_p, hipStream_t st);
+hipError_t launch_fsample(xp_handle* h, int batch, int pass, uint32_t flags,
+                          const int32_t* seed_ids, const float* u_draft, hipStream_t st);
+hipError_t launch_vfilter(xp_handle* h, int batch, const int32_t* draft, const float* tl,
+                          const float* racc, const float* ures, int32_t* out_n, int32_t* out_next,
+                          hipStream_t st);
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
@@ -106,7 +133,7 @@ int prep_ksp(int H);
 hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
                        float* out_logits, hipStream_t st);
 hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,
-                         int32_t* out_iters, float* out_logits, hipStream_t st);
+                         int32_t* out_iters, float* out_logits, hipStream_t st, bool filtering);
 hipError_t launch_verify(xp_handle* h, int batch, const int32_t* draft_ids, const uint8_t* temp,
                          const int32_t* target_ids, const float* target_logits,
                          const float* r_accept, const float* u_res, int32_t* out_n,

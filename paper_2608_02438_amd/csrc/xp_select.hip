@@ -291,7 +291,7 @@ __global__ void k_copy_logits(int M, int V, const float* __restrict__ S,
 hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flags,
                          const int32_t* seed_ids, const uint8_t* temp, const float* u_draft,
                          int32_t* out_traj, int32_t* out_ids, int32_t* out_iters,
-                         hipStream_t st) {
+                         hipStream_t st, bool filtering) {
   const int M = batch * h->B;
   const int mode = pass < 0 ? 0 : 1;
   int32_t* Yprev = h->ws.Y[(pass + 2) % 2];      // pass j reads Y[j % 2]
@@ -301,15 +301,21 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
   const int U = mode == 0 ? h->lm_units_cur : h->read_units;
   const int early = (flags & XP_EARLY_EXIT) ? 1 : 0;
   if (temp) {
+    // rows that truncate are sampled by k_fsample; k_sample takes the others
+    const uint8_t* tsmp = filtering ? h->ws.temp_nf : temp;
+    if (filtering) {
+      const hipError_t e = launch_fsample(h, batch, pass, flags, seed_ids, u_draft, st);
+      if (e != hipSuccess) return e;
+    }
     if (h->dtype == XP_BF16)
       hipLaunchKernelGGL((k_sample<uint16_t>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const uint16_t*)h->W_r, (const uint16_t*)h->ws.z,
-                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
+                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
                          Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
     else
       hipLaunchKernelGGL((k_sample<float>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
-                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, temp, u_draft,
+                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
                          Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
   }
   if (h->dtype == XP_BF16)
@@ -330,13 +336,18 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
 }
 
 hipError_t launch_finish(xp_handle* h, int batch, int K, uint32_t flags, int32_t* out_ids,
-                         int32_t* out_iters, float* out_logits, hipStream_t st) {
+                         int32_t* out_iters, float* out_logits, hipStream_t st, bool filtering) {
   (void)out_ids;
   (void)out_iters;
   const int M = batch * h->B;
   if (K == 0 && (flags & XP_WRITE_LOGITS) && out_logits)
     hipLaunchKernelGGL(k_copy_logits, dim3(1024), dim3(256), 0, st, M, h->V, h->ws.s,
                        out_logits);
+  // with truncation every pass writes its logits to the workspace row buffer
+  // (the last executed pass's stay there): copy them out
+  if (K > 0 && filtering && (flags & XP_WRITE_LOGITS) && out_logits)
+    return hipMemcpyAsync(out_logits, h->ws.lf, (size_t)M * h->V * sizeof(float),
+                          hipMemcpyDeviceToDevice, st);
   return hipGetLastError();
 }
 

@@ -103,15 +103,18 @@ __device__ float refined_logit(int with_read, const float* __restrict__ S, int M
 }
 
 // One wave per sequence: accept scan.  vpos[b] = rejected position, or B.
+// Rows marked in `skip` (truncated sampling: k_vfaccept) are left alone.
 template <typename T>
 __global__ __launch_bounds__(64) void k_vaccept(
     int B, int V, int M, int with_read, const int32_t* __restrict__ draft,
-    const uint8_t* __restrict__ temp, const int32_t* __restrict__ tids,
+    const uint8_t* __restrict__ temp, const uint8_t* __restrict__ skip,
+    const int32_t* __restrict__ tids,
     const float* __restrict__ tl, const float* __restrict__ racc, const float* __restrict__ S,
     int Ms, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
     const double* __restrict__ lseT, int32_t* __restrict__ vpos, int32_t* __restrict__ out_n,
     int32_t* __restrict__ out_next, uint32_t* __restrict__ err, const float* __restrict__ invT) {
   const int b = blockIdx.x, lane = threadIdx.x;
+  if (skip != nullptr && skip[b] != 0) return;
   const bool sample = temp != nullptr && temp[b] != 0;
   int bad = 0;
   if (!sample) {
@@ -372,6 +375,10 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
                            const float* ures, int32_t* out_n, int32_t* out_next, hipStream_t st) {
   const int M = batch * h->B;
   const int with_read = h->state_k0 ? 0 : 1;
+  // truncated rows are verified by launch_vfilter; these kernels take the others
+  const bool filtering = temp != nullptr && h->state_filtered;
+  const uint8_t* skip = filtering ? h->ws.filt : nullptr;
+  if (filtering) temp = h->ws.temp_nf;
   if (temp) {
     const int nc = (h->V + kVChunk - 1) / kVChunk;
     hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1, batch), dim3(256), 0, st, tl, h->B,
@@ -381,7 +388,7 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
                        h->ws.vpart, h->ws.vstat);
   }
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
-                     draft, temp, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
+                     draft, temp, skip, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
                      (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
                      h->ws.err, h->ws.invT);
   if (temp) {
@@ -394,6 +401,11 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
                        with_read, h->ntiles, h->read_units, temp, h->ws.vpos, tl, h->ws.s,
                        M, (const T*)h->W_r, (const T*)h->ws.z, h->ws.lse, h->ws.vstat,
                        h->ws.vmass, ures, out_next, h->ws.invT);
+  }
+  if (filtering) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_vfilter(h, batch, draft, tl, racc, ures, out_n, out_next, st);
   }
   return hipGetLastError();
 }

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libxpress.s
 XP_OK, XP_EINVAL, XP_EUNSUPPORTED, XP_EHIP, XP_ENOMEM = 0, -1, -2, -3, -4
 XP_F32, XP_BF16 = 0, 1
 XP_EARLY_EXIT, XP_WRITE_LOGITS = 1, 2
-XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE = 1, 2
+XP_DEVERR_TOKEN, XP_DEVERR_TEMPERATURE, XP_DEVERR_FILTER = 1, 2, 4
 
 EXPORTS = ("xp_create", "xp_destroy", "xp_last_error", "xp_status_string",
            "xp_refine_block", "xp_verify_block", "xp_device_errors", "xp_timing_enable",
@@ -71,7 +71,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     L.xp_last_error.restype = ctypes.c_char_p
     L.xp_status_string.argtypes = [i32]
     L.xp_status_string.restype = ctypes.c_char_p
-    L.xp_refine_block.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, i32, u32, vp, vp, vp, vp, vp]
+    L.xp_refine_block.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, i32, u32, vp, vp, vp,
+                                  vp, vp]
     L.xp_refine_block.restype = i32
     L.xp_verify_block.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.xp_verify_block.restype = i32
@@ -180,7 +181,7 @@ class Refiner:
     def refine_block(self, hidden, anchor, seed_ids=None, temp=None, u_draft=None, K: int = 6,
                      early_exit: bool = False, write_logits: bool = False,
                      want_traj: bool = False, out: Optional[RefineOut] = None,
-                     stream=None, temperature=None) -> RefineOut:
+                     stream=None, temperature=None, top_k=None, top_p=None) -> RefineOut:
         import torch
         batch = hidden.shape[0]
         if (tuple(hidden.shape) != (batch, self.B, self.H) or hidden.dtype != self.tdtype
@@ -189,7 +190,8 @@ class Refiner:
                              f"{self.tdtype} tensor on {self.device}")
         for name, t, dt in (("anchor", anchor, torch.int32), ("seed_ids", seed_ids, torch.int32),
                             ("temp", temp, torch.uint8), ("u_draft", u_draft, torch.float32),
-                            ("temperature", temperature, torch.float32)):
+                            ("temperature", temperature, torch.float32),
+                            ("top_k", top_k, torch.int32), ("top_p", top_p, torch.float32)):
             if t is not None and (t.dtype != dt or not t.is_contiguous() or t.device != self.device):
                 raise ValueError(f"{name}: expected a contiguous {dt} tensor on {self.device}")
         if out is None:
@@ -204,7 +206,8 @@ class Refiner:
         flags = (XP_EARLY_EXIT if early_exit else 0) | (XP_WRITE_LOGITS if write_logits else 0)
         s = self._L.xp_refine_block(
             self._h, batch, _ptr(hidden), _ptr(anchor), _ptr(seed_ids), _ptr(temp),
-            _ptr(temperature), _ptr(u_draft), K, flags, _ptr(out.ids), _ptr(out.iters),
+            _ptr(temperature), _ptr(top_k), _ptr(top_p), _ptr(u_draft), K, flags, _ptr(out.ids),
+            _ptr(out.iters),
             _ptr(out.logits) if write_logits else None, _ptr(out.traj), _stream(stream))
         self._check(s)
         return out

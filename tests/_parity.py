@@ -54,13 +54,24 @@ class Problem:
     inp: synth.Inputs
     seed_given: bool
     tau: np.ndarray | None = None       # [batch] float32 temperatures (None: 1)
+    top_k: np.ndarray | None = None     # [batch] int32 top-k (None: no truncation)
+    top_p: np.ndarray | None = None     # [batch] float32 top-p (None: no truncation)
 
     def T(self, b) -> float:
         return 1.0 if self.tau is None else float(self.tau[b])
 
+    def filt(self, b):
+        """(top_k, top_p) of sequence b as the device applies them: k outside
+        [1, V) and p outside (0, 1) mean no truncation."""
+        k = 0 if self.top_k is None else int(self.top_k[b])
+        p = 1.0 if self.top_p is None else float(np.float32(self.top_p[b]))
+        k = k if 0 < k < self.V else 0
+        p = p if 0.0 < p < 1.0 else 1.0
+        return k, p
+
 
 def custom_problem(dtype, H, V, B, batch, K, sigmas=None, temp="greedy", seed=0,
-                   seed_given=False, h_sigma=1.0, index=500, tau=None):
+                   seed_given=False, h_sigma=1.0, index=500, tau=None, top_k=None, top_p=None):
     """A problem with per-matrix weight scales (stress trajectories, ragged V)."""
     w = synth.scaled(synth.configs.QWEN_B1, index=index + seed, dtype=dtype, H=H, V=V, B=B,
                      batch=batch, K=K, temp=temp, h_sigma=h_sigma,
@@ -76,7 +87,12 @@ def custom_problem(dtype, H, V, B, batch, K, sigmas=None, temp="greedy", seed=0,
             f[:, ~keep] = 0.0
         weights[n] = gen.f32_to_bf16_bits(f) if dtype == "bf16" else f
     inp = synth.make_inputs(w)
-    return Problem(dtype, H, 256, V, B, batch, K, weights, inp, seed_given, temperatures(tau, batch))
+    return Problem(dtype, H, 256, V, B, batch, K, weights, inp, seed_given, temperatures(tau, batch),
+                   _per_seq(top_k, batch, np.int32), _per_seq(top_p, batch, np.float32))
+
+
+def _per_seq(v, batch, dt):
+    return None if v is None else np.broadcast_to(np.asarray(v, dtype=dt), (batch,)).copy()
 
 
 def temperatures(tau, batch):
@@ -86,11 +102,13 @@ def temperatures(tau, batch):
     return np.broadcast_to(np.asarray(tau, dtype=np.float32), (batch,)).copy()
 
 
-def workload_problem(wl, batch=None, tau=None):
+def workload_problem(wl, batch=None, tau=None, top_k=None, top_p=None):
     weights = synth.make_weights(wl)
     inp = synth.make_inputs(wl, batch=batch)
-    return Problem(wl.dtype, wl.H, wl.r, wl.V, wl.B, batch or wl.batch, wl.K, weights, inp,
-                   wl.seed_mode == "given", temperatures(tau, batch or wl.batch))
+    n = batch or wl.batch
+    return Problem(wl.dtype, wl.H, wl.r, wl.V, wl.B, n, wl.K, weights, inp,
+                   wl.seed_mode == "given", temperatures(tau, n), _per_seq(top_k, n, np.int32),
+                   _per_seq(top_p, n, np.float32))
 
 
 # ---------------------------------------------------------------------------
@@ -116,6 +134,8 @@ def upload(prob: Problem):
     d["u_res"] = device_tensor(i.u_res)
     d["target_logits"] = device_tensor(i.target_logits) if sample_rows else None
     d["temperature"] = device_tensor(prob.tau) if prob.tau is not None else None
+    d["top_k"] = device_tensor(prob.top_k) if prob.top_k is not None else None
+    d["top_p"] = device_tensor(prob.top_p) if prob.top_p is not None else None
     torch.cuda.synchronize()
     return d
 
@@ -132,7 +152,8 @@ def run_device(ref, prob: Problem, dev: dict, K=None, early_exit=False, write_lo
     out = ref.refine_block(dev["hidden"], dev["anchor"], seed_ids=dev["seed_ids"],
                            temp=dev["temp"], u_draft=dev["u_draft"], K=K,
                            early_exit=early_exit, write_logits=write_logits, want_traj=True,
-                           temperature=dev.get("temperature"))
+                           temperature=dev.get("temperature"), top_k=dev.get("top_k"),
+                           top_p=dev.get("top_p"))
     torch.cuda.synchronize()
     return DeviceRun(ids=out.ids.cpu().numpy(), iters=out.iters.cpu().numpy(),
                      traj=out.traj.cpu().numpy(),
@@ -210,24 +231,63 @@ def tempered_bound(l, E, T):
     return E / T + 2 * U32 * np.abs(l) / T
 
 
-def _decision_ok(l, E, y_dev, sample, u, T=1.0):
-    y_o, _ = O.select(l, sample, u, T)
+def filter_boundary(l, E, T, k, p):
+    """Tokens at the truncation boundary whose membership the device error
+    could flip (empty when the boundary is clear): top-k, the k-th and
+    (k+1)-th largest scaled logits closer than twice the bound; top-p, the
+    last kept and first dropped token when the mass before the first dropped
+    one lies within the bound's relative effect (plus the device's 2^-44
+    fixed-point mass units) of p times the top-k mass, or their logits are
+    closer than twice the bound."""
+    x = np.asarray(l, dtype=np.float64) / T
+    ex = tempered_bound(l, E, T).max()
+    V = x.shape[0]
+    out = set()
+    keep_k = np.ones(V, dtype=bool)
+    if 0 < k < V:
+        order = np.argsort(-x, kind="stable")
+        a, b = order[k - 1], order[k]
+        if x[a] - x[b] <= 4 * ex:
+            out |= {int(v) for v in np.nonzero(np.abs(x - x[a]) <= 4 * ex)[0]}
+        keep_k = x >= x[a]
+    if p < 1.0:
+        w = O.softmax_weights(l, T) * keep_k
+        idx = np.nonzero(keep_k)[0]
+        order = idx[np.lexsort((idx, -x[idx]))]
+        before = np.concatenate([[0.0], np.cumsum(w[order])[:-1]])
+        Zk = w.sum()
+        n = int(np.sum(before < p * Zk))              # tokens kept
+        if n < len(order):
+            rel = np.expm1(4 * ex) + V * 2.0 ** -44 + 1e-12
+            last, first_out = order[n - 1], order[n]
+            if (abs(before[n] - p * Zk) <= rel * Zk
+                    or x[last] - x[first_out] <= 4 * ex):
+                out |= {int(last), int(first_out)}
+    return out
+
+
+def _decision_ok(l, E, y_dev, sample, u, T=1.0, k=0, p=1.0):
+    y_o, _ = O.select(l, sample, u, T, k, p)
     if y_o == y_dev:
         return "exact"
     if not sample:
         ok = (l[y_o] - l[y_dev]) <= E[y_o] + E[y_dev]
     else:
-        w = O.softmax_weights(l, T)
-        C = np.cumsum(w)
-        Z = C[-1]
-        lo = C[y_dev - 1] if y_dev > 0 else 0.0
-        f = np.exp(4 * tempered_bound(l, E, T).max())
-        ok = lo / f <= u * Z <= C[y_dev] * f
+        w = O.filtered_weights(l, T, k, p)
+        if filter_boundary(l, E, T, k, p):
+            # the device's kept set may legitimately differ at the boundary
+            ok = bool(w[y_dev] > 0) or y_dev in filter_boundary(l, E, T, k, p)
+        else:
+            C = np.cumsum(w)
+            Z = C[-1]
+            lo = C[y_dev - 1] if y_dev > 0 else 0.0
+            f = np.exp(4 * tempered_bound(l, E, T).max())
+            ok = w[y_dev] > 0 and lo / f <= u * Z <= C[y_dev] * f
     return "excused" if ok else "wrong"
 
 
 def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits, T=1.0,
-                   abs_bar=None):
+                   abs_bar=None, k=0, p=1.0):
     """Validate one sequence's device trajectory; returns (Tally, final logits, final E).
 
     The final logits must lie within E of the oracle's element by element and,
@@ -236,7 +296,7 @@ def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits,
     B = s_b.shape[0]
     t = Tally(seqs=1)
     ref = O.refine_block(P, s_b, h_b, anchor, seed=seed, sample=sample, u=u, K=K,
-                         early_exit=False, T=T)
+                         early_exit=False, T=T, top_k=k, top_p=p)
     tro = ref.traj_padded(K)
     first = 0 if seed is None else 1
     exact_traj = np.array_equal(tro, traj)
@@ -248,9 +308,9 @@ def check_sequence(P, s_b, h_b, anchor, seed, sample, u, K, traj, iters, logits,
         l_final, E_final = l, E
         if exact_traj:
             continue
-        for k in range(B):
-            r = _decision_ok(l[k], E[k], int(traj[j][k]), sample, float(u[k]), T)
-            assert r != "wrong", f"pass {j} position {k}: device token {traj[j][k]} is not a valid selection"
+        for q in range(B):
+            r = _decision_ok(l[q], E[q], int(traj[j][q]), sample, float(u[q]), T, k, p)
+            assert r != "wrong", f"pass {j} position {q}: device token {traj[j][q]} is not a valid selection"
             t.decisions += 1
             t.exact += r == "exact"
             t.excused += r == "excused"
@@ -290,7 +350,8 @@ def check_refine(prob: Problem, run: DeviceRun, seqs=None, P=None, s=None, abs_b
         t, lf, Ef = check_sequence(P, s[n], i.h[b], int(i.anchor[b]), seed, bool(i.temp[b]),
                                    i.u_draft[b], run.traj.shape[0] - 1, run.traj[:, b],
                                    run.iters[b], None if run.logits is None else run.logits[b],
-                                   prob.T(b), abs_bar=abs_bar)
+                                   prob.T(b), abs_bar=abs_bar, k=prob.filt(b)[0],
+                                   p=prob.filt(b)[1])
         tot.add(t)
         finals[b] = (lf, Ef)
     return tot, finals
@@ -301,7 +362,9 @@ def check_verify(prob: Problem, run: DeviceRun, finals: dict, n_dev, next_dev, t
 
     With |l_device - l| <= E and |lse_device - lse| <= Emax the device's q moves
     by a factor within e^(+-2 Emax); the target p (fp32 logits, fp64 sums on
-    both sides) by at most 1e-6 relative.
+    both sides) by at most 1e-6 relative.  Truncated rows use the truncated
+    q and p, and are also excused where a row's truncation boundary is itself
+    a near-tie.
     """
     i = prob.inp
     excused = 0
@@ -313,19 +376,25 @@ def check_verify(prob: Problem, run: DeviceRun, finals: dict, n_dev, next_dev, t
             continue
         lf, Ef = finals[b]
         T = prob.T(b)
+        fk, fp = prob.filt(b)
         pl = i.target_logits[b].astype(np.float64)
-        v = O.verify_sample(lf, y, pl, i.r_accept[b], float(i.u_res[b]), T)
+        v = O.verify_sample(lf, y, pl, i.r_accept[b], float(i.u_res[b]), T, fk, fp)
         if (int(n_dev[b]), int(next_dev[b])) == (v.n, v.next):
             continue
         k = min(int(n_dev[b]), v.n)
         kq = min(k, prob.B - 1)
         tol = (np.exp(2 * tempered_bound(lf[kq], Ef[kq], T).max()) - 1 + 1e-6
-               + 4 * U32 * np.abs(pl[k]).max() / T)
+               + 4 * U32 * np.abs(pl[k]).max() / T + prob.V * 2.0 ** -44)
+        boundary = bool(filter_boundary(lf[kq], Ef[kq], T, fk, fp)) or bool(
+            filter_boundary(pl[k], 4 * U32 * np.abs(pl[k]), T, fk, fp))
+        if boundary:
+            excused += 1
+            continue
         if int(n_dev[b]) != v.n:
             assert v.accept_margins[k] <= tol, f"seq {b}: accept decision at {k} is not a near-tie"
         else:
-            p = O.softmax(pl[k], T)
-            res = np.maximum(p - O.softmax(lf[k], T), 0.0) if k < prob.B else p
+            p = O.softmax(pl[k], T, fk, fp)
+            res = np.maximum(p - O.softmax(lf[k], T, fk, fp), 0.0) if k < prob.B else p
             if not res.sum() > 0:
                 res = p
             C = np.cumsum(res)

@@ -66,7 +66,8 @@ def test_create_rejects_bad_batch():
 
 def test_calls_on_a_null_handle_are_rejected():
     L = X.load_library()
-    assert L.xp_refine_block(None, 1, 1, 1, None, None, None, None, 6, 0, 1, None, None, None, None) == X.XP_EINVAL
+    assert L.xp_refine_block(None, 1, 1, 1, None, None, None, None, None, None, 6, 0, 1, None, None,
+                             None, None) == X.XP_EINVAL
     assert L.xp_verify_block(None, 1, 1, None, 1, None, None, None, 1, 1, None) == X.XP_EINVAL
     assert L.xp_device_errors(None, None, None) == X.XP_EINVAL
     L.xp_destroy(None)
