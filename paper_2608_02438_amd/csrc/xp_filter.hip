@@ -360,10 +360,10 @@ __global__ __launch_bounds__(kFThreads) void k_fsample(
     const uint8_t* __restrict__ filt, const int32_t* __restrict__ fk, const float* __restrict__ fp,
     const float* __restrict__ invT, const float* __restrict__ u_draft,
     const int32_t* __restrict__ seed_ids, int32_t* __restrict__ Ynew, FState* __restrict__ fst,
-    const int32_t* __restrict__ ctrl, int early_exit) {
+    const int32_t* __restrict__ iters, int early_exit) {
   const int p = blockIdx.x, b = p / B;
   if (!filt[b]) return;
-  if (MODE == 1 && early_exit && ctrl[1] != 0) return;      // the selection keeps Y^(j)
+  if (MODE == 1 && early_exit && iters[b] != 0) return;     // the sequence keeps Y^(j)
   __shared__ FShared sh;
   const float it = invT[b];
   auto x = [&](int v) -> float {
@@ -510,11 +510,11 @@ hipError_t launch_fsample(xp_handle* h, int batch, int pass, uint32_t flags,
   if (pass < 0)
     hipLaunchKernelGGL((k_fsample<0>), dim3(M), dim3(kFThreads), 0, st, h->B, h->V, M, h->ws.s, M,
                        h->ws.lf, h->ws.filt, h->ws.fk, h->ws.fp, h->ws.invT, u_draft, seed_ids,
-                       Ynew, h->ws.fst, h->ws.ctrl, early);
+                       Ynew, h->ws.fst, h->ws.iters, early);
   else
     hipLaunchKernelGGL((k_fsample<1>), dim3(M), dim3(kFThreads), 0, st, h->B, h->V, M, h->ws.s, M,
                        h->ws.lf, h->ws.filt, h->ws.fk, h->ws.fp, h->ws.invT, u_draft, nullptr,
-                       Ynew, h->ws.fst, h->ws.ctrl, early);
+                       Ynew, h->ws.fst, h->ws.iters, early);
   return hipGetLastError();
 }
 

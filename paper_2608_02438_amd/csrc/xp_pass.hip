@@ -39,7 +39,18 @@ __global__ __launch_bounds__(256) void k_pass(
   __shared__ floatx4 red[4][64];
   const int b = blockIdx.x, rt = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, g = lane >> 4, li = lane & 15;
-  const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
+  // early exit: a sequence already at its fixed point keeps its block (the
+  // first workgroup carries it over to the next iterate buffer)
+  const bool skip = mode == 1 && early_exit && iters[b] != 0;
+  if (skip) {
+    if (rt == 0 && tid < B) {
+      const size_t p = (size_t)b * B + tid;
+      const int y = Yprev[p];
+      Ynew[p] = y;
+      if (traj) traj[p] = y;
+    }
+    return;
+  }
 
   // --- every independent load first -----------------------------------------
   const int kk = tid & 15, kkc = kk < B ? kk : B - 1;          // key role: position kk
@@ -102,14 +113,26 @@ __global__ __launch_bounds__(256) void k_pass(
       }
     }
     ys[tid] = y;
-    if (rt == 0 && tid < B) {
-      const size_t p = (size_t)b * B + tid;
-      Ynew[p] = y;
-      if (traj) traj[p] = y;
+    if (tid < B) {
+      if (rt == 0) {
+        const size_t p = (size_t)b * B + tid;
+        Ynew[p] = y;
+        if (traj) traj[p] = y;
+      }
       if (mode == 1 && y != yp) atomicOr(&chg, 1);
     }
   }
   __syncthreads();
+  // --- fixed-point bookkeeping of the selection (Algorithm 1) -----------------
+  // Every workgroup of the sequence sees the same selection: when it has just
+  // reached the fixed point (or had before), the rest of this pass is not
+  // needed under the early exit.
+  const bool now_fixed = mode == 1 && !skip && chg == 0 && it0 == 0;
+  if (rt == 0 && tid == 0 && now_fixed) {
+    iters[b] = pass;                               // the selection of pass `pass - 1`
+    if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
+  }
+  if (skip || (early_exit && now_fixed)) return;   // whole workgroup
 
   // --- Fuse: a_k = Pa_k + T[x_{k-1}] ------------------------------------------
   {
@@ -179,11 +202,6 @@ __global__ __launch_bounds__(256) void k_pass(
       *reinterpret_cast<float4*>(h1 + ((size_t)b * B + li) * r2 + rt * 16 + 4 * g) =
           make_float4(o[0], o[1], o[2], o[3]);
     }
-  }
-  // --- fixed-point bookkeeping of the selection (Algorithm 1) -----------------
-  if (rt == 0 && tid == 0 && mode == 1 && !skip && chg == 0 && it0 == 0) {
-    iters[b] = pass;                               // the selection of pass `pass - 1`
-    if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
   }
 }
 

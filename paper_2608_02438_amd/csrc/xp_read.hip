@@ -247,13 +247,18 @@ constexpr int kRmStages = 4;
 __device__ __forceinline__ int rm_wslot(int r, int c) { return 32 * r + (c ^ r); }
 __device__ __forceinline__ int rm_sslot(int q, int c) { return 4 * q + ((c ^ (q >> 2)) & 3); }
 
-template <int P>
+// EE (early exit): a wave whose positions all belong to sequences at their
+// fixed point is dead: its s loads go to one fixed address (every wave still
+// issues the same number of loads per tile, which the waits count on, and its
+// part of each W_r tile, which the other waves read), and its products,
+// selection partials and outputs are skipped.
+template <int P, bool EE>
 __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     const uint16_t* __restrict__ W, const uint16_t* __restrict__ Z, const float* __restrict__ S,
     int Ms, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B,
     float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done,
-    int nwg, int ny, const float* __restrict__ invT) {
+    int nwg, int ny, const float* __restrict__ invT, const int32_t* __restrict__ iters) {
   static_assert(kReadWaves == 8, "one 1 KB load per wave fills a 16-row tile");
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   using RT = ReadTile<uint16_t>;
@@ -271,22 +276,42 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   const int t0 = unit_tile_lo(u_lo, ntiles, U), n = unit_tile_lo(u_hi, ntiles, U) - t0;
   const int pw = py * (kReadWaves * kTile * P) + wave * (kTile * P);
   __shared__ u32x4 lds[kRmStages * (WSL + SSL)];                // [stage][W tile | s]
+  if (EE) {
+    // early exit: nothing to do when every sequence of the workgroup's
+    // positions is at its fixed point (the flag lives in the first ring
+    // slot, which no load has touched yet)
+    const int P0 = py * (kReadWaves * kTile * P);
+    const int P1 = min(M, P0 + kReadWaves * kTile * P);
+    const int b0 = P0 / B, nb = (P1 - 1) / B - b0 + 1;
+    bool live = false;
+    for (int i = threadIdx.x; i < nb; i += kReadWaves * kWave) live |= iters[b0 + i] == 0;
+    uint32_t* flag = reinterpret_cast<uint32_t*>(&lds[0]);
+    if (threadIdx.x == 0) *flag = 0u;
+    __syncthreads();
+    if (live) *flag = 1u;
+    __syncthreads();
+    const bool any = *flag != 0u;
+    __syncthreads();
+    if (!any) return;                             // whole workgroup
+  }
 
   u32x4 zf[P][NU];
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) RT::load_z(Z, M, pw + kTile * pb, lane, zf[pb]);
   bool act[P], sample[P];
   float pit[P];                                   // sampled rows: softmax(l / T)
-  bool any = false;
+  bool any = false, live = false;
 #pragma unroll
   for (int pb = 0; pb < P; ++pb) {
     const int p = pw + kTile * pb + (lane & 15);
     act[pb] = p < M;
+    if (EE) live = live || (act[pb] && iters[(act[pb] ? p : M - 1) / B] == 0);
     sample[pb] = act[pb] && load_flag(temp, (act[pb] ? p : M - 1) / B, S) != 0;
     pit[pb] = invT[(act[pb] ? p : M - 1) / B];
     any = any || sample[pb];
   }
   const bool any_sample = __ballot(any) != 0;    // wave-uniform
+  const bool wdead = EE && __ballot(live) == 0;   // wave-uniform
   // greedy rows: running maximum and its row (rows arrive in increasing order
   // in every lane, so a strict comparison keeps the lowest index of a tie;
   // -0 == +0 as in the key order).  Other rows start at +inf, which no value
@@ -311,6 +336,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   for (int pb = 0; pb < P; ++pb) {
     const int p = pw + kTile * pb + sq;
     sbase[pb] = S + s_index(p < M ? p : M - 1, 4 * sc, Ms);
+    if (wdead) sbase[pb] = S + 4 * (lane & 3);    // fixed, in cache after the first tile
   }
   auto issue = [&](int j) {
     const int t = t0 + (j < n ? j : n - 1);
@@ -320,7 +346,8 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     lds_dma16(W + (size_t)row * 256 + 8 * wchunk, stage + kWave * wave);
 #pragma unroll
     for (int pb = 0; pb < P; ++pb)
-      lds_dma16(sbase[pb] + (size_t)t * Ms * kTile, stage + WSL + kWave * (P * wave + pb));
+      lds_dma16(sbase[pb] + (wdead ? (size_t)0 : (size_t)t * Ms * kTile),
+                stage + WSL + kWave * (P * wave + pb));
   };
   // (max, sum) of every unit that ends at or before tile boundary tend
   int uc = u_lo, ue = unit_tile_lo(u_lo + 1, ntiles, U);
@@ -336,7 +363,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
             q = stat_merge(q, o);
           }
           const int p = pw + kTile * pb + (lane & 15);
-          if (lane < 16 && sample[pb]) stats[(size_t)p * U + uc] = q;
+          if (lane < 16 && sample[pb] && !wdead) stats[(size_t)p * U + uc] = q;
           st[pb] = stat_empty();
         }
       }
@@ -359,6 +386,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     issue(j + kRmStages - 1);
+    if (wdead) continue;                           // wave-uniform
     const u32x4* stage = lds + (j % kRmStages) * (WSL + SSL);
     u32x4 a[NU];
 #pragma unroll
@@ -417,7 +445,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
 #pragma unroll
     for (int m = 16; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
     const int p = pw + kTile * pb + (lane & 15);
-    if (lane < 16 && act[pb]) keys[(size_t)g * M + p] = best;
+    if (lane < 16 && act[pb] && !wdead) keys[(size_t)g * M + p] = best;
   }
 }
 
@@ -436,27 +464,26 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     grid = dim3((h->read_wgs + 7) / 8 * 8 * ny);
     const uint16_t* Wr = (const uint16_t*)h->W_r;
     const uint16_t* Zb = (const uint16_t*)h->ws.z;
-    switch (P) {
-      case 1:
-        hipLaunchKernelGGL((k_read_multi<1>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
-                           M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
-        break;
-      case 2:
-        hipLaunchKernelGGL((k_read_multi<2>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
-                           M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
-        break;
-      case 3:
-        hipLaunchKernelGGL((k_read_multi<3>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
-                           M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
-        break;
-      default:
-        hipLaunchKernelGGL((k_read_multi<4>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V,
-                           M, h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B,
-                           out_logits, h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT);
+#define XP_RM(PP, EEV)                                                                       \
+  hipLaunchKernelGGL((k_read_multi<PP, EEV>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V, M, \
+                     h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, \
+                     h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT, h->ws.iters)
+    if (skip) {
+      switch (P) {
+        case 1: XP_RM(1, true); break;
+        case 2: XP_RM(2, true); break;
+        case 3: XP_RM(3, true); break;
+        default: XP_RM(4, true);
+      }
+    } else {
+      switch (P) {
+        case 1: XP_RM(1, false); break;
+        case 2: XP_RM(2, false); break;
+        case 3: XP_RM(3, false); break;
+        default: XP_RM(4, false);
+      }
     }
+#undef XP_RM
     return hipGetLastError();
   }
   if (h->dtype == XP_BF16)

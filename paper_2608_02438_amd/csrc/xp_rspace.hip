@@ -205,9 +205,9 @@ template <typename T, int BP>
 __global__ __launch_bounds__(256) void k_fusemix(
     int B, int V, int M, const float* __restrict__ Pa, const float* __restrict__ Ttab,
     const T* __restrict__ Lp, const int32_t* __restrict__ anchor, const int32_t* __restrict__ Y,
-    float* __restrict__ c, uint32_t* __restrict__ err, const int32_t* __restrict__ ctrl,
+    float* __restrict__ c, uint32_t* __restrict__ err, const int32_t* __restrict__ iters,
     int skip_when_done) {
-  if (skip_when_done && ctrl[1]) return;
+  if (skip_when_done && iters[blockIdx.x]) return;    // the sequence is at its fixed point
   constexpr int r = 256;
   constexpr int EPT = BP / 16;                       // positions per thread
   constexpr int NPAIR = BP * (BP - 1) / 2;
@@ -280,9 +280,9 @@ template <typename T, int BP>
 __global__ __launch_bounds__(256) void k_trans1(int B, const T* __restrict__ W1,
                                                 const float* __restrict__ c,
                                                 float* __restrict__ h1,
-                                                const int32_t* __restrict__ ctrl,
+                                                const int32_t* __restrict__ iters,
                                                 int skip_when_done) {
-  if (skip_when_done && ctrl[1]) return;
+  if (skip_when_done && iters[blockIdx.x]) return;    // the sequence is at its fixed point
   constexpr int r = 256, r2 = 512, NPB = BP / 16;
   constexpr bool kBf = sizeof(T) == 2;
   const int b = blockIdx.x, rt = blockIdx.y;
@@ -359,9 +359,9 @@ template <typename T, int BP>
 __global__ __launch_bounds__(256) void k_trans2(int B, const T* __restrict__ W2,
                                                 const float* __restrict__ c,
                                                 const float* __restrict__ h1, T* __restrict__ z,
-                                                const int32_t* __restrict__ ctrl,
+                                                const int32_t* __restrict__ iters,
                                                 int skip_when_done) {
-  if (skip_when_done && ctrl[1]) return;
+  if (skip_when_done && iters[blockIdx.x]) return;    // the sequence is at its fixed point
   constexpr int r = 256, r2 = 512, NPB = BP / 16;
   constexpr bool kBf = sizeof(T) == 2;
   const int b = blockIdx.x, zt = blockIdx.y;
@@ -476,12 +476,12 @@ static void rspace_t(xp_handle* h, int batch, int pass, int skip, const int32_t*
   if (front) {
     hipLaunchKernelGGL((k_fusemix<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B, h->V, M,
                        h->ws.Pa, h->ws.T, (const T*)h->ws.Lp, anchor, h->ws.Y[pass % 2], h->ws.c,
-                       h->ws.err, h->ws.ctrl, skip);
+                       h->ws.err, h->ws.iters, skip);
     hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
-                       (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.ctrl, skip);
+                       (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.iters, skip);
   }
   hipLaunchKernelGGL((k_trans2<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B,
-                     (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.ctrl, skip);
+                     (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.iters, skip);
 }
 
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,

@@ -53,11 +53,11 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
     const T* __restrict__ W_r, const T* __restrict__ Z, const Stat* __restrict__ stats,
     int ntiles, int U, const int32_t* __restrict__ seed_ids, const uint8_t* __restrict__ temp,
     const float* __restrict__ u_draft, int32_t* __restrict__ Ynew, double* __restrict__ lse,
-    const int32_t* __restrict__ ctrl, int early_exit, const float* __restrict__ invT) {
+    const int32_t* __restrict__ iters, int early_exit, const float* __restrict__ invT) {
   const int p = blockIdx.x;
   if (temp[p / B] == 0) return;
   const float it = invT[p / B];                   // the unit partials hold l / T
-  if (mode == 1 && early_exit && ctrl[1] != 0) return;     // the selection keeps Y^(j)
+  if (mode == 1 && early_exit && iters[p / B] != 0) return;   // the sequence keeps Y^(j)
   const bool pick = !(mode == 0 && seed_ids != nullptr);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ float wmax[kSmpWaves];
@@ -213,7 +213,18 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
   const int b = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ int changed;
-  const bool skip = mode == 1 && early_exit && ctrl[1] != 0;
+  const bool skip = mode == 1 && early_exit && iters[b] != 0;   // at its fixed point
+  if (skip) {                                     // the block carries over
+    for (int k = threadIdx.x; k < B; k += kSelWaves * kWave) {
+      const int p = b * B + k;
+      const int y = Yprev[p];
+      Ynew[p] = y;
+      if (traj) traj[p] = y;
+      if (out_ids) out_ids[p] = y;
+    }
+    if (threadIdx.x == 0 && out_iters) out_iters[b] = iters[b];
+    return;
+  }
   // independent loads first (keys unconditionally: unused ones are harmless)
   uint64_t kv[kSelPPW][kSelKPL];
   int yprev[kSelPPW];
@@ -311,12 +322,12 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
       hipLaunchKernelGGL((k_sample<uint16_t>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const uint16_t*)h->W_r, (const uint16_t*)h->ws.z,
                          h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
-                         Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
+                         Ynew, h->ws.lse, h->ws.iters, early, h->ws.invT);
     else
       hipLaunchKernelGGL((k_sample<float>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
                          h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
                          h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
-                         Ynew, h->ws.lse, h->ws.ctrl, early, h->ws.invT);
+                         Ynew, h->ws.lse, h->ws.iters, early, h->ws.invT);
   }
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,

@@ -368,3 +368,40 @@ def test_qwen3_shape_batch32_greedy(full_sizes, seqs):
 @pytest.mark.parametrize("seqs", _groups(QWEN_B64_MIXED.batch))
 def test_qwen3_shape_batch64_block32_mixed(full_sizes, seqs):
     _full_size_groups(QWEN_B64_MIXED, full_sizes, seqs)
+
+
+@pytest.mark.parametrize("H,V,B,batch,temp", [
+    (512, 2000, 16, 6, "greedy"),      # fused greedy pass, one stream launch per pass
+    (512, 2000, 16, 6, "mixed"),       # separate kernels, sampled rows
+    (512, 1000, 16, 24, "greedy"),     # 384 positions: LM-head GEMM and many-position Read
+    (256, 777, 32, 5, "mixed"),        # blocks of 32
+])
+def test_per_sequence_early_exit_equals_fixed_K(H, V, B, batch, temp):
+    """Algorithm 1 stops each sequence at its own fixed point: with the early
+    exit, a sequence's kernels skip every pass after it converged, while the
+    others go on.  Since a fixed point maps to itself, ids, pass counts,
+    trajectories, final logits and the verification that follows must equal
+    the fixed-K run bit for bit, for every sequence."""
+    import torch
+    _say(f"case: per-sequence early exit, bf16 H={H} V={V} B={B} batch={batch} {temp}")
+    # milder stress weights: the sequences reach their fixed points after
+    # 7 to 28 passes (the oracle's counts), within K = B + 2 (Theorem 1: B)
+    mild = dict(STRESS, W_e=0.25, W_r=0.075)
+    prob = custom_problem("bf16", H=H, V=V, B=B, batch=batch, K=B + 2, sigmas=mild, temp=temp,
+                          seed=91 + batch + B)
+    ref = make_refiner(prob)
+    dev = upload(prob)
+    fixed = run_device(ref, prob, dev)
+    tids = prob.inp.target_ids(fixed.ids)
+    nf, xf = _verify(ref, prob, fixed, dev, tids)
+    early = run_device(ref, prob, dev, early_exit=True)
+    ne, xe = _verify(ref, prob, early, dev, tids)
+    _say(f"  iters={fixed.iters.tolist()}")
+    assert len(set(fixed.iters.tolist())) >= 2, "sequences should converge at different passes"
+    assert fixed.iters.max() < prob.K, "every sequence should converge within K"
+    assert np.array_equal(early.ids, fixed.ids) and np.array_equal(early.iters, fixed.iters)
+    assert np.array_equal(early.traj, fixed.traj)
+    assert np.array_equal(early.logits, fixed.logits)
+    assert np.array_equal(ne, nf) and np.array_equal(xe, xf)
+    tally, _ = check_refine(prob, early)
+    assert tally.exact >= 0.97 * tally.decisions
