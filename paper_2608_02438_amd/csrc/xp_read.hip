@@ -238,7 +238,9 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read(
 // kernel and the sampling rescan (ReadTile), so all of them produce the same
 // fp32 logits.  Outputs have the stream kernel's layout: one key row per
 // workgroup, one (max, sum) per wave unit and position.
-constexpr int kRmStages = 4;
+constexpr int kRmLds = 163840;                   // bytes of LDS the ring may take
+constexpr int kRmMaxStages = 8;
+constexpr int kRmMaxP = 4;                       // position blocks per wave (launch cap)
 
 // W_r tile in LDS: 16 rows x 32 chunks of 16 bytes, chunk c of row r at slot
 // 32 r + (c ^ r); s of 16 positions x 16 rows: chunk c (4 rows) of position q
@@ -275,6 +277,9 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   const int u_lo = g * kReadWaves, u_hi = u_lo + kReadWaves;
   const int t0 = unit_tile_lo(u_lo, ntiles, U), n = unit_tile_lo(u_hi, ntiles, U) - t0;
   const int pw = py * (kReadWaves * kTile * P) + wave * (kTile * P);
+  // as many stages as fit: the deeper the ring, the more tiles are in flight
+  constexpr int NS0 = kRmLds / ((WSL + SSL) * 16);
+  constexpr int kRmStages = NS0 < kRmMaxStages ? NS0 : kRmMaxStages;
   __shared__ u32x4 lds[kRmStages * (WSL + SSL)];                // [stage][W tile | s]
   if (EE) {
     // early exit: nothing to do when every sequence of the workgroup's
@@ -312,6 +317,15 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   }
   const bool any_sample = __ballot(any) != 0;    // wave-uniform
   const bool wdead = EE && __ballot(live) == 0;   // wave-uniform
+  // per position block, wave-uniform: does any lane take the greedy maximum,
+  // any the softmax partials?  (With B a multiple of 16 a block lies in one
+  // sequence and does only one of the two.)
+  bool do_max[P], do_sum[P];
+#pragma unroll
+  for (int pb = 0; pb < P; ++pb) {
+    do_max[pb] = __ballot(act[pb] && !sample[pb]) != 0;
+    do_sum[pb] = __ballot(sample[pb]) != 0;
+  }
   // greedy rows: running maximum and its row (rows arrive in increasing order
   // in every lane, so a strict comparison keeps the lowest index of a tie;
   // -0 == +0 as in the key order).  Other rows start at +inf, which no value
@@ -375,14 +389,14 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   flush_until(t0);                                // units without tiles
 #pragma unroll
   for (int j = 0; j < kRmStages - 1; ++j) issue(j);
-  constexpr int kPend = (kRmStages - 2) * (1 + P); // loads of the two later tiles
-  static_assert(kPend < 16, "vmcnt field");
+  constexpr int kPend = (kRmStages - 2) * (1 + P); // loads of the later tiles
+  static_assert(kPend < 64, "vmcnt field");
   for (int j = 0; j < n; ++j) {
-    // tile j's loads are done once only the two later tiles' are outstanding;
+    // tile j's loads are done once only the later tiles' are outstanding;
     // the barrier then covers every wave's part of stage j, and every wave's
     // reads of the stage that the next issue overwrites (tile j - 1)
     asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt(0x0070 | kPend);
+    __builtin_amdgcn_s_waitcnt(0x0070 | (kPend & 15) | ((kPend >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     issue(j + kRmStages - 1);
@@ -417,13 +431,15 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
 #pragma unroll
     for (int pb = 0; pb < P; ++pb) {
       const floatx4 acc = accs[pb];
+      if (do_max[pb]) {                            // wave-uniform
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool take = acc[i] > bv[pb];
-        bv[pb] = take ? acc[i] : bv[pb];
-        bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
+        for (int i = 0; i < 4; ++i) {
+          const bool take = acc[i] > bv[pb];
+          bv[pb] = take ? acc[i] : bv[pb];
+          bi[pb] = take ? (uint32_t)(row0 + i) : bi[pb];
+        }
       }
-      if (any_sample) {
+      if (do_sum[pb]) {                            // wave-uniform
         float x[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) x[i] = sample[pb] ? acc[i] * pit[pb] : -INFINITY;
@@ -459,7 +475,7 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     // 16 P positions per wave, P = 1..4 (P = 4 from 512 positions on)
     const int per = kReadWaves * kTile;
     int P = (M + per - 1) / per;
-    P = P < 4 ? P : 4;
+    P = P < kRmMaxP ? P : kRmMaxP;
     const int ny = (M + per * P - 1) / (per * P);
     grid = dim3((h->read_wgs + 7) / 8 * 8 * ny);
     const uint16_t* Wr = (const uint16_t*)h->W_r;
