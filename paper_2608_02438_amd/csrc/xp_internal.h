@@ -63,6 +63,11 @@ struct Workspace {
 
 // Target rows are reduced in chunks of kVChunk entries (16 per thread).
 constexpr int kVChunk = 4096;
+// Verification computes the target rows' log-sum-exp for the first kVRows1
+// rows of every sampled sequence, and for the rest only where the accept scan
+// got past them (marked kVMore in vpos).
+constexpr int kVRows1 = 4;
+constexpr int kVMore = -2;
 
 }  // namespace xp
 

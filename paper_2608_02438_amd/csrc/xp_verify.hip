@@ -21,13 +21,16 @@ namespace xp {
 // kVChunk entries of a row to (max, sum of exp(x - max)), the exponentials in
 // fp32 and the sums in fp64;
 // then one wave per row merges the chunks in a fixed order.
+// Rows k0 + blockIdx.y only; with `more` given, only of sequences whose
+// accept scan went past the first round's rows (vpos == kVMore).
 __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ tl, int B, int V,
                                                       const uint8_t* __restrict__ temp,
                                                       const float* __restrict__ invT,
-                                                      double* __restrict__ part) {
+                                                      double* __restrict__ part, int k0,
+                                                      const int32_t* __restrict__ more) {
   constexpr int PER = kVChunk / 256;
-  const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z, nc = gridDim.x;
-  if (temp[b] == 0) return;
+  const int c = blockIdx.x, k = k0 + blockIdx.y, b = blockIdx.z, nc = gridDim.x;
+  if (temp[b] == 0 || (more != nullptr && more[b] != kVMore)) return;
   const float it = invT[b];
   const float* row = tl + ((size_t)b * (B + 1) + k) * V;
   float x[PER];
@@ -62,9 +65,10 @@ __global__ __launch_bounds__(256) void k_vtarget_part(const float* __restrict__ 
 
 __global__ __launch_bounds__(64) void k_vtarget_comb(int B, int nc, const uint8_t* __restrict__ temp,
                                                      const double* __restrict__ part,
-                                                     double* __restrict__ lseT) {
-  const int i = blockIdx.x, lane = threadIdx.x;           // one wave per row
-  if (temp[i / (B + 1)] == 0) return;
+                                                     double* __restrict__ lseT, int k0,
+                                                     const int32_t* __restrict__ more) {
+  const int b = blockIdx.y, i = b * (B + 1) + k0 + blockIdx.x, lane = threadIdx.x;   // one wave per row
+  if (temp[b] == 0 || (more != nullptr && more[b] != kVMore)) return;
   const double* q = part + (size_t)i * nc * 2;
   double m = -INFINITY;
   for (int c = lane; c < nc; c += kWave) m = fmax(m, q[2 * c]);
@@ -102,8 +106,11 @@ __device__ float refined_logit(int with_read, const float* __restrict__ S, int M
   return with_read ? d : S[s_index(p, v, Ms)];
 }
 
-// One wave per sequence: accept scan.  vpos[b] = rejected position, or B.
-// Rows marked in `skip` (truncated sampling: k_vfaccept) are left alone.
+// One wave per sequence: accept scan over draft positions [kb, min(ke, B)),
+// the target rows [kb, ke) having their log-sum-exp.  vpos[b] = rejected
+// position, or B once all are accepted (which needs row B, ke = B + 1);
+// kVMore when the scan got through without row B (the next round goes on).  kb > 0 continues only such sequences.  Rows
+// marked in `skip` (truncated sampling: k_vfaccept) are left alone.
 template <typename T>
 __global__ __launch_bounds__(64) void k_vaccept(
     int B, int V, int M, int with_read, const int32_t* __restrict__ draft,
@@ -112,9 +119,11 @@ __global__ __launch_bounds__(64) void k_vaccept(
     const float* __restrict__ tl, const float* __restrict__ racc, const float* __restrict__ S,
     int Ms, const T* __restrict__ W_r, const T* __restrict__ Z, const double* __restrict__ lse,
     const double* __restrict__ lseT, int32_t* __restrict__ vpos, int32_t* __restrict__ out_n,
-    int32_t* __restrict__ out_next, uint32_t* __restrict__ err, const float* __restrict__ invT) {
+    int32_t* __restrict__ out_next, uint32_t* __restrict__ err, const float* __restrict__ invT,
+    int kb, int ke) {
   const int b = blockIdx.x, lane = threadIdx.x;
   if (skip != nullptr && skip[b] != 0) return;
+  if (kb > 0 && vpos[b] != kVMore) return;        // decided in the first round
   const bool sample = temp != nullptr && temp[b] != 0;
   int bad = 0;
   if (!sample) {
@@ -139,8 +148,11 @@ __global__ __launch_bounds__(64) void k_vaccept(
     return;
   }
   const float it = invT[b];
-  int n = B;
-  for (int k = 0; k < B; ++k) {
+  // rows [kb, ke) have their log-sum-exp: positions up to min(ke, B) can be
+  // tested, and "all accepted" can be decided only with the bonus row B too
+  const int kend = ke < B ? ke : B;
+  int n = ke >= B + 1 ? B : kVMore;
+  for (int k = kb; k < kend; ++k) {
     const int p = b * B + k;
     int y = draft[p];
     if (y < 0 || y >= V) {
@@ -157,7 +169,7 @@ __global__ __launch_bounds__(64) void k_vaccept(
     }
   }
   if (lane == 0) {
-    out_n[b] = n;
+    if (n != kVMore) out_n[b] = n;
     vpos[b] = n;
     if (bad) atomicOr(err, XP_DEVERR_TOKEN);
   }
@@ -379,18 +391,31 @@ static hipError_t verify_t(xp_handle* h, int batch, const int32_t* draft, const 
   const bool filtering = temp != nullptr && h->state_filtered;
   const uint8_t* skip = filtering ? h->ws.filt : nullptr;
   if (filtering) temp = h->ws.temp_nf;
+  // Round 1: the target rows [0, r1) of every sampled sequence and the accept
+  // scan over them; most sequences reject there.  Round 2: rows [r1, B] of
+  // the sequences that accepted all of the first r1 drafts.
+  const int nc = (h->V + kVChunk - 1) / kVChunk;
+  const int r1 = h->B + 1 < kVRows1 ? h->B + 1 : kVRows1;
   if (temp) {
-    const int nc = (h->V + kVChunk - 1) / kVChunk;
-    hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1, batch), dim3(256), 0, st, tl, h->B,
-                       h->V, temp, h->ws.invT, h->ws.vpart);
-    const int rows = batch * (h->B + 1);
-    hipLaunchKernelGGL(k_vtarget_comb, dim3(rows), dim3(kWave), 0, st, h->B, nc, temp,
-                       h->ws.vpart, h->ws.vstat);
+    hipLaunchKernelGGL(k_vtarget_part, dim3(nc, r1, batch), dim3(256), 0, st, tl, h->B, h->V,
+                       temp, h->ws.invT, h->ws.vpart, 0, (const int32_t*)nullptr);
+    hipLaunchKernelGGL(k_vtarget_comb, dim3(r1, batch), dim3(kWave), 0, st, h->B, nc, temp,
+                       h->ws.vpart, h->ws.vstat, 0, (const int32_t*)nullptr);
   }
   hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
                      draft, temp, skip, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
                      (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
-                     h->ws.err, h->ws.invT);
+                     h->ws.err, h->ws.invT, 0, r1);
+  if (temp && r1 < h->B + 1) {
+    hipLaunchKernelGGL(k_vtarget_part, dim3(nc, h->B + 1 - r1, batch), dim3(256), 0, st, tl,
+                       h->B, h->V, temp, h->ws.invT, h->ws.vpart, r1, h->ws.vpos);
+    hipLaunchKernelGGL(k_vtarget_comb, dim3(h->B + 1 - r1, batch), dim3(kWave), 0, st, h->B, nc,
+                       temp, h->ws.vpart, h->ws.vstat, r1, h->ws.vpos);
+    hipLaunchKernelGGL((k_vaccept<T>), dim3(batch), dim3(64), 0, st, h->B, h->V, M, with_read,
+                       draft, temp, skip, tids, tl, racc, h->ws.s, M, (const T*)h->W_r,
+                       (const T*)h->ws.z, h->ws.lse, h->ws.vstat, h->ws.vpos, out_n, out_next,
+                       h->ws.err, h->ws.invT, r1, h->B + 1);
+  }
   if (temp) {
     hipLaunchKernelGGL((k_vresid<T>), dim3(h->read_wgs, (batch + 15) / 16),
                        dim3(kReadWaves * kWave), 0, st, batch, h->B, h->V, M, with_read,

@@ -121,13 +121,15 @@ def test_largest_built_sizes(H, V, batch, B):
     _full_check(prob, ref, upload(prob), min_exact=0.97)
 
 
-@pytest.mark.parametrize("tau", [None, 0.7])
-def test_sampled_rows_all_accepted_take_the_bonus_token(tau):
+@pytest.mark.parametrize("tau,agree", [(None, 8), (0.7, 8), (None, 5)])
+def test_sampled_rows_all_accepted_take_the_bonus_token(tau, agree):
     """Target logits equal to the refined logits (p = q) accept every draft
     token, so the next token is the inverse-CDF sample of p_{B+1} at u_res:
-    the bonus path of verification, rarely reached with random targets."""
+    the bonus path of verification, rarely reached with random targets.  With
+    p = q on the first five positions only, the first rejection comes at
+    position 5 or later, past the target rows verification reduces first."""
     import torch
-    _say(f"case: sampled rows with p = q (all accepted, bonus token), T={tau}")
+    _say(f"case: sampled rows with p = q on {agree} positions, T={tau}")
     prob = custom_problem("bf16", H=256, V=777, B=8, batch=4, K=4, sigmas=STRESS,
                           temp="sample", seed=61, tau=tau)
     ref = make_refiner(prob)
@@ -136,13 +138,13 @@ def test_sampled_rows_all_accepted_take_the_bonus_token(tau):
     tally, finals = check_refine(prob, run)
     assert tally.exact >= 0.97 * tally.decisions
     tl = prob.inp.target_logits.copy()
-    tl[:, :prob.B, :] = run.logits                 # p_k = q_k for k = 1..B
+    tl[:, :agree, :] = run.logits[:, :agree]       # p_k = q_k for k = 1..agree
     prob.inp.target_logits = tl
     dev["target_logits"] = torch.from_numpy(tl).cuda()
     target_ids = prob.inp.target_ids(run.ids)
     n, nx = _verify(ref, prob, run, dev, target_ids)
     _say(f"  verify: n={n.tolist()} next={nx.tolist()}")
-    assert (n == prob.B).all()
+    assert (n >= agree).all() and (n == prob.B).any() == (agree == prob.B)
     assert check_verify(prob, run, finals, n, nx, target_ids, range(prob.batch)) == 0
 
 
