@@ -32,14 +32,31 @@ def _run(cmd):
     return r.returncode, [l for l in out.splitlines() if "packed-fp32-ops" not in l]
 
 
-def build(verbose: bool = False) -> str:
+# Host AddressSanitizer: the host code only (argument validation, the
+# handles, the launch sequences); device code is built as usual.
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+ASAN_LIB = os.path.join(ROOT, "_build", "libxpress_asan.so")
+
+
+def asan_runtime() -> str:
+    """Path of the host ASan runtime that a process loading ASAN_LIB must preload."""
+    clang = os.path.join(os.path.dirname(os.path.dirname(HIPCC)), "lib", "llvm", "lib", "clang")
+    for ver in sorted(os.listdir(clang), reverse=True):
+        p = os.path.join(clang, ver, "lib", "linux", "libclang_rt.asan-x86_64.so")
+        if os.path.exists(p):
+            return p
+    raise RuntimeError("host ASan runtime not found under " + clang)
+
+
+def build(verbose: bool = False, asan: bool = False) -> str:
     """Compile every HIP source (one hipcc process per file, in parallel) and
-    link them into libxpress.so; returns its path."""
+    link them into libxpress.so (with asan: the host-ASan build ASAN_LIB);
+    returns its path."""
     from concurrent.futures import ThreadPoolExecutor
-    objdir = os.path.join(ROOT, "_build", "obj")
+    objdir = os.path.join(ROOT, "_build", "obj_asan" if asan else "obj")
     os.makedirs(objdir, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include")]
-    compile_flags = [f for f in FLAGS if f != "-shared"]
+    compile_flags = [f for f in FLAGS if f != "-shared"] + (ASAN_FLAGS if asan else [])
     jobs = []
     for src in sources():
         obj = os.path.join(objdir, os.path.basename(src) + ".o")
@@ -57,13 +74,15 @@ def build(verbose: bool = False) -> str:
         for (src, _, _), (_, lines) in zip(jobs, results):
             if lines:
                 print("\n".join(lines))
-    tmp = LIB + ".tmp"
-    rc, lines = _run([HIPCC, *FLAGS, *[j[1] for j in jobs], "-o", tmp])
+    out = ASAN_LIB if asan else LIB
+    tmp = out + ".tmp"
+    rc, lines = _run([HIPCC, *FLAGS, *(ASAN_FLAGS if asan else []), *[j[1] for j in jobs],
+                      "-o", tmp])
     if rc != 0:
         raise RuntimeError("link failed:\n" + "\n".join(lines))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, asan="--asan" in sys.argv))

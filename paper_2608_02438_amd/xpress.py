@@ -14,7 +14,10 @@ from typing import Dict, Optional
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libxpress.so")
+# the library this process loads; XPRESS_LIB names another build of it (the
+# host-ASan one of build.py --asan)
+LIB_PATH = os.environ.get("XPRESS_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libxpress.so")
 
 XP_OK, XP_EINVAL, XP_EUNSUPPORTED, XP_EHIP, XP_ENOMEM = 0, -1, -2, -3, -4
 XP_F32, XP_BF16 = 0, 1
