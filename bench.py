@@ -39,12 +39,12 @@ METRIC = "refined draft blocks/sec (refine+LM-head+verify), Qwen3-8B shape; % HB
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2517.0          # dense bf16 matrix peak of the MI355X
 CSRC = os.path.join(ROOT, "paper_2608_02438_amd", "csrc")
-# committed counter summaries of the LM-head kernel, per workload: (file, kernel source)
+# committed counter summaries of the LM-head kernel, per workload: (file, kernel sources)
+GEMM_SRC = ("xp_gemm.hip", "xp_gemm_pipe.h")
 TRAFFIC = {
-    "qwen3-8b-bf16-B16-b1-greedy": ("k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md", "xp_lmhead.hip"),
-    "qwen3-8b-bf16-B16-b32-greedy": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b32_traffic.md", "xp_gemm.hip"),
-    "qwen3-8b-bf16-B16-b8-sample": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b8_traffic.md", "xp_gemm.hip"),
-    "qwen3-8b-bf16-B32-b64-mixed": ("k_lmhead_gemm_qwen3-8b-bf16-B32-b64_traffic.md", "xp_gemm.hip"),
+    "qwen3-8b-bf16-B16-b1-greedy": ("k_lmhead_qwen3-8b-bf16-B16-b1_traffic.md", ("xp_lmhead.hip",)),
+    "qwen3-8b-bf16-B16-b32-greedy": ("k_lmhead_gemm_qwen3-8b-bf16-B16-b32_traffic.md", GEMM_SRC),
+    "qwen3-8b-bf16-B32-b64-mixed": ("k_lmhead_gemm_qwen3-8b-bf16-B32-b64_traffic.md", GEMM_SRC),
 }
 
 
@@ -52,8 +52,12 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash(src: str) -> str:
-    return hashlib.sha256(open(os.path.join(CSRC, src), "rb").read()).hexdigest()[:16]
+def kernel_source_hash(srcs) -> str:
+    """First 16 hex digits of the sha256 of the kernel's source files, concatenated."""
+    h = hashlib.sha256()
+    for src in srcs:
+        h.update(open(os.path.join(CSRC, src), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(workload: str):
