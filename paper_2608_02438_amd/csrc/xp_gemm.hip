@@ -66,7 +66,10 @@ struct LmEpi {
   int M, Ms, V, ntiles, U2, p0;
   bool psamp[NB];
   float pit[NB];                                   // sampled rows: softmax(s / T)
-  bool any_sample;
+  // per 32-position block, wave-uniform: does any lane take the greedy
+  // maximum, any the softmax partials?  (A block inside one sequence, as
+  // with B a multiple of 32, does only one of the two.)
+  bool do_max[NB], do_sum[NB];
 
   // The position tile is fixed per workgroup, so the sampling flags and 1/T
   // of this wave's positions are loaded once, before the stage loads, and
@@ -77,16 +80,15 @@ struct LmEpi {
       : sc(sc_), S(S_), keys(keys_), stats(stats_), M(M_), Ms(Ms_), V(V_), ntiles(ntiles_),
         U2(U2_), p0(p0_) {
     const int lane = threadIdx.x & 63, wp = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >> 1;
-    bool anyp = false;
 #pragma unroll
     for (int c = 0; c < NB; ++c) {
       const int p = p0 + wp * PW + c * 32 + (lane & 31);
       const int pc = p < M ? p : M - 1;
       psamp[c] = (p < M) & (load_flag(temp, pc / B, W) != 0);
       pit[c] = invT[pc / B];
-      anyp = anyp | psamp[c];
+      do_max[c] = __ballot((p < M) && !psamp[c]) != 0;
+      do_sum[c] = __ballot(psamp[c]) != 0;
     }
-    any_sample = __ballot(anyp) != 0;
 #pragma unroll
     for (int c = 0; c < NB; ++c) asm volatile("" ::"v"(pit[c]));
   }
@@ -115,14 +117,16 @@ struct LmEpi {
             *reinterpret_cast<float4*>(S + s_index(p, rbase + rl, Ms)) =
                 make_float4(acc[a][c][4 * q], acc[a][c][4 * q + 1], acc[a][c][4 * q + 2],
                             acc[a][c][4 * q + 3]);
+          if (do_max[c]) {                                         // wave-uniform
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float x = acc[a][c][4 * q + e];
-            const bool take = rv && !psample && rbase + rl + e < V && x > bvv;
-            bvv = take ? x : bvv;
-            bix = take ? (uint32_t)(rbase + rl + e) : bix;
+            for (int e = 0; e < 4; ++e) {
+              const float x = acc[a][c][4 * q + e];
+              const bool take = rv && !psample && rbase + rl + e < V && x > bvv;
+              bvv = take ? x : bvv;
+              bix = take ? (uint32_t)(rbase + rl + e) : bix;
+            }
           }
-          if (any_sample) {
+          if (do_sum[c]) {                                         // wave-uniform
             float x[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
