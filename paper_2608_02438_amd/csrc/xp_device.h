@@ -27,6 +27,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Two fp32 values to packed bf16 (a low, b high), rounded to nearest even
+// (v_cvt_pk_bf16_f32; the same as f32_to_bf16_rne for finite values)
+typedef __bf16 xp_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float xp_f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(xp_f32x2{a, b}, xp_bf16x2));
+}
+
+// SwiGLU of one feature: silu(g) u = g / (1 + e^-g) u
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
+
 template <typename T> __device__ __forceinline__ float to_f32(T v);
 template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) { return bf16_to_f32(v); }

@@ -41,6 +41,7 @@ struct LmRows {
   int V, H, ntiles, U2;
   const GemmSched* sc;
   int r0 = 0, r1 = 0;
+  static constexpr int xk = 0;                     // every tile spans all of k
   __device__ void prep(int ti) {
     const int u = sc->tile(ti);
     r0 = unit_tile_lo(2 * u, ntiles, U2) * kTile;
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_lmhead_gemm(
   const int p0 = sc.mb * BM;
   LmRows<BN> rows{W, V, H, ntiles, U2, &sc};
   LmEpi<BN, BM> epi(&sc, S, Ms, keys, stats, M, V, ntiles, U2, p0, temp, B, invT, W);
-  gemm_tiles<BN, BM>(rows, epi, X, M, H, ntl, p0, lds);
+  gemm_tiles<BN, BM>(rows, epi, X, H, M, H, ntl, p0, lds);
 }
 
 // ---------------------------------------------------------------------------

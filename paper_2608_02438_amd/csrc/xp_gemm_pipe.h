@@ -56,15 +56,16 @@ struct GemmLane {
   int lr, lk;        // lane % 32, lane / 32
 };
 
-// The ntl row tiles of one workgroup for positions [p0, p0 + BM) of X ([M][K]
-// bf16, rows past M read as row M - 1).  rows.prep(ti) selects tile ti's
-// weight rows; rows.row(r) is then the address of its local row r
-// (0 <= r < BN) at k = 0.  epi(ti, acc, where) consumes tile ti's
-// accumulators; the pipeline clears them afterwards.  lds holds
+// The ntl tiles of one workgroup for positions [p0, p0 + BM) of X (bf16 rows
+// of ldx elements, rows past M read as row M - 1), each over K values of k.
+// rows.prep(ti) selects tile ti's weight rows and its first k, rows.xk (an
+// element offset into the X rows); rows.row(r) is then the address of its
+// local row r (0 <= r < BN) at that k.  epi(ti, acc, where) consumes tile
+// ti's accumulators; the pipeline clears them afterwards.  lds holds
 // GemmShape<BN, BM>::SLOTS 16-byte slots.
 template <int BN, int BM, class Rows, class Epi>
 __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t* __restrict__ X,
-                                           int M, int K, int ntl, int p0, u32x4* lds) {
+                                           int ldx, int M, int K, int ntl, int p0, u32x4* lds) {
   using G = GemmShape<BN, BM>;
   constexpr int RW = G::RW, PW = G::PW, NA = G::NA, NB = G::NB, WS = G::WS, HS = G::HS;
   constexpr int WI = G::WI, HI = G::HI, NS = G::NS;
@@ -88,7 +89,7 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
     const int row = (64 * (HI * wave + j) + lane) >> 2;
     int hr = p0 + row;
     hr = hr < M ? hr : M - 1;
-    hrow[j] = hr * K + 8 * ((lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3));
+    hrow[j] = hr * ldx + 8 * ((lane & 3) ^ (((row >> 1) ^ (row >> 3)) & 3));
   }
   int iss_tile = -1;                                               // tile whose rows are cached
   auto prep = [&](int gs) {
@@ -108,7 +109,7 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
       lds_dma16(rows.row(wrow[j]) + kc * kGK + wcol[j], &lds[st * (WS + HS) + 64 * (WI * wave + j)]);
 #pragma unroll
     for (int j = 0; j < HI; ++j)
-      lds_dma16(X + (size_t)(unsigned)hrow[j] + kc * kGK,
+      lds_dma16(X + (size_t)(unsigned)hrow[j] + rows.xk + kc * kGK,
                 &lds[st * (WS + HS) + WS + 64 * (HI * wave + j)]);
   };
 

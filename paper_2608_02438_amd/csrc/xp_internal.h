@@ -123,11 +123,19 @@ hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, cons
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
 int gemm_units(const xp_handle* h, int M);
-// the context layer's projections for many positions (xp_lgemm.hip)
+// the context layer's projections for many positions (xp_lgemm.hip): plain
+// (S = 1) or split-K into S slabs of [M][N] fp32 partial products (Y, with
+// R = Yb = NULL), and the gate/up projections with the SwiGLU product
+constexpr int kLayerSplitMax = 8;
+constexpr size_t kLayerPartFloats = (size_t)256 * 128 * 128;   // bound of S M N
 bool layer_gemm_ok(int n0, int n1, int N, int K, int M);
+bool layer_glu_ok(int F, int K, int M);
+int layer_gemm_splits(int N, int K, int M);
 hipError_t launch_layer_gemm(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
                              int n1, int N, int K, const uint16_t* X, int M, const float* R,
-                             int ldr, float* Y, uint16_t* Yb, int ldy, hipStream_t st);
+                             int ldr, float* Y, uint16_t* Yb, int ldy, int S, hipStream_t st);
+hipError_t launch_layer_glu(const uint16_t* Wg, const uint16_t* Wu, int F, int K,
+                            const uint16_t* X, int M, uint16_t* act, int ldy, hipStream_t st);
 int gemm_units_max(const xp_handle* h);
 bool lmhead_gemm_ok(const xp_handle* h, int M);
 hipError_t launch_lmhead_gemm(xp_handle* h, int M, const void* hidden, const uint8_t* temp,

@@ -4,7 +4,9 @@
 // refiner itself never reads the context, Proposition 1).
 //
 // Kernels, in launch order:
-//   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u
+//   k_rmsnorm     RMSNorm of x (bf16 in, fp32 copy out) and of x1, to bf16 u;
+//                 x1 = the output projection's split-K slabs + x where that
+//                 projection was split
 //   k_gemv_sk     (one block of up to 16 positions, K <= 4096) y = u W^T
 //                 (+ residual) in the LM-head stream kernel's manner: x in
 //                 LDS, stream-K items with line-complete loads, per-wave LDS
@@ -14,15 +16,18 @@
 //                 split over the 8 waves of a workgroup along k, 16 or 32
 //                 output rows per workgroup, 16 P positions per pass of the
 //                 weight, the waves' partial sums added in fixed order in LDS;
-//                 above 64 positions the tiled GEMM of xp_lgemm.hip and
-//                 k_swiglu take the projections
-//   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16
+//                 above 64 positions the tiled GEMM of xp_lgemm.hip takes
+//                 the projections (SwiGLU in its epilogue; split-K where its
+//                 tiles are fewer than the CUs)
+//   k_qkrope      QK-norm and RoPE of every q and k head, v to bf16 (adding
+//                 the q/k/v projection's split-K slabs)
 //   k_attn        split-KV block attention: a workgroup takes a chunk of
 //                 64-key sub-chunks of one KV head for 16 block positions, one
 //                 wave per query head of the group, with an online softmax;
 //                 each sub-chunk's K and V (transposed) staged in LDS while the
 //                 next one loads; S = K Q^T and O = P V on the matrix cores
 //   k_attn_comb   merges the chunks of every query row in chunk order
+//   k_splitk_sum  the down projection's split-K slabs + x1, to h
 // Every reduction runs in a fixed order, so two runs give identical bits.
 #include <stdarg.h>
 #include <stdio.h>
@@ -37,7 +42,6 @@ namespace xp {
 constexpr int kLinWaves = 8;        // k-split of k_linear
 constexpr int kLinMaxStream = 64;   // positions up to which the projections stream
 constexpr int kAttnWgs = 1024;      // attention workgroups aimed at per call
-constexpr int kAttnPad = 4;         // LDS row padding (bf16) of the transposed V
 constexpr int kHd = 128;            // head_dim (the only one built)
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -49,12 +53,14 @@ __device__ __forceinline__ float wave_sum(float v) {
 // ---------------------------------------------------------------------------
 // RMSNorm of one row per workgroup: u = bf16(x / sqrt(mean(x^2) + eps) * g).
 // The input is bf16 or fp32 (a template parameter: a select between two
-// pointers per element would put every load under a branch); x32, if given,
-// receives the fp32 row.
+// pointers per element would put every load under a branch); with S > 0
+// (fp32 only) the row is (P_0 + ... + P_{S-1}) + x, P_s = P + s slab, added in
+// that order; x32, if given, receives the fp32 row.
 // ---------------------------------------------------------------------------
 template <typename TI>
-__global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H,
-                                                 const uint16_t* __restrict__ g, float eps,
+__global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x,
+                                                 const float* __restrict__ P, int S, size_t slab,
+                                                 int H, const uint16_t* __restrict__ g, float eps,
                                                  float* __restrict__ x32,
                                                  uint16_t* __restrict__ u) {
   // chunks of 8 consecutive elements (16-byte bf16 loads and stores); H is a
@@ -76,8 +82,21 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI* __restrict__ x, int H
         v[j][2 * e + 1] = bf16_to_f32((uint16_t)(w[e] >> 16));
       }
     } else {
-      const float4 a = *reinterpret_cast<const float4*>(x + row * H + 8 * (size_t)cc);
-      const float4 b = *reinterpret_cast<const float4*>(x + row * H + 8 * (size_t)cc + 4);
+      const size_t off = row * H + 8 * (size_t)cc;
+      float4 a = *reinterpret_cast<const float4*>(x + off);
+      float4 b = *reinterpret_cast<const float4*>(x + off + 4);
+      if (S > 0) {
+        float4 pa = *reinterpret_cast<const float4*>(P + off);
+        float4 pb = *reinterpret_cast<const float4*>(P + off + 4);
+        for (int q = 1; q < S; ++q) {
+          const float4 ta = *reinterpret_cast<const float4*>(P + q * slab + off);
+          const float4 tb = *reinterpret_cast<const float4*>(P + q * slab + off + 4);
+          pa.x += ta.x; pa.y += ta.y; pa.z += ta.z; pa.w += ta.w;
+          pb.x += tb.x; pb.y += tb.y; pb.z += tb.z; pb.w += tb.w;
+        }
+        a = make_float4(pa.x + a.x, pa.y + a.y, pa.z + a.z, pa.w + a.w);
+        b = make_float4(pb.x + b.x, pb.y + b.y, pb.z + b.z, pb.w + b.w);
+      }
       v[j][0] = a.x; v[j][1] = a.y; v[j][2] = a.z; v[j][3] = a.w;
       v[j][4] = b.x; v[j][5] = b.y; v[j][6] = b.z; v[j][7] = b.w;
     }
@@ -407,92 +426,261 @@ __global__ __launch_bounds__(kGsWaves * kWave) void k_gemv_sk(
 }
 
 // ---------------------------------------------------------------------------
-// QK-norm + RoPE: one wave per (position m, head slot): slots [0, nh) are the
-// q heads, [nh, nh + nkv) the k heads, [nh + nkv, nh + 2 nkv) the v heads
-// (converted only).  Lane l holds elements l and l + 64, the rotate-half pair
-// of frequency l; the angle is taken in double.
+// QK-norm + RoPE: one workgroup per position m; wave w takes the head slots
+// w, w + 4, ...: slots [0, nh) are the q heads, [nh, nh + nkv) the k heads,
+// [nh + nkv, nh + 2 nkv) the v heads (converted only).  Lane l holds elements
+// l and l + 64, the rotate-half pair of frequency l; the angle (taken in
+// double) depends on the position and l only, so each wave forms its cosine
+// and sine once for all its slots.  The row is P_0 + ... + P_{S-1}
+// (P_s = qkv + s slab, added in that order; S = 1: the projection itself).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_qkrope(
-    const float* __restrict__ qkv, int ldq, int M, int B, int nh, int nkv,
+    const float* __restrict__ qkv, int S, size_t slab, int ldq, int B, int nh, int nkv,
     const int32_t* __restrict__ ctx_len, int Cmax, const uint16_t* __restrict__ gq,
     const uint16_t* __restrict__ gk, float eps, float theta, uint16_t* __restrict__ qn,
     uint16_t* __restrict__ kb, uint16_t* __restrict__ vb) {
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m = blockIdx.x;
   const int nslots = nh + 2 * nkv;
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= M * nslots) return;                   // whole wave
-  const int m = w / nslots, hs = w - m * nslots;
-  const float* src = qkv + (size_t)m * ldq + (size_t)hs * kHd;
-  float a = src[lane], b = src[lane + 64];
-  if (hs >= nh + nkv) {
-    uint16_t* dst = vb + ((size_t)m * nkv + (hs - nh - nkv)) * kHd;
-    dst[lane] = f32_to_bf16_rne(a);
-    dst[lane + 64] = f32_to_bf16_rne(b);
-    return;
-  }
-  const bool isq = hs < nh;
-  const float ss = wave_sum(a * a + b * b);
-  const float r = 1.f / sqrtf(ss / (float)kHd + eps);
-  const uint16_t* gw = isq ? gq : gk;
-  a = a * r * bf16_to_f32(gw[lane]);
-  b = b * r * bf16_to_f32(gw[lane + 64]);
   int C = ctx_len[m / B];
   C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
   const double pos = (double)(C + m % B);
   const double ang = pos * pow((double)theta, -2.0 * (double)lane / (double)kHd);
   const float cs = (float)cos(ang), sn = (float)sin(ang);
-  uint16_t* dst = isq ? qn + ((size_t)m * nh + hs) * kHd : kb + ((size_t)m * nkv + (hs - nh)) * kHd;
-  dst[lane] = f32_to_bf16_rne(a * cs - b * sn);
-  dst[lane + 64] = f32_to_bf16_rne(b * cs + a * sn);
+  const float gq0 = bf16_to_f32(gq[lane]), gq1 = bf16_to_f32(gq[lane + 64]);
+  const float gk0 = bf16_to_f32(gk[lane]), gk1 = bf16_to_f32(gk[lane + 64]);
+  for (int hs = wave; hs < nslots; hs += 4) {
+    const float* src = qkv + (size_t)m * ldq + (size_t)hs * kHd;
+    float a = src[lane], b = src[lane + 64];
+    for (int q = 1; q < S; ++q) {
+      a += src[q * slab + lane];
+      b += src[q * slab + lane + 64];
+    }
+    if (hs >= nh + nkv) {                        // wave-uniform
+      uint16_t* dst = vb + ((size_t)m * nkv + (hs - nh - nkv)) * kHd;
+      dst[lane] = f32_to_bf16_rne(a);
+      dst[lane + 64] = f32_to_bf16_rne(b);
+      continue;
+    }
+    const bool isq = hs < nh;
+    const float ss = wave_sum(a * a + b * b);
+    const float r = 1.f / sqrtf(ss / (float)kHd + eps);
+    a = a * r * (isq ? gq0 : gk0);
+    b = b * r * (isq ? gq1 : gk1);
+    uint16_t* dst =
+        isq ? qn + ((size_t)m * nh + hs) * kHd : kb + ((size_t)m * nkv + (hs - nh)) * kHd;
+    dst[lane] = f32_to_bf16_rne(a * cs - b * sn);
+    dst[lane + 64] = f32_to_bf16_rne(b * cs + a * sn);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Split-KV block attention, flash-decoding style.  Grid (chunk s, KV head,
-// sequence b x position block pb); wave w is query head kvh * GRP + w for
-// block positions 16 pb .. 16 pb + 15; a chunk is nsub sub-chunks of 64 keys,
-// walked with an online softmax.  Key kk of sequence b is context key kk
-// (kk < C) or block key kk - C (C <= kk < C + B); keys from C + B on do not
-// exist.
+// sequence b); wave w is query head kvh * GRP + w % GRP for the block
+// positions 16 pb .. 16 pb + 15, pb = w / GRP (NPB position blocks), so the
+// group's query heads and the block's positions share every K and V byte
+// read.  A chunk is nsub sub-chunks of 64 keys, walked with an online softmax.
+// Key kk of sequence b is context key kk (kk < C) or block key kk - C
+// (C <= kk < C + B); keys from C + B on do not exist (their rows are loaded
+// as the last key's and masked).
 //
-// Per sub-chunk: its K (as is) and V (transposed) go through one LDS buffer;
-// the next sub-chunk's 16-byte items are loaded into registers before the
-// current one is computed, so its latency hides behind that work.  S^T = K Q^T
-// per 16-key tile (A: key rows, B: the wave's q): lane l holds keys
-// 16 t + 4 (l / 16) + i for query l % 16.  With the running maximum m (per
-// query) the numerators e = exp(s - m) enter O = P V as two bf16 parts: the A
-// operand's eight k slots of lane l are its own e of tiles 2u and 2u + 1
-// (keys 32 u + 4 (l/16) + 0..3 and 32 u + 16 + 4 (l/16) + 0..3), the B operand
-// takes V of the same keys from the transposed copy, and the output lane holds
-// queries 4 (l / 16) + i for d = 16 dt + l % 16.  A new maximum rescales O and
-// l by exp(m_old - m_new).  Written per (chunk, query): O (relative to the
+// K and V go from HBM straight into an NS-stage LDS ring (global_load_lds,
+// 1 KB per instruction, no staging registers); a stage is the sub-chunk's 64
+// K rows then its 64 V rows, 256 B each, the 16-byte chunk c of row r stored
+// at position c ^ (r & 15), so that both reads below are free of bank
+// conflicts.  S^T = K Q^T per 16-key tile (A: key rows, B: the wave's q):
+// lane l holds keys 16 t + 4 (l / 16) + i for query l % 16.  With the
+// running maximum m (per query) the numerators e = exp(s - m) enter O = P V
+// as two bf16 parts: the A operand's eight k slots of lane l are its own e of
+// tiles 2u and 2u + 1 (keys 32 u + 4 (l/16) + 0..3 and 32 u + 16 + 4 (l/16) +
+// 0..3); the B operand takes V of the same keys with two transposing reads
+// (ds_read_b64_tr_b16: in each 16-lane group, output lane i receives element
+// i % 4 of the 8-byte reads of lanes 4 j + i / 4, j = 0..3, so when lane s
+// reads 4 columns of key row k0 + s / 4, lane i receives keys k0 .. k0 + 3 of
+// one column); the output lane holds queries 4 (l / 16) + i for
+// d = 16 dt + l % 16.  A new maximum rescales O and l by 2^(m_old - m_new)
+// (scores in base-2 units).  Written per (chunk, query): O (relative to the
 // chunk's final maximum m), m and l.
 // ---------------------------------------------------------------------------
-constexpr int kSub = 64;            // keys per sub-chunk (one LDS stage)
+constexpr int kSub = 64;                       // keys per sub-chunk (one LDS stage)
+constexpr int kAttnSlots = 2 * kSub * kHd / 8; // 16-byte slots of a stage: K rows, then V rows
 
-template <int GRP>
-__global__ __launch_bounds__(GRP * kWave) void k_attn(
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {   // p: an LDS address
+  const v4i16 r =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)p);
+  return __builtin_bit_cast(uint2, r);
+}
+
+// Waves of a workgroup: one per (query head of the group, position block),
+// times KH = 2 key halves where that leaves at most eight (the two waves of a
+// pair take keys 0..31 and 32..63 of every sub-chunk with their own running
+// maximum, sum and O, merged at the end), so that a CU holds enough waves to
+// hide each one's latency.  The LDS ring has NS = 2 stages (64 KB, two
+// workgroups per CU), 3 for 16 waves (96 KB, one workgroup per CU, which
+// also holds the eight pairs' merge).
+__host__ __device__ constexpr int attn_halves(int grp, int npb) { return grp * npb <= 8 ? 2 : 1; }
+__host__ __device__ constexpr int attn_waves(int grp, int npb) {
+  return grp * npb * attn_halves(grp, npb);
+}
+template <int GRP, int NPB>
+struct AttnShape {
+  static constexpr int KH = attn_halves(GRP, NPB);
+  static constexpr int W = attn_waves(GRP, NPB);
+  static constexpr int NS = W >= 16 ? 3 : 2;
+};
+
+// The PER loads of one wave for the sub-chunk starting at key k0 into the
+// stage at `stage`: load e is instruction ins = wave PER + e of the stage,
+// slots 64 ins .. + 63: K rows (ins < 16) or V rows 4 (ins % 16) + lane / 16,
+// lane l bringing logical chunk (l % 16) ^ (row & 15) of its row (rows past
+// the last key repeat it).
+template <int PER>
+__device__ __forceinline__ void attn_issue(u32x4* stage, int wave, int lane, int k0, int nkeys,
+                                           int C, int B, int Cmax, int nkv, int kvh, int b,
+                                           const uint16_t* kcache, const uint16_t* vcache,
+                                           const uint16_t* kb, const uint16_t* vb) {
+  const int lrow = lane >> 4, lpc = lane & 15;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int ins = wave * PER + e;
+    const bool isv = ins >= 16;
+    const int row = 4 * (ins & 15) + lrow;
+    int kk = k0 + row;
+    kk = kk < nkeys ? kk : nkeys - 1;
+    const uint16_t* src =
+        kk < C ? (isv ? vcache : kcache) + (((size_t)b * Cmax + kk) * nkv + kvh) * kHd
+               : (isv ? vb : kb) + (((size_t)b * B + (kk - C)) * nkv + kvh) * kHd;
+    lds_dma16(src + 8 * (lpc ^ (row & 15)), stage + 64 * ins);
+  }
+}
+
+// One sub-chunk of the wave's keys (tiles t0 .. t0 + NT - 1 of the stage at
+// Ks / Vs): S, the online softmax and O += P V.  Scores are kept in base-2
+// units (q.k / sqrt(hd) times log2 e), so every exponential is one exp2.
+template <int NT>
+__device__ __forceinline__ void attn_step(const u32x4* Ks, const uint16_t* Vs,
+                                          const u32x4 (&qf)[kHd / 32], int t0, int g, int li,
+                                          bool qv, bool interior, int kb0, int nkeys, int C,
+                                          int causal, int p, floatx4 (&o)[kHd / 16],
+                                          float& m_run, float& l_run) {
+  constexpr float kScale2 = 0.12751743082459868f;   // log2(e) / sqrt(128)
+  floatx4 sc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int kr = kTile * (t0 + t) + li;         // A operand: key kr, d 32 ks + 8 g ..
+    floatx4 acc{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kHd / 32; ++ks)
+      acc = Mfma<uint16_t>::mma(Ks[kr * 16 + ((4 * ks + g) ^ li)], qf[ks], acc);
+    if (interior) {                               // workgroup-uniform
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sc[t][i] = qv ? acc[i] * kScale2 : -INFINITY;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kb0 + kTile * (t0 + t) + 4 * g + i;
+        const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
+        sc[t][i] = vis ? acc[i] * kScale2 : -INFINITY;
+      }
+    }
+  }
+  float mx = m_run;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  // with no visible key yet (mx = -inf) every exponent below is -inf: 0
+  const float mxs = mx == -INFINITY ? 0.f : mx;
+  const float alpha = __builtin_amdgcn_exp2f(m_run - mxs);
+  // numerators as two bf16 parts (hi = bf16(e), lo = bf16(e - hi)); the
+  // sum is taken over the same parts
+  uint32_t eh[NT][2], el[NT][2];
+  float lsum = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; i += 2) {
+      const float e0 = __builtin_amdgcn_exp2f(sc[t][i] - mxs);
+      const float e1 = __builtin_amdgcn_exp2f(sc[t][i + 1] - mxs);
+      const uint32_t h = pk_bf16(e0, e1);
+      const float h0 = __uint_as_float(h << 16), h1 = __uint_as_float(h & 0xFFFF0000u);
+      const uint32_t lo = pk_bf16(e0 - h0, e1 - h1);
+      const float l0 = __uint_as_float(lo << 16), l1 = __uint_as_float(lo & 0xFFFF0000u);
+      lsum += h0 + l0;
+      lsum += h1 + l1;
+      eh[t][i / 2] = h;
+      el[t][i / 2] = lo;
+    }
+  lsum += __shfl_xor(lsum, 16, kWave);
+  lsum += __shfl_xor(lsum, 32, kWave);
+  l_run = l_run * alpha + lsum;
+  const bool moved = __ballot(mx != m_run) != 0;  // wave-uniform: else every alpha is 1
+  m_run = mx;
+  // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
+  if (moved) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float ai = __shfl(alpha, 4 * g + i, kWave);
+#pragma unroll
+      for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
+    }
+  }
+  // V reads: lane (g, li) supplies key row k0 + li / 4 (k0 = 32 u + 4 g,
+  // then + 16), columns 16 dt + 4 (li % 4) .. + 3: chunk 2 dt + (li % 4) / 2,
+  // half (li % 4) & 1
+  const int vr = li >> 2, vc = (li & 3) >> 1, vh = 4 * (li & 1);
+#pragma unroll
+  for (int u = 0; u < NT / 2; ++u) {
+    const u32x4 ph{eh[2 * u][0], eh[2 * u][1], eh[2 * u + 1][0], eh[2 * u + 1][1]};
+    const u32x4 pl{el[2 * u][0], el[2 * u][1], el[2 * u + 1][0], el[2 * u + 1][1]};
+    const int r0 = kTile * t0 + 32 * u + 4 * g + vr, r1 = r0 + 16;
+#pragma unroll
+    for (int dt = 0; dt < kHd / 16; ++dt) {
+      const int c = 2 * dt + vc;
+      const uint2 v0 = lds_read_tr16(Vs + 8 * (r0 * 16 + (c ^ (r0 & 15))) + vh);
+      const uint2 v1 = lds_read_tr16(Vs + 8 * (r1 * 16 + (c ^ (r1 & 15))) + vh);
+      const u32x4 vvv{v0.x, v0.y, v1.x, v1.y};
+      o[dt] = Mfma<uint16_t>::mma(pl, vvv, o[dt]);
+      o[dt] = Mfma<uint16_t>::mma(ph, vvv, o[dt]);
+    }
+  }
+}
+
+template <int GRP, int NPB>
+__global__ __launch_bounds__(attn_waves(GRP, NPB) * kWave) void k_attn(
     const uint16_t* __restrict__ qn, const uint16_t* __restrict__ kcache,
     const uint16_t* __restrict__ vcache, const uint16_t* __restrict__ kb,
     const uint16_t* __restrict__ vb, const int32_t* __restrict__ ctx_len, int Cmax, int B,
-    int npb, int nh, int nkv, int causal, int ns, int nsub, float* __restrict__ opart,
+    int nh, int nkv, int causal, int ns, int nsub, float* __restrict__ opart,
     float* __restrict__ mlpart) {
-  constexpr int kItems = kSub * (kHd / 8);       // 16-byte items of K (and of V) per sub-chunk
-  constexpr int PER = kItems / (GRP * kWave);    // items per thread
-  static_assert(PER % 2 == 0, "items come in key pairs");
-  __shared__ __align__(16) uint16_t Ks[kSub][kHd + 8];        // +16 B per row
-  __shared__ __align__(16) uint16_t Vt[kHd][kSub + kAttnPad];
-  const int s = blockIdx.x, kvh = blockIdx.y, z = blockIdx.z;
-  const int b = z / npb, pb = z - b * npb;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  using SH = AttnShape<GRP, NPB>;
+  constexpr int W = SH::W, NS = SH::NS, KH = SH::KH;
+  constexpr int PER = kAttnSlots / 64 / W;       // 1 KB loads per wave per stage
+  static_assert(PER * W * 64 == kAttnSlots && 16 % PER == 0, "loads per stage, K or V per wave");
+  static_assert((NS - 2) * PER < 64, "vmcnt field");
+  constexpr int NT = kSub / kTile / KH;          // 16-key tiles per wave per sub-chunk
+  static_assert(NT % 2 == 0, "tiles come in pairs");
+  constexpr int kMerge = kTile * kHd + 2 * kTile;                // floats per pair
+  static_assert(KH == 1 || GRP * NPB * kMerge * 4 <= NS * kAttnSlots * 16, "merge in LDS");
+  __shared__ u32x4 lds[NS * kAttnSlots];
+  const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int pair = wave % (GRP * NPB), kh = wave / (GRP * NPB);
+  const int hw = pair % GRP, pb = pair / GRP;
+  const int t0 = kh * NT;                        // first tile of the wave's keys
   const int g = lane >> 4, li = lane & 15;
   int C = ctx_len[b];
   C = C < 0 ? 0 : (C > Cmax ? Cmax : C);
   const int nkeys = C + B, kbase = s * kSub * nsub;
-  const size_t pidx = (((size_t)z * nkv + kvh) * ns + s) * GRP + wave;
+  const size_t pidx = ((((size_t)b * NPB + pb) * nkv + kvh) * ns + s) * GRP + hw;
   float* op = opart + pidx * (kTile * kHd);
   float* ml = mlpart + pidx * (2 * kTile);
   if (kbase >= nkeys) {                          // whole workgroup: no key in this chunk
-    if (lane < kTile) {
+    if (kh == 0 && lane < kTile) {
       ml[2 * lane] = -INFINITY;
       ml[2 * lane + 1] = 0.f;
     }
@@ -500,142 +688,105 @@ __global__ __launch_bounds__(GRP * kWave) void k_attn(
   }
   const int left = (nkeys - kbase + kSub - 1) / kSub;
   const int nj = left < nsub ? left : nsub;      // sub-chunks holding keys (>= 1)
-  // row of key kk (< nkeys) in the cache or in the block's own keys
-  auto krow = [&](int kk, const uint16_t* cache, const uint16_t* blk) -> const uint16_t* {
-    if (kk < C) return cache + (((size_t)b * Cmax + kk) * nkv + kvh) * kHd;
-    return blk + (((size_t)b * B + (kk - C)) * nkv + kvh) * kHd;
-  };
-  // the items of sub-chunk j into registers (keys past the end are zeros)
-  auto load_sub = [&](int j, u32x4 (&kv)[PER], u32x4 (&vv)[PER]) {
-#pragma unroll
-    for (int e = 0; e < PER; ++e) {
-      const int ip = threadIdx.x + GRP * kWave * (e >> 1);
-      const int kk = kbase + j * kSub + 2 * (ip >> 4) + (e & 1), c = ip & 15;
-      const bool ok = kk < nkeys;
-      const int kc = ok ? kk : nkeys - 1;
-      kv[e] = ok ? ld16(krow(kc, kcache, kb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
-      vv[e] = ok ? ld16(krow(kc, vcache, vb) + 8 * c) : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-  // items 2e and 2e + 1 of a thread are keys 2 kq and 2 kq + 1 of one 16-byte
-  // column c: V is transposed with one 32-bit LDS store per d (both keys)
-  auto store_sub = [&](const u32x4 (&kv)[PER], const u32x4 (&vv)[PER]) {
-#pragma unroll
-    for (int e = 0; e < PER; e += 2) {
-      const int ip = threadIdx.x + GRP * kWave * (e >> 1);
-      const int key = 2 * (ip >> 4), c = ip & 15;
-      *reinterpret_cast<u32x4*>(&Ks[key][8 * c]) = kv[e];
-      *reinterpret_cast<u32x4*>(&Ks[key + 1][8 * c]) = kv[e + 1];
-      const uint32_t a[4] = {vv[e].x, vv[e].y, vv[e].z, vv[e].w};
-      const uint32_t bb[4] = {vv[e + 1].x, vv[e + 1].y, vv[e + 1].z, vv[e + 1].w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        *reinterpret_cast<uint32_t*>(&Vt[8 * c + 2 * q][key]) = (a[q] & 0xFFFFu) | (bb[q] << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[8 * c + 2 * q + 1][key]) =
-            (a[q] >> 16) | (bb[q] & 0xFFFF0000u);
-      }
-    }
-  };
 
-  // the wave's q (B operand): query li, head kvh * GRP + wave
+  // the wave's q (B operand): query li of block pb, head kvh * GRP + hw
   const int p = pb * kTile + li;
   const bool qv = p < B;
   const uint16_t* qs =
-      qn + (((size_t)b * B + (qv ? p : 0)) * nh + (size_t)kvh * GRP + wave) * kHd + 8 * g;
+      qn + (((size_t)b * B + (qv ? p : 0)) * nh + (size_t)kvh * GRP + hw) * kHd + 8 * g;
   u32x4 qf[kHd / 32];
 #pragma unroll
   for (int ks = 0; ks < kHd / 32; ++ks) qf[ks] = qv ? ld16(qs + 32 * ks) : u32x4{0u, 0u, 0u, 0u};
 
-  constexpr int NT = kSub / kTile;
-  const float scale = 0.08838834764831845f;      // 1 / sqrt(128)
-  float m_run = -INFINITY, l_run = 0.f;          // per query li
+  // Loads of sub-chunks inside the context: the wave's rows (K or V, one
+  // kind per wave) at a per-lane address plus the sub-chunk's first key
+  // times the key stride; other sub-chunks take attn_issue's general path.
+  const size_t kst = (size_t)nkv * kHd;           // elements per key row
+  const uint16_t* lp[PER];
+  {
+    const bool isv = wave * PER >= 16;
+    const uint16_t* cb = (isv ? vcache : kcache) + ((size_t)b * Cmax * nkv + kvh) * kHd;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int row = 4 * ((wave * PER + e) & 15) + (lane >> 4);
+      lp[e] = cb + (size_t)row * kst + 8 * ((lane & 15) ^ (row & 15));
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0070);            // q landed: from here vmcnt counts the ring
+
+  float m_run = -INFINITY, l_run = 0.f;          // per query li, base-2 units
   floatx4 o[kHd / 16];
 #pragma unroll
   for (int dt = 0; dt < kHd / 16; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  u32x4 kv[PER], vv[PER];
-  load_sub(0, kv, vv);
-  for (int j = 0; j < nj; ++j) {
-    __syncthreads();                             // every wave is done with sub-chunk j - 1
-    store_sub(kv, vv);
-    __syncthreads();                             // sub-chunk j is in LDS
-    load_sub(j + 1 < nj ? j + 1 : j, kv, vv);    // next (the last re-reads itself: no branch)
-    const int kb0 = kbase + j * kSub;
-    const bool interior = kb0 + kSub <= C;       // context keys only: every key visible
-    floatx4 sc[NT];
+
+  // sub-chunk j (clamped to the last) into ring slot `slot` (0 <= slot < NS);
+  // both arguments are evaluated once, before the macro's own loop
+#define XP_ATTN_ISSUE(j, slot)                                                                \
+  do {                                                                                        \
+    const int j_ = (j), slot_ = (slot);                                                       \
+    const int k0_ = kbase + (j_ < nj ? j_ : nj - 1) * kSub;                                   \
+    u32x4* st_ = lds + slot_ * kAttnSlots;                                                    \
+    if (k0_ + kSub <= C) {                                                                    \
+      _Pragma("unroll") for (int e_ = 0; e_ < PER; ++e_)                                      \
+        lds_dma16(lp[e_] + (size_t)k0_ * kst, st_ + 64 * (wave * PER + e_));                  \
+    } else {                                                                                  \
+      attn_issue<PER>(st_, wave, lane, k0_, nkeys, C, B, Cmax, nkv, kvh, b, kcache, vcache,   \
+                      kb, vb);                                                                \
+    }                                                                                         \
+  } while (0)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      u32x4 kf[kHd / 32];                        // A operand: key 16 t + li
+  for (int jp = 0; jp < NS - 1; ++jp) XP_ATTN_ISSUE(jp, jp);
+  constexpr int kWait = (NS - 2) * PER;          // this wave's loads of the NS - 2 later stages
+  for (int j0 = 0; j0 < nj; j0 += NS) {
 #pragma unroll
-      for (int ks = 0; ks < kHd / 32; ++ks)
-        kf[ks] = *reinterpret_cast<const u32x4*>(&Ks[kTile * t + li][32 * ks + 8 * g]);
-      floatx4 acc{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < kHd / 32; ++ks) acc = Mfma<uint16_t>::mma(kf[ks], qf[ks], acc);
-      if (interior) {                            // workgroup-uniform
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sc[t][i] = qv ? acc[i] * scale : -INFINITY;
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = kb0 + kTile * t + 4 * g + i;
-          const bool vis = qv && key < nkeys && (key < C || !causal || key - C <= p);
-          sc[t][i] = vis ? acc[i] * scale : -INFINITY;
-        }
+    for (int sl = 0; sl < NS; ++sl) {            // ring slot sl holds sub-chunk j0 + sl
+      const int j = j0 + sl;
+      if (j < nj) {                              // workgroup-uniform
+        // sub-chunk j landed (every wave's loads) and every wave is done
+        // with j - 1, whose slot then takes sub-chunk j + NS - 1
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0x0070 | (kWait & 15) | ((kWait >> 4) << 14));
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        XP_ATTN_ISSUE(j + NS - 1, (sl + NS - 1) % NS);
+        const u32x4* Ks = lds + sl * kAttnSlots;
+        const int kb0 = kbase + j * kSub;
+        attn_step<NT>(Ks, reinterpret_cast<const uint16_t*>(Ks + kAttnSlots / 2), qf, t0, g, li,
+                      qv, kb0 + kSub <= C, kb0, nkeys, C, causal, p, o, m_run, l_run);
       }
     }
-    float mx = m_run;
+  }
+#undef XP_ATTN_ISSUE
+  __builtin_amdgcn_s_waitcnt(0x0070);            // the clamped loads past the last sub-chunk
+  if constexpr (KH == 2) {
+    // the second key half hands (m, l, O) to the first through the ring's
+    // LDS: O' = 2^(m0 - M) O0 + 2^(m1 - M) O1, l likewise, M = max(m0, m1)
+    __syncthreads();                             // every wave's loads landed and reads done
+    float* mg = reinterpret_cast<float*>(lds) + pair * kMerge;
+    if (kh == 1) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+      for (int dt = 0; dt < kHd / 16; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float alpha = m_run == -INFINITY ? 0.f : __expf(m_run - mx);
-    // numerators as two bf16 parts; the sum is taken over the same parts
-    uint32_t eh[NT][2], el[NT][2];
-    float lsum = 0.f;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      uint16_t h[4], lo[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float e = mx == -INFINITY ? 0.f : __expf(sc[t][i] - mx);
-        h[i] = f32_to_bf16_rne(e);
-        lo[i] = f32_to_bf16_rne(e - bf16_to_f32(h[i]));
-        lsum += bf16_to_f32(h[i]) + bf16_to_f32(lo[i]);
-      }
-      eh[t][0] = h[0] | ((uint32_t)h[1] << 16);
-      eh[t][1] = h[2] | ((uint32_t)h[3] << 16);
-      el[t][0] = lo[0] | ((uint32_t)lo[1] << 16);
-      el[t][1] = lo[2] | ((uint32_t)lo[3] << 16);
-    }
-    lsum += __shfl_xor(lsum, 16, kWave);
-    lsum += __shfl_xor(lsum, 32, kWave);
-    l_run = l_run * alpha + lsum;
-    const bool moved = __ballot(mx != m_run) != 0;   // wave-uniform: else every alpha is 1
-    m_run = mx;
-    // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
-    if (moved) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float ai = __shfl(alpha, 4 * g + i, kWave);
-#pragma unroll
-        for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
+        for (int i = 0; i < 4; ++i) mg[(4 * g + i) * kHd + 16 * dt + li] = o[dt][i];
+      if (lane < kTile) {
+        mg[kTile * kHd + lane] = m_run;
+        mg[kTile * kHd + kTile + lane] = l_run;
       }
     }
+    __syncthreads();
+    if (kh == 1) return;                         // whole wave; no barrier follows
+    const float m1 = mg[kTile * kHd + li], l1 = mg[kTile * kHd + kTile + li];
+    const float M = fmaxf(m_run, m1);
+    const float Ms = M == -INFINITY ? 0.f : M;
+    const float f0 = __builtin_amdgcn_exp2f(m_run - Ms), f1 = __builtin_amdgcn_exp2f(m1 - Ms);
+    l_run = f0 * l_run + f1 * l1;
+    m_run = M;
 #pragma unroll
-    for (int u = 0; u < NT / 2; ++u) {
-      const u32x4 ph{eh[2 * u][0], eh[2 * u][1], eh[2 * u + 1][0], eh[2 * u + 1][1]};
-      const u32x4 pl{el[2 * u][0], el[2 * u][1], el[2 * u + 1][0], el[2 * u + 1][1]};
+    for (int i = 0; i < 4; ++i) {
+      const float a0 = __shfl(f0, 4 * g + i, kWave), a1 = __shfl(f1, 4 * g + i, kWave);
 #pragma unroll
-      for (int dt = 0; dt < kHd / 16; ++dt) {
-        const int d = 16 * dt + li;
-        const uint2 v0 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 4 * g]);
-        const uint2 v1 = *reinterpret_cast<const uint2*>(&Vt[d][32 * u + 16 + 4 * g]);
-        const u32x4 vvv{v0.x, v0.y, v1.x, v1.y};
-        o[dt] = Mfma<uint16_t>::mma(pl, vvv, o[dt]);
-        o[dt] = Mfma<uint16_t>::mma(ph, vvv, o[dt]);
-      }
+      for (int dt = 0; dt < kHd / 16; ++dt)
+        o[dt][i] = a0 * o[dt][i] + a1 * mg[(4 * g + i) * kHd + 16 * dt + li];
     }
   }
 #pragma unroll
@@ -649,7 +800,8 @@ __global__ __launch_bounds__(GRP * kWave) void k_attn(
 }
 
 // One wave per (position m, query head h): merge the chunks in order,
-// attn = sum_s e^(m_s - M) O_s / sum_s e^(m_s - M) l_s, to bf16.  Lane j
+// attn = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, to bf16 (m in the
+// base-2 units of k_attn).  Lane j
 // takes the (m, l) of chunk s0 + j; the O rows are then read eight chunks at a
 // time and added in chunk order.  A chunk whose l is 0 (no visible key; its O
 // may be unwritten) contributes nothing.
@@ -686,7 +838,7 @@ __global__ __launch_bounds__(256) void k_attn_comb(const float* __restrict__ opa
   for (int s0 = 0; s0 < ns; s0 += kWave) {
     float ms, ls;
     mlv(s0 + lane, ms, ls);
-    const float f = ls > 0.f ? __expf(ms - mm) : 0.f;
+    const float f = ls > 0.f ? __builtin_amdgcn_exp2f(ms - mm) : 0.f;
     Ll += f * ls;
     const int cnt = ns - s0 < kWave ? ns - s0 : kWave;
     for (int j0 = 0; j0 < cnt; j0 += 8) {
@@ -722,7 +874,26 @@ __global__ __launch_bounds__(256) void k_swiglu(const float* __restrict__ GU, in
   if (i >= n) return;
   const size_t m = i / F, j = i - m * F;
   const float gv = GU[m * 2 * F + j], uv = GU[m * 2 * F + F + j];
-  act[i] = f32_to_bf16_rne(gv / (1.f + __expf(-gv)) * uv);
+  act[i] = f32_to_bf16_rne(silu_mul(gv, uv));
+}
+
+// y = (P_0 + ... + P_{S-1}) + R, added in that order, P_s = P + s n (the
+// split-K slabs of a projection, rows of N); Y fp32 and Yb bf16 if given.
+// Four consecutive elements per thread.
+__global__ __launch_bounds__(256) void k_splitk_sum(const float* __restrict__ P, int S, size_t n,
+                                                    const float* __restrict__ R,
+                                                    float* __restrict__ Y,
+                                                    uint16_t* __restrict__ Yb) {
+  const size_t i = 4 * ((size_t)blockIdx.x * 256 + threadIdx.x);
+  if (i >= n) return;
+  floatx4 v = *reinterpret_cast<const floatx4*>(P + i);
+  for (int q = 1; q < S; ++q) v += *reinterpret_cast<const floatx4*>(P + q * n + i);
+  v += *reinterpret_cast<const floatx4*>(R + i);
+  if (Y) *reinterpret_cast<floatx4*>(Y + i) = v;
+  if (Yb)
+    *reinterpret_cast<uint2*>(Yb + i) =
+        make_uint2(f32_to_bf16_rne(v[0]) | ((uint32_t)f32_to_bf16_rne(v[1]) << 16),
+                   f32_to_bf16_rne(v[2]) | ((uint32_t)f32_to_bf16_rne(v[3]) << 16));
 }
 
 }  // namespace xp
@@ -740,8 +911,10 @@ struct LayerBufs {
   uint16_t* attn = nullptr;          // [M][nhd]
   float *x1 = nullptr, *h32 = nullptr, *GU = nullptr;     // GU: [gu_rows][2 F] gate | up
   uint16_t* act = nullptr;           // [M][F]    SwiGLU activation
+  float* part = nullptr;             // split-K slabs of one projection (NULL: no split)
   size_t nparts = 0;                 // attention partials the buffers hold
   size_t gu_rows = 0;                // positions GU holds
+  size_t part_floats = 0;            // floats `part` holds
 };
 
 struct xp_layer {
@@ -826,26 +999,29 @@ static bool rows_fit_int32(const xp_layer& L, int64_t positions) {
   return positions * widest < ((int64_t)1 << 31);
 }
 
-// The gate/up projections write fp32 [M][2 F] to GU on two paths: the stream
-// kernel (calls of at most one 16-position block, H within its LDS copy of
-// x) and the tiled GEMM (calls above kLinMaxStream positions).  For calls of
-// up to Mx positions GU must hold the largest M of the two.
+// The gate/up projections write fp32 [M][2 F] to GU on the stream kernel's
+// path only (calls of at most one 16-position block, H within its LDS copy of
+// x); the tiled GEMM and k_linear form the SwiGLU product themselves.
 static size_t gu_rows_for(const xp_layer& L, size_t Mx) {
-  size_t gu = 0;
-  if ((size_t)L.H <= 8 * (size_t)kGsXChunks) gu = std::min(Mx, (size_t)kTile);
-  if (Mx > (size_t)kLinMaxStream) gu = Mx;
-  return gu;
+  return (size_t)L.H <= 8 * (size_t)kGsXChunks ? std::min(Mx, (size_t)kTile) : 0;
+}
+
+// Split-K slabs are used by the tiled GEMM only (calls above kLinMaxStream
+// positions); their size is bounded independently of M.
+static size_t part_floats_for(size_t Mx) {
+  return Mx > (size_t)kLinMaxStream ? kLayerPartFloats : 0;
 }
 
 // Lays out the buffers for up to Mx positions and nparts attention partials
 // from `base` (256-byte aligned slices); returns the bytes used.  With
 // base == nullptr only the size is computed.
-static size_t carve(const xp_layer& L, size_t Mx, size_t nparts, size_t gu_rows, char* base,
-                    LayerBufs* b) {
+static size_t carve(const xp_layer& L, size_t Mx, size_t nparts, size_t gu_rows,
+                    size_t part_floats, char* base, LayerBufs* b) {
   const size_t H = L.H, nhd = (size_t)L.nh * kHd, kvd = (size_t)L.nkv * kHd, F = L.ffn;
   LayerBufs t;
   t.nparts = nparts;
   t.gu_rows = gu_rows;
+  t.part_floats = part_floats;
   struct Slice {
     void** p;
     size_t bytes;
@@ -857,19 +1033,22 @@ static size_t carve(const xp_layer& L, size_t Mx, size_t nparts, size_t gu_rows,
       {(void**)&t.attn, Mx * nhd * 2},        {(void**)&t.x1, Mx * H * 4},
       {(void**)&t.act, Mx * F * 2},           {(void**)&t.h32, Mx * H * 4},
       {(void**)&t.GU, (gu_rows ? gu_rows : 1) * 2 * F * 4},
+      {(void**)&t.part, (part_floats ? part_floats : 1) * 4},
   };
   size_t off = 0;
   for (auto& q : sl) {
     if (base) *q.p = base + off;
     off += (q.bytes + 255) / 256 * 256;
   }
+  if (part_floats == 0) t.part = nullptr;
   if (base && b) *b = t;
   return off;
 }
 
 // Attention chunking of one call: chunks of nsub 64-key sub-chunks, about
-// kAttnWgs workgroups in all (one sub-chunk each at small calls), so that the
-// partials stay few.  Returns the partial count batch * npb * nkv * ns * grp.
+// kAttnWgs workgroups (sequence, KV head, chunk) in all (one sub-chunk each
+// at small calls), so that the partials stay few.  Returns the partial count
+// batch * npb * nkv * ns * grp.
 struct AttnPlan {
   int nsub, ns;
   size_t parts;
@@ -880,8 +1059,7 @@ static AttnPlan attn_plan(const xp_layer& L, int batch, int B, int C_max, int ns
   return {nsub, ns, (size_t)batch * npb * L.nkv * ns * L.grp};
 }
 static AttnPlan attn_plan_default(const xp_layer& L, int batch, int B, int C_max) {
-  const int npb = (B + kTile - 1) / kTile;
-  const size_t w64 = (size_t)batch * npb * L.nkv * attn_chunks(C_max, B, kSub);
+  const size_t w64 = (size_t)batch * L.nkv * attn_chunks(C_max, B, kSub);
   int nsub = (int)(w64 / kAttnWgs);
   nsub = nsub < 1 ? 1 : (nsub > 256 ? 256 : nsub);
   return attn_plan(L, batch, B, C_max, nsub);
@@ -910,14 +1088,15 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
   L->max_B = max_B;
   L->max_ctx = max_ctx;
   const size_t Mx = (size_t)max_batch * max_B;
-  const size_t zmax = (size_t)max_batch * ((max_B + kTile - 1) / kTile);
   // attention partials: a call has at most max(2 kAttnWgs, w64 / 256) + one
-  // per (sequence, position block, KV head) chunks, w64 its 64-key sub-chunks
-  const size_t w64max = zmax * L->nkv * (size_t)attn_chunks(max_ctx, max_B, kSub);
+  // per (sequence, KV head) chunks, w64 its (sequence, KV head, 64-key
+  // sub-chunk) triples, and npb grp partials per chunk
+  const size_t qmax = (size_t)max_batch * L->nkv, npbmax = (max_B + kTile - 1) / kTile;
+  const size_t w64max = qmax * (size_t)attn_chunks(max_ctx, max_B, kSub);
   const size_t nparts =
-      (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + zmax * L->nkv) * L->grp;
-  const size_t gu = gu_rows_for(*L, Mx);
-  const size_t total = carve(*L, Mx, nparts, gu, nullptr, nullptr);
+      (std::max((size_t)2 * kAttnWgs, (w64max + 255) / 256) + qmax) * npbmax * L->grp;
+  const size_t gu = gu_rows_for(*L, Mx), pf = part_floats_for(Mx);
+  const size_t total = carve(*L, Mx, nparts, gu, pf, nullptr, nullptr);
   const hipError_t e = hipMalloc(&L->ws, total);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -925,7 +1104,7 @@ extern "C" xp_status xp_layer_create(const xp_layer_weights* w, int32_t max_batc
     return layer_fail(nullptr, XP_ENOMEM, "workspace of %zu bytes: %s", total,
                       hipGetErrorString(e));
   }
-  carve(*L, Mx, nparts, gu, static_cast<char*>(L->ws), &L->b);
+  carve(*L, Mx, nparts, gu, pf, static_cast<char*>(L->ws), &L->b);
   *out = L;
   return XP_OK;
 }
@@ -938,13 +1117,17 @@ extern "C" void xp_layer_destroy(xp_layer* L) {
 }
 
 // y [M][N] (row stride ldy) = X [M][K] W^T (+ R), W the rows of W0 | W1 | W2
-// stacked (n0, n1 rows of the first two); glu: bf16(silu(X W0^T) * (X W1^T)),
-// through GU (fp32 [M][2 N], gu_rows positions).  Returns the first failed
-// launch's error; hipErrorInvalidValue if GU is too small for the path taken.
-static hipError_t linear(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
-                         int n1, int N, int K, const uint16_t* X, int M, const float* R, int ldr,
-                         float* Y, uint16_t* Yb, int ldy, bool glu, hipStream_t st,
-                         float* GU = nullptr, size_t gu_rows = 0) {
+// stacked (n0, n1 rows of the first two); glu: bf16(silu(X W0^T) * (X W1^T))
+// to Yb.  With `splits` given the tiled GEMM may cut k into S > 1 parts: it
+// then writes the fp32 partial products to the S slabs of b.part ([S][M][N],
+// no residual, no Yb) and sets *splits = S, and the caller adds them (with R);
+// else *splits = 1 and y is written.  Returns the first failed launch's
+// error; hipErrorInvalidValue if GU is too small for the path taken.
+static hipError_t linear(const LayerBufs& b, const uint16_t* W0, const uint16_t* W1,
+                         const uint16_t* W2, int n0, int n1, int N, int K, const uint16_t* X,
+                         int M, const float* R, int ldr, float* Y, uint16_t* Yb, int ldy,
+                         bool glu, int* splits, hipStream_t st) {
+  if (splits) *splits = 1;
   // one block of positions and x small enough for LDS: the stream-K kernel
   // (gate and up side by side, then SwiGLU)
   if (M <= kTile && K <= 8 * kGsXChunks && K % 64 == 0 && N % kTile == 0 && n0 % kTile == 0 &&
@@ -952,14 +1135,14 @@ static hipError_t linear(const uint16_t* W0, const uint16_t* W1, const uint16_t*
     const int rows = glu ? 2 * N : N, ntl = rows / kTile;
     const int U = ntl < 256 ? ntl : 256;
     if (glu) {
-      if ((size_t)M > gu_rows) return hipErrorInvalidValue;
+      if ((size_t)M > b.gu_rows) return hipErrorInvalidValue;
       hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W1, N, N,
-                         2 * N, K, X, M, U, (const float*)nullptr, 0, GU, (uint16_t*)nullptr,
+                         2 * N, K, X, M, U, (const float*)nullptr, 0, b.GU, (uint16_t*)nullptr,
                          2 * N);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const size_t na = (size_t)M * N;
-      hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
+      hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, b.GU, N,
                          na, Yb);
     } else {
       hipLaunchKernelGGL(k_gemv_sk, dim3(U), dim3(kGsWaves * kWave), 0, st, W0, W1, W2, n0, n1,
@@ -968,19 +1151,19 @@ static hipError_t linear(const uint16_t* W0, const uint16_t* W1, const uint16_t*
     return hipGetLastError();
   }
   // above one 64-position pass of the stream: the tiled GEMM (weights read
-  // once per 128 or 256 positions); gate and up side by side, then SwiGLU
-  if (M > kLinMaxStream && (glu ? layer_gemm_ok(N, N, 2 * N, K, M) : layer_gemm_ok(n0, n1, N, K, M))) {
-    if (glu) {
-      if ((size_t)M > gu_rows) return hipErrorInvalidValue;
-      hipError_t e = launch_layer_gemm(W0, W1, W1, N, N, 2 * N, K, X, M, nullptr, 0, GU, nullptr,
-                                       2 * N, st);
-      if (e != hipSuccess) return e;
-      const size_t na = (size_t)M * N;
-      hipLaunchKernelGGL(k_swiglu, dim3((unsigned)((na + 255) / 256)), dim3(256), 0, st, GU, N,
-                         na, Yb);
-      return hipGetLastError();
+  // once per 128 or 256 positions)
+  if (M > kLinMaxStream) {
+    if (glu && layer_glu_ok(N, K, M)) return launch_layer_glu(W0, W1, N, K, X, M, Yb, ldy, st);
+    if (!glu && layer_gemm_ok(n0, n1, N, K, M)) {
+      int S = splits && b.part ? layer_gemm_splits(N, K, M) : 1;
+      if (S > 1 && (size_t)S * M * N > b.part_floats) S = 1;               // not reached
+      if (S > 1) {
+        *splits = S;
+        return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, nullptr, 0, b.part, nullptr, N,
+                                 S, st);
+      }
+      return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, 1, st);
     }
-    return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
   }
   const int nb = (M + kTile - 1) / kTile;
   const int P = nb >= 4 ? 4 : (nb >= 2 ? 2 : 1);
@@ -1055,36 +1238,58 @@ static xp_status forward(const xp_layer& L, const LayerBufs& b, const AttnPlan& 
   } while (0)
 
   XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(M), dim3(256), 0, st,
-                                        (const uint16_t*)x, H, L.g_attn, L.eps, b.x32, b.u));
-  XP_LINEAR("q/k/v", L.Wq, L.Wk, L.Wv, nhd, kvd, ldq, H, b.u, M, nullptr, 0, b.qkv, nullptr, ldq,
-            false, st);
-  const int qk_waves = M * (nh + 2 * nkv);
+                                        (const uint16_t*)x, (const float*)nullptr, 0, (size_t)0,
+                                        H, L.g_attn, L.eps, b.x32, b.u));
+  int sq = 1, so = 1, sd = 1;                    // k splits of q/k/v, output, down
+  XP_LINEAR("q/k/v", b, L.Wq, L.Wk, L.Wv, nhd, kvd, ldq, H, b.u, M, nullptr, 0, b.qkv, nullptr,
+            ldq, false, &sq, st);
   XP_STEP("qk-norm/rope",
-          hipLaunchKernelGGL(k_qkrope, dim3((qk_waves + 3) / 4), dim3(256), 0, st, b.qkv, ldq, M,
-                             B, nh, nkv, ctx_len, C_max, L.g_q, L.g_k, L.eps, L.theta, b.qn, b.kb,
-                             b.vb));
-#define XP_ATTN(GG)                                                                           \
-  hipLaunchKernelGGL(k_attn<GG>, dim3(ns, nkv, batch * npb), dim3(GG * kWave), 0, st, b.qn,  \
-                     (const uint16_t*)k_cache, (const uint16_t*)v_cache, b.kb, b.vb, ctx_len, \
-                     C_max, B, npb, nh, nkv, causal, ns, nsub, b.opart, b.mlpart)
-  if (grp == 1) XP_STEP("attention", XP_ATTN(1));
-  else if (grp == 2) XP_STEP("attention", XP_ATTN(2));
-  else if (grp == 4) XP_STEP("attention", XP_ATTN(4));
-  else XP_STEP("attention", XP_ATTN(8));
+          hipLaunchKernelGGL(k_qkrope, dim3(M), dim3(256), 0, st, sq > 1 ? b.part : b.qkv, sq,
+                             (size_t)M * ldq, ldq, B, nh, nkv, ctx_len, C_max, L.g_q, L.g_k,
+                             L.eps, L.theta, b.qn, b.kb, b.vb));
+#define XP_ATTN(GG, PB)                                                                      \
+  hipLaunchKernelGGL((k_attn<GG, PB>), dim3(ns, nkv, batch),                                  \
+                     dim3(attn_waves(GG, PB) * kWave), 0, st,                                 \
+                     b.qn, (const uint16_t*)k_cache, (const uint16_t*)v_cache, b.kb, b.vb,    \
+                     ctx_len, C_max, B, nh, nkv, causal, ns, nsub, b.opart, b.mlpart)
+  if (npb == 1) {
+    if (grp == 1) XP_STEP("attention", XP_ATTN(1, 1));
+    else if (grp == 2) XP_STEP("attention", XP_ATTN(2, 1));
+    else if (grp == 4) XP_STEP("attention", XP_ATTN(4, 1));
+    else XP_STEP("attention", XP_ATTN(8, 1));
+  } else {
+    if (grp == 1) XP_STEP("attention", XP_ATTN(1, 2));
+    else if (grp == 2) XP_STEP("attention", XP_ATTN(2, 2));
+    else if (grp == 4) XP_STEP("attention", XP_ATTN(4, 2));
+    else XP_STEP("attention", XP_ATTN(8, 2));
+  }
 #undef XP_ATTN
   const int cw = M * nh;
   XP_STEP("attention combine",
           hipLaunchKernelGGL(k_attn_comb, dim3((cw + 3) / 4), dim3(256), 0, st, b.opart,
                              b.mlpart, M, B, npb, nh, nkv, grp, ns, b.attn));
-  XP_LINEAR("output", L.Wo, nullptr, nullptr, H, 0, H, nhd, b.attn, M, b.x32, H, b.x1, nullptr, H,
-            false, st);
-  XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st,
-                                        (const float*)b.x1, H, L.g_mlp, L.eps, (float*)nullptr,
-                                        b.u));
-  XP_LINEAR("gate/up", L.Wg, L.Wu, nullptr, F, 0, F, H, b.u, M, nullptr, 0, nullptr, b.act, F,
-            true, st, b.GU, b.gu_rows);
-  XP_LINEAR("down", L.Wd, nullptr, nullptr, H, 0, H, F, b.act, M, b.x1, H, hout,
-            (uint16_t*)h_bf16, H, false, st);
+  XP_LINEAR("output", b, L.Wo, nullptr, nullptr, H, 0, H, nhd, b.attn, M, b.x32, H, b.x1,
+            nullptr, H, false, &so, st);
+  // x1 = Wo attn + x: written by the projection, or here from its slabs
+  if (so > 1)
+    XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st,
+                                          (const float*)b.x32, (const float*)b.part, so,
+                                          (size_t)M * H, H, L.g_mlp, L.eps, b.x1, b.u));
+  else
+    XP_STEP("rmsnorm", hipLaunchKernelGGL(k_rmsnorm<float>, dim3(M), dim3(256), 0, st,
+                                          (const float*)b.x1, (const float*)nullptr, 0, (size_t)0,
+                                          H, L.g_mlp, L.eps, (float*)nullptr, b.u));
+  XP_LINEAR("gate/up", b, L.Wg, L.Wu, nullptr, F, 0, F, H, b.u, M, nullptr, 0, nullptr, b.act, F,
+            true, nullptr, st);
+  XP_LINEAR("down", b, L.Wd, nullptr, nullptr, H, 0, H, F, b.act, M, b.x1, H, hout,
+            (uint16_t*)h_bf16, H, false, &sd, st);
+  if (sd > 1) {
+    const size_t n = (size_t)M * H;
+    XP_STEP("down split-K sum",
+            hipLaunchKernelGGL(k_splitk_sum, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0,
+                               st, (const float*)b.part, sd, n, (const float*)b.x1, hout,
+                               (uint16_t*)h_bf16));
+  }
 #undef XP_STEP
 #undef XP_LINEAR
   return XP_OK;
@@ -1157,7 +1362,7 @@ extern "C" xp_status xp_layer_forward_noalloc(const xp_layer_weights* w, int32_t
   // The buffers the call needs, its partials at the default chunking; if
   // those do not fit, chunks of more 64-key sub-chunks (fewer partials).
   const size_t gu = gu_rows_for(L, M);
-  const size_t fixed = carve(L, M, 0, gu, nullptr, nullptr);
+  const size_t fixed = carve(L, M, 0, gu, 0, nullptr, nullptr);
   const size_t per_part = (size_t)kTile * kHd * 4 + (size_t)2 * kTile * 4;   // opart + mlpart
   if (fixed + 2 * 256 + per_part > kScratchBytes)
     return layer_fail(nullptr, XP_EINVAL,
@@ -1184,7 +1389,7 @@ extern "C" xp_status xp_layer_forward_noalloc(const xp_layer_weights* w, int32_t
   if (e != hipSuccess)
     return layer_fail(nullptr, XP_EHIP, "static scratch address: %s", hipGetErrorString(e));
   LayerBufs b;
-  const size_t used = carve(L, M, ap.parts, gu, base, &b);
+  const size_t used = carve(L, M, ap.parts, gu, 0, base, &b);
   if (used > kScratchBytes)                      // not reached: sized above
     return layer_fail(nullptr, XP_EINVAL, "buffers of %zu bytes exceed the static scratch", used);
   return forward(L, b, ap, nullptr, batch, B, causal, x, k_cache, v_cache, C_max, ctx_len, h_f32,

@@ -5,19 +5,23 @@ Small shapes span several k-split chunks of every projection, several
 attention chunks (64-key ones for small calls, 128-key ones for large) with
 ragged context lengths (0, chunk boundaries),
 every built query-group size, blocks of 1, 8, 16 and 32 positions, and the
-three projection paths (streaming up to 64 positions, the tiled GEMM with
-128 x 128 tiles, and 256 x 256 ones where a launch has 512 of them or more);
+projection paths (streaming up to 64 positions, the tiled GEMM with 128 x 128
+tiles, split over k where those are fewer than the CUs, and 256 x 256 ones
+where a launch has 512 of them or more);
 the full-size case runs the
 Qwen3-8B layer at batch 1 with a 2048-key context.
 
 Tolerance: h is compared in fp32 against the oracle's fp64 h with the bf16
 rounding points of the device (u, q, k, v, the attention output, u2 and the
 SwiGLU activation); what remains is fp32 accumulation order, the softmax
-numerators of P.V (two bf16 parts each) and the rare bf16 rounding that the fp32 and fp64
-values of an intermediate take to different neighbours.  The bar is the
-2e-2 absolute of bf16 logits; with the numerators in one bf16 part instead of
-two the Qwen3-shape case would reach 0.020 (measured in the oracle), with two
-it stays near 1e-3.
+numerators of P.V (two bf16 parts each) and the rare bf16 rounding that the
+fp32 and fp64 values of an intermediate take to different neighbours.  That
+remainder is not the device's own: the oracle's steps evaluated in fp32 with
+the same rounding points (tests/layer_fp32_floor.py) lie up to 0.0196 from
+the fp64 result at the batch-64 shape, 1.6e-3 of its largest |h| (12.3).  The
+bar is therefore one bf16 unit at the output's scale, 2^-8 max|h|, and never
+below the 2e-2 absolute of bf16 logits: 2e-2 on the small shapes, 0.048 at
+|h| = 12.3, 2.4 times the fp32 floor.
 """
 import numpy as np
 import pytest
@@ -67,9 +71,11 @@ def _check(w, weights, inp, h32, hb_bits, causal=True, seqs=None):
     ref = O.layer_ref.layer_forward(P, inp.x[sl], inp.k_cache[sl], inp.v_cache[sl],
                                     inp.ctx_len[sl], causal)
     err = np.abs(h32[sl] - ref)
-    _say(f"  max|h|={np.abs(ref).max():.3g} max|dh|={err.max():.3g} mean|dh|={err.mean():.3g}")
+    bar = max(ATOL, 2.0 ** -8 * float(np.abs(ref).max()))
+    _say(f"  max|h|={np.abs(ref).max():.3g} max|dh|={err.max():.3g} mean|dh|={err.mean():.3g} "
+         f"bar={bar:.3g}")
     assert np.all(np.isfinite(h32))
-    assert err.max() <= ATOL
+    assert err.max() <= bar
     # the bf16 output is the rounding of the fp32 one
     assert np.array_equal(hb_bits, synth.f32_to_bf16_bits(h32))
 
@@ -109,6 +115,20 @@ def test_layer_projections_as_gemm_with_128_tiles():
     ctx = [5, 700, 33, 0, 256, 1000, 64, 129, 300, 2, 511, 90]
     _say(f"case: layer GEMM path H=512 heads 8/2 ffn=512 B=16 batch=12 ctx={ctx}")
     w, weights, inp = _case(512, 8, 2, 512, 16, 12, ctx, index=833)
+    h32, hb, layer, _ = _run(w, weights, inp)
+    _check(w, weights, inp, h32, hb)
+    layer.close()
+
+
+def test_layer_projections_split_over_k():
+    """96 positions at H = 1024, ffn = 2048: the tiled GEMM's 128 x 128 tiles
+    are fewer than the CUs, so the q/k/v (12 tiles, K = 1024), output (8
+    tiles, K = 1024) and down (8 tiles, K = 2048) projections cut k into 2, 2
+    and 4 parts whose slabs the next kernel adds; the gate/up projection
+    forms the SwiGLU product in its epilogue."""
+    ctx = [0, 129, 1000, 64, 7, 513]
+    _say(f"case: layer split-K H=1024 heads 8/2 ffn=2048 B=16 batch=6 ctx={ctx}")
+    w, weights, inp = _case(1024, 8, 2, 2048, 16, 6, ctx, index=845)
     h32, hb, layer, _ = _run(w, weights, inp)
     _check(w, weights, inp, h32, hb)
     layer.close()
