@@ -516,10 +516,10 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {   // p: an L
 // times KH = 2 key halves where that leaves at most eight (the two waves of a
 // pair take keys 0..31 and 32..63 of every sub-chunk with their own running
 // maximum, sum and O, merged at the end), so that a CU holds enough waves to
-// hide each one's latency.  The LDS ring has NS = 2 stages (64 KB, two
-// workgroups per CU), 3 for 16 waves (96 KB, one workgroup per CU, which
-// also holds the eight pairs' merge).
-__host__ __device__ constexpr int attn_halves(int grp, int npb) { return grp * npb <= 8 ? 2 : 1; }
+// hide each one's latency (with eight pairs the halves' extra registers cost
+// more than they hide: measured).  The LDS ring has NS = 2 stages (64 KB, two
+// workgroups per CU), 3 for 16 waves (96 KB, one workgroup per CU).
+__host__ __device__ constexpr int attn_halves(int grp, int npb) { return grp * npb <= 4 ? 2 : 1; }
 __host__ __device__ constexpr int attn_waves(int grp, int npb) {
   return grp * npb * attn_halves(grp, npb);
 }
