@@ -123,18 +123,21 @@ hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, cons
                          bool front, hipStream_t st);
 bool pass_fused_ok(const xp_handle* h, const uint8_t* temp);
 int gemm_units(const xp_handle* h, int M);
-// the context layer's projections for many positions (xp_lgemm.hip): plain
-// (S = 1) or split-K into S slabs of [M][N] fp32 partial products (Y, with
-// R = Yb = NULL), and the gate/up projections with the SwiGLU product
+// the context layer's projections for many positions (xp_lgemm.hip): tile
+// size bn (128 or 256; 0: no plan) and S k splits; with S > 1 the launch
+// writes S slabs of [M][N] fp32 partial products (Y, with R = Yb = NULL);
+// the gate/up projections form the SwiGLU product (S = 1)
 constexpr int kLayerSplitMax = 8;
-constexpr size_t kLayerPartFloats = (size_t)256 * 128 * 128;   // bound of S M N
-bool layer_gemm_ok(int n0, int n1, int N, int K, int M);
-bool layer_glu_ok(int F, int K, int M);
-int layer_gemm_splits(int N, int K, int M);
-hipError_t launch_layer_gemm(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
-                             int n1, int N, int K, const uint16_t* X, int M, const float* R,
-                             int ldr, float* Y, uint16_t* Yb, int ldy, int S, hipStream_t st);
-hipError_t launch_layer_glu(const uint16_t* Wg, const uint16_t* Wu, int F, int K,
+constexpr size_t kLayerPartFloats = (size_t)16 << 20;   // slab values a layer holds (64 MB)
+struct LayerPlan {
+  int bn, S;
+};
+LayerPlan layer_plan(int n0, int n1, int N, int K, int M, bool glu, size_t part_floats);
+hipError_t launch_layer_gemm(LayerPlan pl, const uint16_t* W0, const uint16_t* W1,
+                             const uint16_t* W2, int n0, int n1, int N, int K, const uint16_t* X,
+                             int M, const float* R, int ldr, float* Y, uint16_t* Yb, int ldy,
+                             hipStream_t st);
+hipError_t launch_layer_glu(LayerPlan pl, const uint16_t* Wg, const uint16_t* Wu, int F, int K,
                             const uint16_t* X, int M, uint16_t* act, int ldy, hipStream_t st);
 int gemm_units_max(const xp_handle* h);
 bool lmhead_gemm_ok(const xp_handle* h, int M);

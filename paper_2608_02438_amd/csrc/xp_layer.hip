@@ -1153,16 +1153,17 @@ static hipError_t linear(const LayerBufs& b, const uint16_t* W0, const uint16_t*
   // above one 64-position pass of the stream: the tiled GEMM (weights read
   // once per 128 or 256 positions)
   if (M > kLinMaxStream) {
-    if (glu && layer_glu_ok(N, K, M)) return launch_layer_glu(W0, W1, N, K, X, M, Yb, ldy, st);
-    if (!glu && layer_gemm_ok(n0, n1, N, K, M)) {
-      int S = splits && b.part ? layer_gemm_splits(N, K, M) : 1;
-      if (S > 1 && (size_t)S * M * N > b.part_floats) S = 1;               // not reached
-      if (S > 1) {
-        *splits = S;
-        return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, nullptr, 0, b.part, nullptr, N,
-                                 S, st);
+    const size_t pf = splits && b.part ? b.part_floats : 0;   // no slabs: S = 1
+    const LayerPlan pl = glu ? layer_plan(N, N, 2 * N, K, M, true, 0)
+                             : layer_plan(n0, n1, N, K, M, false, pf);
+    if (pl.bn != 0) {
+      if (glu) return launch_layer_glu(pl, W0, W1, N, K, X, M, Yb, ldy, st);
+      if (pl.S > 1) {
+        *splits = pl.S;
+        return launch_layer_gemm(pl, W0, W1, W2, n0, n1, N, K, X, M, nullptr, 0, b.part, nullptr,
+                                 N, st);
       }
-      return launch_layer_gemm(W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, 1, st);
+      return launch_layer_gemm(pl, W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
     }
   }
   const int nb = (M + kTile - 1) / kTile;

@@ -11,21 +11,18 @@
 //
 // Above one 64-position pass of the streaming projection kernel the weights
 // would be re-read per 64 positions; here a tile is BN weight rows x BM
-// positions (256 x 256 where every workgroup then gets two tiles or more, else
-// 128 x 128), so every weight is read once per BM positions.  Where the 128 x
-// 128 tiles are fewer than the CUs (the output and down projections of a few
-// hundred positions), split-K multiplies the work items up to one per CU.  Up
-// to three weights stacked by rows share the launch (the q, k and v
-// projections of one input); BN divides each one's row count, so a tile never
-// straddles two of them.  Persistent and XCD-aware as the LM-head GEMM
+// positions (128 x 128 or 256 x 256, layer_plan), so every weight is read
+// once per BM positions.  Where the tiles are fewer than the CUs (the output
+// and down projections of a few hundred positions), split-K multiplies the
+// work items up to one per CU.  Up to three weights stacked by rows share the
+// launch (the q, k and v projections of one input); BN divides each one's
+// row count, so a tile never straddles two of them.  Persistent and XCD-aware as the LM-head GEMM
 // (GemmSched), over the virtual row tiles rt S + s.
 #include "xp_internal.h"
 #include "xp_gemm_pipe.h"
 
 namespace xp {
 
-static_assert(kLayerPartFloats == (size_t)8 * kGPerXcd * 128 * 128,
-              "split-K slabs: one 128 x 128 tile per workgroup of the persistent grid");
 
 // Rows of tile ti (virtual row tile v = sc.tile(ti) = rt S + s, k from s kt).
 // Plain: BN consecutive rows of whichever of W0 | W1 | W2 holds stacked row
@@ -154,67 +151,75 @@ __global__ __launch_bounds__(kGWaves * kWave) void k_layer_gemm(
   gemm_tiles<BN, BM>(rows, epi, X, K, M, kt, ntl, p0, lds);
 }
 
-// Position and row tile size: 256 x 256 only when that still gives every
-// workgroup of the persistent grid two tiles or more; else 128 x 128 (four
-// times as many tiles for the same work).
-static int layer_bm(int N, int M) {
-  const long t256 = (long)(N / 256) * ((M + 255) / 256);
-  return M <= 128 || t256 < 2 * 8 * kGPerXcd ? 128 : 256;
-}
-
-bool layer_gemm_ok(int n0, int n1, int N, int K, int M) {
-  const int bn = layer_bm(N, M);
-  return K % kGK == 0 && N % bn == 0 && n0 % bn == 0 && n1 % bn == 0 && M >= 1;
-}
-
-bool layer_glu_ok(int F, int K, int M) {
-  const int bn = layer_bm(2 * F, M);
-  return K % kGK == 0 && F % (bn / 2) == 0 && M >= 1;
-}
-
-// k splits of a plain projection: the largest S <= kLayerSplitMax with at
-// most one 128 x 128 tile per workgroup of the persistent grid, S dividing
-// the k steps and at least 16 k steps per split (1: no split).  S M N stays
-// within kLayerPartFloats.
-int layer_gemm_splits(int N, int K, int M) {
-  if (layer_bm(N, M) != 128 || K % kGK != 0) return 1;
-  const long nt = (long)(N / 128) * ((M + 127) / 128);
-  const int nk = K / kGK;
-  int S = 1;
-  for (int c = 2; c <= kLayerSplitMax; ++c)
-    if (nt * c <= 8 * kGPerXcd && nk % c == 0 && nk / c >= 16) S = c;
-  return S;
+// Tile size and k splits of one projection: among 128 x 128 and 256 x 256
+// tiles (BN dividing every stacked weight's rows) and S = 1 .. kLayerSplitMax
+// splits (S dividing the k steps, at least 16 k steps per split, S M N fp32
+// slab values within part_floats; GLU: S = 1), the one with the least
+// estimated time: rounds of one work item per workgroup of the persistent
+// grid, an item costing 17 us plus its flops at 3.6 TFLOP/s per CU on 128 x
+// 128 tiles or 4.3 on 256 x 256 (fitted to the measured launches of the
+// Qwen3-8B projections at 128 to 2048 positions), plus one read of the slabs
+// at 5 TB/s by the kernel that adds them.  bn = 0: no plan (K not a multiple
+// of 32 or no tile divides the rows).
+LayerPlan layer_plan(int n0, int n1, int N, int K, int M, bool glu, size_t part_floats) {
+  LayerPlan best{0, 1};
+  if (K % kGK != 0 || M < 1) return best;
+  const int nk = K / kGK, slots = 8 * kGPerXcd;
+  double tbest = 0.0;
+  for (int bn = 128; bn <= 256; bn *= 2) {
+    if (N % bn != 0 || n0 % bn != 0 || n1 % bn != 0) continue;
+    const double rate = bn == 128 ? 3.6e12 : 4.3e12;
+    const long tiles = (long)(N / bn) * ((M + bn - 1) / bn);
+    for (int S = 1; S <= (glu ? 1 : kLayerSplitMax); ++S) {
+      if (nk % S != 0 || (S > 1 && nk / S < 16)) continue;
+      if (S > 1 && (double)S * M * N > (double)part_floats) continue;
+      const long items = tiles * S;
+      const double rounds = (double)((items + slots - 1) / slots);
+      double t = rounds * (17e-6 + 2.0 * bn * bn * (double)(K / S) / rate);
+      if (S > 1) t += 4.0 * S * (double)M * N / 5e12;
+      if (best.bn == 0 || t < tbest) {
+        best = LayerPlan{bn, S};
+        tbest = t;
+      }
+    }
+  }
+  return best;
 }
 
 template <bool GLU>
-static void launch(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0, int n1,
-                   int N, int K, int S, const uint16_t* X, int M, const float* R, int ldr,
+static void launch(LayerPlan pl, const uint16_t* W0, const uint16_t* W1, const uint16_t* W2,
+                   int n0, int n1, int N, int K, const uint16_t* X, int M, const float* R, int ldr,
                    float* Y, uint16_t* Yb, int ldy, hipStream_t st) {
-  const int bm = layer_bm(N, M);
+  const int bm = pl.bn;
   const int nMb = (M + bm - 1) / bm;
   const int per = gemm_per_xcd(nMb);              // workgroups per XCD: whole position groups
   const int gpx = per / nMb;
   const size_t slab = (size_t)M * ldy;
   if (bm == 128)
     hipLaunchKernelGGL((k_layer_gemm<128, 128, GLU>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
-                       W0, W1, W2, n0, n1, N, K, S, X, M, nMb, gpx, R, ldr, Y, slab, Yb, ldy);
+                       W0, W1, W2, n0, n1, N, K, pl.S, X, M, nMb, gpx, R, ldr, Y, slab, Yb, ldy);
   else
     hipLaunchKernelGGL((k_layer_gemm<256, 256, GLU>), dim3(8 * per), dim3(kGWaves * kWave), 0, st,
-                       W0, W1, W2, n0, n1, N, K, S, X, M, nMb, gpx, R, ldr, Y, slab, Yb, ldy);
+                       W0, W1, W2, n0, n1, N, K, pl.S, X, M, nMb, gpx, R, ldr, Y, slab, Yb, ldy);
 }
 
-hipError_t launch_layer_gemm(const uint16_t* W0, const uint16_t* W1, const uint16_t* W2, int n0,
-                             int n1, int N, int K, const uint16_t* X, int M, const float* R,
-                             int ldr, float* Y, uint16_t* Yb, int ldy, int S, hipStream_t st) {
-  if (S < 1 || K % (S * kGK) != 0 || (S > 1 && (R || Yb || !Y || ldy != N)))
+hipError_t launch_layer_gemm(LayerPlan pl, const uint16_t* W0, const uint16_t* W1,
+                             const uint16_t* W2, int n0, int n1, int N, int K, const uint16_t* X,
+                             int M, const float* R, int ldr, float* Y, uint16_t* Yb, int ldy,
+                             hipStream_t st) {
+  if ((pl.bn != 128 && pl.bn != 256) || pl.S < 1 || K % (pl.S * kGK) != 0 || N % pl.bn != 0 ||
+      n0 % pl.bn != 0 || n1 % pl.bn != 0 || (pl.S > 1 && (R || Yb || !Y || ldy != N)))
     return hipErrorInvalidValue;
-  launch<false>(W0, W1, W2, n0, n1, N, K, S, X, M, R, ldr, Y, Yb, ldy, st);
+  launch<false>(pl, W0, W1, W2, n0, n1, N, K, X, M, R, ldr, Y, Yb, ldy, st);
   return hipGetLastError();
 }
 
-hipError_t launch_layer_glu(const uint16_t* Wg, const uint16_t* Wu, int F, int K,
+hipError_t launch_layer_glu(LayerPlan pl, const uint16_t* Wg, const uint16_t* Wu, int F, int K,
                             const uint16_t* X, int M, uint16_t* act, int ldy, hipStream_t st) {
-  launch<true>(Wg, Wu, Wu, F, F, 2 * F, K, 1, X, M, nullptr, 0, nullptr, act, ldy, st);
+  if ((pl.bn != 128 && pl.bn != 256) || pl.S != 1 || K % kGK != 0 || (2 * F) % pl.bn != 0 ||
+      F % pl.bn != 0)
+    return hipErrorInvalidValue;
+  launch<true>(pl, Wg, Wu, Wu, F, F, 2 * F, K, X, M, nullptr, 0, nullptr, act, ldy, st);
   return hipGetLastError();
 }
 
