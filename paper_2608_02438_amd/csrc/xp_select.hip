@@ -43,11 +43,14 @@ __device__ __forceinline__ float wave_max(float x) {
 // Every wave loads all of its unit partials at once, and the crossing unit's
 // logits are recomputed by one wave per tile into LDS before one wave scans
 // them, so a selection costs a few memory round trips.
+// CH is the number of 64-unit chunks a wave holds, ceil(U / 512): the
+// partition's size, not the largest one supported, so no fp64 exponential or
+// scan runs on masked lanes and the registers allow more workgroups per CU.
 constexpr int kSmpWaves = 8;
-constexpr int kSmpChunks = 8;        // 64-unit chunks per wave: up to 4096 units
+constexpr int kSmpChunks = 8;        // 64-unit chunks per wave at most: up to 4096 units
 constexpr int kSmpRows = 128;        // rows of the largest unit (8 tiles)
 
-template <typename T>
+template <typename T, int CH>
 __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
     int mode, int B, int V, int M, const float* __restrict__ S, int Ms,
     const T* __restrict__ W_r, const T* __restrict__ Z, const Stat* __restrict__ stats,
@@ -68,16 +71,16 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
 
   // wave w owns the units [ua, ub) (in order), all loaded at once
   const int ua = (int)((int64_t)U * wave / kSmpWaves), ub = (int)((int64_t)U * (wave + 1) / kSmpWaves);
-  Stat q[kSmpChunks];
+  Stat q[CH];
 #pragma unroll
-  for (int j = 0; j < kSmpChunks; ++j) {
+  for (int j = 0; j < CH; ++j) {
     const int i = ua + 64 * j + lane;
     q[j] = stats[(size_t)p * U + (i < ub ? i : (ub > 0 ? ub - 1 : 0))];
     if (i >= ub) q[j] = stat_empty();
   }
   float m = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < kSmpChunks; ++j)
+  for (int j = 0; j < CH; ++j)
     if (q[j].s > 0.f) m = fmaxf(m, q[j].m);
   m = wave_max(m);
   if (lane == 0) wmax[wave] = m;
@@ -87,10 +90,10 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
   for (int w = 1; w < kSmpWaves; ++w) m = fmaxf(m, wmax[w]);
 
   // unit masses sum_u e^{max_u - m} in fp64; in-order wave scans per chunk
-  double incl[kSmpChunks], carry_before[kSmpChunks];
+  double incl[CH], carry_before[CH];
   double carry = 0.0;
 #pragma unroll
-  for (int j = 0; j < kSmpChunks; ++j) {
+  for (int j = 0; j < CH; ++j) {
     const double w = q[j].s > 0.f ? (double)q[j].s * exp((double)q[j].m - (double)m) : 0.0;
     incl[j] = wave_incl_scan(w, lane);
     carry_before[j] = carry;
@@ -130,7 +133,7 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
     double pre = start + carry;
     bool found = false;
 #pragma unroll
-    for (int j = 0; j < kSmpChunks; ++j) {
+    for (int j = 0; j < CH; ++j) {
       const int base = ua + 64 * j;
       const double tot = start + (carry_before[j] + incl[j]);
       const unsigned long long hit = __ballot(!found && base + lane < ub && tot > target);
@@ -318,16 +321,31 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
       const hipError_t e = launch_fsample(h, batch, pass, flags, seed_ids, u_draft, st);
       if (e != hipSuccess) return e;
     }
-    if (h->dtype == XP_BF16)
-      hipLaunchKernelGGL((k_sample<uint16_t>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
-                         h->V, M, h->ws.s, M, (const uint16_t*)h->W_r, (const uint16_t*)h->ws.z,
-                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
-                         Ynew, h->ws.lse, h->ws.iters, early, h->ws.invT);
-    else
-      hipLaunchKernelGGL((k_sample<float>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,
-                         h->V, M, h->ws.s, M, (const float*)h->W_r, (const float*)h->ws.z,
-                         h->ws.stats, h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft,
-                         Ynew, h->ws.lse, h->ws.iters, early, h->ws.invT);
+    // 64-unit chunks per wave (xp_create keeps U within kSmpWaves * 64 * kSmpChunks)
+    const int ch = (U + kSmpWaves * kWave - 1) / (kSmpWaves * kWave);
+#define XP_SMP(TT, CC)                                                                        \
+  hipLaunchKernelGGL((k_sample<TT, CC>), dim3(M), dim3(kSmpWaves * kWave), 0, st, mode, h->B,  \
+                     h->V, M, h->ws.s, M, (const TT*)h->W_r, (const TT*)h->ws.z, h->ws.stats,  \
+                     h->ntiles, U, mode == 0 ? seed_ids : nullptr, tsmp, u_draft, Ynew,        \
+                     h->ws.lse, h->ws.iters, early, h->ws.invT)
+#define XP_SMP_CH(TT)                                                                         \
+  switch (ch) {                                                                               \
+    case 1: XP_SMP(TT, 1); break;                                                             \
+    case 2: XP_SMP(TT, 2); break;                                                             \
+    case 3: XP_SMP(TT, 3); break;                                                             \
+    case 4: XP_SMP(TT, 4); break;                                                             \
+    case 5: XP_SMP(TT, 5); break;                                                             \
+    case 6: XP_SMP(TT, 6); break;                                                             \
+    case 7: XP_SMP(TT, 7); break;                                                             \
+    default: XP_SMP(TT, 8);                                                                   \
+  }
+    if (h->dtype == XP_BF16) {
+      XP_SMP_CH(uint16_t)
+    } else {
+      XP_SMP_CH(float)
+    }
+#undef XP_SMP_CH
+#undef XP_SMP
   }
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_select<uint16_t>), dim3(batch), dim3(kSelWaves * kWave), 0, st, mode, pass, batch,
