@@ -260,21 +260,25 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     int Ms, int V, int M, int ntiles, int U, uint64_t* __restrict__ keys,
     Stat* __restrict__ stats, const uint8_t* __restrict__ temp, int B,
     float* __restrict__ out_logits, const int32_t* __restrict__ ctrl, int skip_when_done,
-    int nwg, int ny, const float* __restrict__ invT, const int32_t* __restrict__ iters) {
+    int nwg, int ny, int gs, const float* __restrict__ invT, const int32_t* __restrict__ iters) {
   static_assert(kReadWaves == 8, "one 1 KB load per wave fills a 16-row tile");
   if (skip_when_done && ctrl[1]) return;          // every sequence is at its fixed point
   using RT = ReadTile<uint16_t>;
   constexpr int NU = RT::NU;
   constexpr int WSL = 512, SSL = kReadWaves * P * 64;          // 16-byte slots per stage
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  // workgroup b runs on XCD b % 8; the ny position groups of one read
-  // workgroup g are b = 8 (ny (g / 8) + y) + g % 8, y < ny: the same XCD at
-  // about the same time, so W_r tiles read by the first come from L2 for the
-  // others
+  // A workgroup takes the gs consecutive read workgroups [g_lo, g_hi) (their
+  // tiles in order, one key row per read workgroup) for position group py.
+  // Workgroup b runs on XCD b % 8; the ny position groups of one group of
+  // read workgroups sg are b = 8 (ny (sg / 8) + y) + sg % 8, y < ny: the
+  // same XCD at about the same time, so W_r tiles read by the first come
+  // from L2 for the others
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int g = (slot / ny) * 8 + xcd, py = slot - (slot / ny) * ny;
-  if (g >= nwg) return;                           // whole workgroup
-  const int u_lo = g * kReadWaves, u_hi = u_lo + kReadWaves;
+  const int sg = (slot / ny) * 8 + xcd, py = slot - (slot / ny) * ny;
+  const int g_lo = sg * gs;
+  if (g_lo >= nwg) return;                        // whole workgroup
+  const int g_hi = min(nwg, g_lo + gs);
+  const int u_lo = g_lo * kReadWaves, u_hi = g_hi * kReadWaves;
   const int t0 = unit_tile_lo(u_lo, ntiles, U), n = unit_tile_lo(u_hi, ntiles, U) - t0;
   const int pw = py * (kReadWaves * kTile * P) + wave * (kTile * P);
   // as many stages as fit: the deeper the ring, the more tiles are in flight
@@ -339,6 +343,25 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     bi[pb] = 0xFFFFFFFFu;
     st[pb] = stat_empty();
   }
+  // the key row of every read workgroup that ends at or before tile boundary
+  // tend, from the running maxima, which then restart
+  int gc = g_lo, ge = unit_tile_lo((g_lo + 1) * kReadWaves, ntiles, U);
+  auto flush_keys = [&](int tend) {
+    while (gc < g_hi && ge <= tend) {             // wave-uniform
+#pragma unroll
+      for (int pb = 0; pb < P; ++pb) {
+        uint64_t best = bi[pb] == 0xFFFFFFFFu ? kKeyMin : argmax_key(bv[pb], bi[pb]);
+#pragma unroll
+        for (int m = 16; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
+        const int p = pw + kTile * pb + (lane & 15);
+        if (lane < 16 && act[pb] && !wdead) keys[(size_t)gc * M + p] = best;
+        bv[pb] = (act[pb] && !sample[pb]) ? -INFINITY : INFINITY;
+        bi[pb] = 0xFFFFFFFFu;
+      }
+      ++gc;
+      ge = unit_tile_lo((gc + 1) * kReadWaves, ntiles, U);
+    }
+  };
 
   // loads of tile j (clamped into the range, so that every wave issues the
   // same number of loads per tile) into stage j % kRmStages
@@ -387,6 +410,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
   };
 
   flush_until(t0);                                // units without tiles
+  flush_keys(t0);                                 // read workgroups without tiles
 #pragma unroll
   for (int j = 0; j < kRmStages - 1; ++j) issue(j);
   constexpr int kPend = (kRmStages - 2) * (1 + P); // loads of the later tiles
@@ -453,16 +477,9 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
       }
     }
     flush_until(t + 1);
+    flush_keys(t + 1);
   }
   __builtin_amdgcn_s_waitcnt(0x0070);             // the clamped loads past the end
-#pragma unroll
-  for (int pb = 0; pb < P; ++pb) {
-    uint64_t best = bi[pb] == 0xFFFFFFFFu ? kKeyMin : argmax_key(bv[pb], bi[pb]);
-#pragma unroll
-    for (int m = 16; m < 64; m <<= 1) best = umax64(best, shfl_xor_u64(best, m));
-    const int p = pw + kTile * pb + (lane & 15);
-    if (lane < 16 && act[pb] && !wdead) keys[(size_t)g * M + p] = best;
-  }
 }
 
 hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const uint8_t* temp,
@@ -477,13 +494,17 @@ hipError_t launch_read(xp_handle* h, int batch, int pass, uint32_t flags, const 
     int P = (M + per - 1) / per;
     P = P < kRmMaxP ? P : kRmMaxP;
     const int ny = (M + per * P - 1) / (per * P);
-    grid = dim3((h->read_wgs + 7) / 8 * 8 * ny);
+    // one workgroup per CU and position group at most: a workgroup takes gs
+    // read workgroups in a row, so that the launch runs in one round
+    const int gs = ny;
+    const int nsg = (h->read_wgs + gs - 1) / gs;
+    grid = dim3((nsg + 7) / 8 * 8 * ny);
     const uint16_t* Wr = (const uint16_t*)h->W_r;
     const uint16_t* Zb = (const uint16_t*)h->ws.z;
 #define XP_RM(PP, EEV)                                                                       \
   hipLaunchKernelGGL((k_read_multi<PP, EEV>), grid, block, 0, st, Wr, Zb, h->ws.s, M, h->V, M, \
                      h->ntiles, h->read_units, h->ws.keys, h->ws.stats, temp, h->B, out_logits, \
-                     h->ws.ctrl, skip, h->read_wgs, ny, h->ws.invT, h->ws.iters)
+                     h->ws.ctrl, skip, h->read_wgs, ny, gs, h->ws.invT, h->ws.iters)
     if (skip) {
       switch (P) {
         case 1: XP_RM(1, true); break;
