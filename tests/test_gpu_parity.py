@@ -206,6 +206,18 @@ def test_lmhead_gemm_and_read_multi_ragged_positions(batch, temp):
     _full_check(prob, ref, upload(prob), min_exact=0.97)
 
 
+def test_read_multi_workgroups_spanning_several_read_groups():
+    """1536 positions (B = 32): three position groups of 512, so each Read
+    workgroup walks the tiles of three read workgroups in a row and flushes a
+    key row at each of their boundaries; V = 2000 gives 16 read workgroups
+    (the last group of three holds one) and units of one tile or none."""
+    _say("case: read_multi over groups of read workgroups, bf16 H=512 V=2000 B=32 batch=48 K=4")
+    prob = custom_problem("bf16", H=512, V=2000, B=32, batch=48, K=4, sigmas=STRESS,
+                          temp="mixed", seed=97)
+    ref = make_refiner(prob)
+    _full_check(prob, ref, upload(prob), min_exact=0.97)
+
+
 @pytest.mark.parametrize("B,batch", [(16, 4), (8, 3)])
 def test_fused_greedy_pass_matches_separate_kernels(B, batch):
     """All-greedy batches run selection + Fuse + Mix + W_1 as one kernel; an
