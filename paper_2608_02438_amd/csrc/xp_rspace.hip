@@ -444,6 +444,88 @@ __global__ __launch_bounds__(256) void k_trans2(int B, const T* __restrict__ W2,
 }
 
 // ---------------------------------------------------------------------------
+// The two Trans products for many positions (bf16 weights, M >= kTransTiled):
+// MODE 0 h1 = silu(W_1 c) (K = r), MODE 1 z = bf16(c + W_2 h1) (K = 2r).  The
+// per-sequence kernels above re-read a sequence's inputs once per 16-row
+// tile; here a workgroup takes 64 output rows x 32 positions, stages the
+// positions' fp32 inputs once in LDS (rows padded by 16 bytes, so the 16
+// positions of a fragment read fall in different banks), and each wave holds
+// its 16 weight rows for the whole contraction in registers.  Products are
+// the same exact split-term products, summed in fp32 in k order.  The
+// results of sequences already at their fixed point are recomputed from
+// unchanged inputs, so they do not change; a launch after the whole batch
+// converged returns at once.
+// ---------------------------------------------------------------------------
+constexpr int kTransTiled = 1024;      // positions from which the tiled kernels run
+constexpr int kTransPT = 32;           // positions per workgroup
+
+template <int K, int MODE>
+__global__ __launch_bounds__(256) void k_trans_tiled(const uint16_t* __restrict__ W,
+                                                     const float* __restrict__ x, int M,
+                                                     const float* __restrict__ c,
+                                                     float* __restrict__ h1,
+                                                     uint16_t* __restrict__ z,
+                                                     const int32_t* __restrict__ ctrl,
+                                                     int skip_when_done) {
+  if (skip_when_done && ctrl[1]) return;             // every sequence is at its fixed point
+  constexpr int LDX = K + 4;                         // floats per staged row
+  constexpr int r = 256, NO = MODE == 0 ? 2 * r : r; // output rows
+  __shared__ float xs[kTransPT * LDX];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, li = lane & 15;
+  const int m0 = blockIdx.y * kTransPT;
+  const int ob = blockIdx.x * 64 + wave * 16;        // the wave's first output row
+  // the wave's weight rows (A operand: row ob + li, k = 32 ks + 8 g ..)
+  u32x4 w[K / 32];
+#pragma unroll
+  for (int ks = 0; ks < K / 32; ++ks) w[ks] = ld16(W + (size_t)(ob + li) * K + 32 * ks + 8 * g);
+  // the positions' inputs (rows past M repeat row M - 1)
+#pragma unroll
+  for (int j = 0; j < kTransPT * K / 4 / 256; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    const int row = i / (K / 4), col = 4 * (i - row * (K / 4));
+    const int m = m0 + row < M ? m0 + row : M - 1;
+    *reinterpret_cast<float4*>(&xs[row * LDX + col]) =
+        *reinterpret_cast<const float4*>(x + (size_t)m * K + col);
+  }
+  __syncthreads();
+  floatx4 acc[kTransPT / 16];
+#pragma unroll
+  for (int pb = 0; pb < kTransPT / 16; ++pb) acc[pb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < K / 32; ++ks)
+#pragma unroll
+    for (int pb = 0; pb < kTransPT / 16; ++pb) {
+      const float* xr = &xs[(pb * 16 + li) * LDX + 32 * ks + 8 * g];
+      acc[pb] = mma_split_b(w[ks], *reinterpret_cast<const float4*>(xr),
+                            *reinterpret_cast<const float4*>(xr + 4), acc[pb]);
+    }
+  // lane holds output rows ob + 4 g + i of position pb * 16 + li
+#pragma unroll
+  for (int pb = 0; pb < kTransPT / 16; ++pb) {
+    const int m = m0 + pb * 16 + li;
+    if (m >= M) continue;
+    if constexpr (MODE == 0) {
+      float o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = acc[pb][i];
+        o[i] = v / (1.f + expf(-v));
+      }
+      *reinterpret_cast<float4*>(h1 + (size_t)m * NO + ob + 4 * g) = make_float4(o[0], o[1], o[2], o[3]);
+    } else {
+      const float4 cr = *reinterpret_cast<const float4*>(c + (size_t)m * r + ob + 4 * g);
+      const float cv[4] = {cr.x, cr.y, cr.z, cr.w};
+      uint16_t o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = f32_to_bf16_rne(cv[i] + acc[pb][i]);
+      *reinterpret_cast<uint2*>(z + (size_t)m * r + ob + 4 * g) =
+          make_uint2(o[0] | ((uint32_t)o[1] << 16), o[2] | ((uint32_t)o[3] << 16));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, const uint8_t* temp,
                        const float* temperature, hipStream_t st) {
   const int M = batch * h->B;
@@ -473,15 +555,27 @@ template <typename T, int BP>
 static void rspace_t(xp_handle* h, int batch, int pass, int skip, const int32_t* anchor,
                      bool front, hipStream_t st) {
   const int M = batch * h->B;
+  const bool tiled = sizeof(T) == 2 && M >= kTransTiled;
+  const dim3 tgrid1(512 / 64, (M + kTransPT - 1) / kTransPT), tgrid2(256 / 64, tgrid1.y);
   if (front) {
     hipLaunchKernelGGL((k_fusemix<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B, h->V, M,
                        h->ws.Pa, h->ws.T, (const T*)h->ws.Lp, anchor, h->ws.Y[pass % 2], h->ws.c,
                        h->ws.err, h->ws.iters, skip);
-    hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
-                       (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.iters, skip);
+    if (tiled)
+      hipLaunchKernelGGL((k_trans_tiled<256, 0>), tgrid1, dim3(256), 0, st,
+                         (const uint16_t*)h->W_1, h->ws.c, M, h->ws.c, h->ws.h1,
+                         (uint16_t*)nullptr, h->ws.ctrl, skip);
+    else
+      hipLaunchKernelGGL((k_trans1<T, BP>), dim3(batch, 32), dim3(256), 0, st, h->B,
+                         (const T*)h->W_1, h->ws.c, h->ws.h1, h->ws.iters, skip);
   }
-  hipLaunchKernelGGL((k_trans2<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B,
-                     (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.iters, skip);
+  if (tiled)
+    hipLaunchKernelGGL((k_trans_tiled<512, 1>), tgrid2, dim3(256), 0, st,
+                       (const uint16_t*)h->W_2, h->ws.h1, M, h->ws.c, (float*)nullptr,
+                       (uint16_t*)h->ws.z, h->ws.ctrl, skip);
+  else
+    hipLaunchKernelGGL((k_trans2<T, BP>), dim3(batch, 16), dim3(256), 0, st, h->B,
+                       (const T*)h->W_2, h->ws.c, h->ws.h1, (T*)h->ws.z, h->ws.iters, skip);
 }
 
 hipError_t launch_rspace(xp_handle* h, int batch, int pass, uint32_t flags, const int32_t* anchor,
