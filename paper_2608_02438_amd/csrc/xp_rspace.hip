@@ -32,12 +32,16 @@ __device__ __forceinline__ floatx4 mma4(float4 a, float4 b, floatx4 c) {
 // k_prep: part[mat][ks][m][o] = F_mat[o][slice ks] . h[m][slice ks] for
 // F_0 = W_in[:,0:r] W_h and F_1 = W_in[:,r:2r] W_g (fp32 [r][H]); the KSP
 // slice partials are added (in slice order) by their consumer.  Grid (16 row
-// tiles, KSP k-slices, 2 * position-block groups); 4 waves split a slice and
-// sum their 16x16 tiles in LDS in wave order.  F is split into three bf16
-// terms on the fly (exact), so the products run on the bf16 matrix cores.
-// Workgroup (0,0,0) also clears the per-call Jacobi state.
+// tiles, KSP k-slices, 2 * groups of pbg position blocks); 4 waves split a
+// slice and sum their 16x16 tiles in LDS in wave order.  F is split into
+// three bf16 terms (exact), so the products run on the bf16 matrix cores;
+// with bf16 h and slices of at most kPrepSteps steps a wave loads and splits
+// its F fragments once for all its position blocks, and takes the blocks
+// four at a time (their h loads issued together, one LDS reduction per four,
+// wave w summing block w).  Workgroup (0,0,0) also clears the per-call
+// Jacobi state.
 // ---------------------------------------------------------------------------
-constexpr int kPrepPBG = 8;            // position blocks per workgroup
+constexpr int kPrepPBG = 8;            // position blocks per workgroup, at least
 constexpr int kMaxKsp = 8;             // most k-slices of the prep product
 constexpr int kPrepSteps = 4;          // 32-wide steps per wave loaded at once
 
@@ -53,7 +57,8 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
                                               const float* __restrict__ Fg,
                                               const T* __restrict__ hid, int H, int M,
-                                              int ksp, float* __restrict__ part, int batch,
+                                              int ksp, int pbg, float* __restrict__ part,
+                                              int batch,
                                               int32_t* __restrict__ iters,
                                               int32_t* __restrict__ ctrl,
                                               const uint8_t* __restrict__ temp,
@@ -61,7 +66,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
                                               float* __restrict__ invT,
                                               uint32_t* __restrict__ err) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt = blockIdx.x, ks = blockIdx.y, mat = blockIdx.z & 1, pbg = blockIdx.z >> 1;
+  const int rt = blockIdx.x, ks = blockIdx.y, mat = blockIdx.z & 1, pgi = blockIdx.z >> 1;
   if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
     for (int i = threadIdx.x; i < batch; i += blockDim.x) {
       iters[i] = 0;
@@ -79,9 +84,62 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
   const int g = lane >> 4, li = lane & 15;
   const int k0 = ks * (H / ksp) + wave * kw;
   const float* arow = F + (size_t)(rt * 16 + li) * H + k0;
-  __shared__ floatx4 red[4][64];
+  __shared__ floatx4 red[4][4][64];
   const int npb = (M + 15) / 16;
-  const int pb0 = pbg * kPrepPBG, pb1 = min(npb, (pbg + 1) * kPrepPBG);
+  const int pb0 = pgi * pbg, pb1 = min(npb, (pgi + 1) * pbg);
+  if constexpr (sizeof(T) == 2) {
+    if (kw / 32 <= kPrepSteps) {
+      const int ns = kw / 32;
+      u32x4 fh[kPrepSteps], fm[kPrepSteps], fl[kPrepSteps];
+#pragma unroll
+      for (int u = 0; u < kPrepSteps; ++u) {
+        const int uc = u < ns ? u : ns - 1;
+        split3x8(*reinterpret_cast<const float4*>(arow + uc * 32 + 8 * g),
+                 *reinterpret_cast<const float4*>(arow + uc * 32 + 8 * g + 4), fh[u], fm[u], fl[u]);
+      }
+      for (int pq = pb0; pq < pb1; pq += 4) {
+        u32x4 bv[4][kPrepSteps];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int p = (pq + q) * 16 + li;
+          const T* brow = hid + (size_t)(p < M ? p : M - 1) * H + k0 + 8 * g;
+#pragma unroll
+          for (int u = 0; u < kPrepSteps; ++u) {
+            bv[q][u] = ld16(brow + (u < ns ? u : ns - 1) * 32);
+            if (pq + q >= pb1 || p >= M) bv[q][u] = u32x4{0u, 0u, 0u, 0u};
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int u = 0; u < kPrepSteps; ++u)
+            if (u < ns) {
+              acc = Mfma<uint16_t>::mma(fh[u], bv[q][u], acc);
+              acc = Mfma<uint16_t>::mma(fm[u], bv[q][u], acc);
+              acc = Mfma<uint16_t>::mma(fl[u], bv[q][u], acc);
+            }
+          red[wave][q][lane] = acc;
+        }
+        __syncthreads();
+        if (pq + wave < pb1) {                        // wave w sums block pq + w in wave order
+          floatx4 s = red[0][wave][lane];
+#pragma unroll
+          for (int w = 1; w < 4; ++w) {
+            const floatx4 o = red[w][wave][lane];
+            s[0] += o[0]; s[1] += o[1]; s[2] += o[2]; s[3] += o[3];
+          }
+          const int p = (pq + wave) * 16 + li;
+          if (p < M) {
+            float* dst = part + (((size_t)mat * ksp + ks) * M + p) * 256 + rt * 16 + 4 * g;
+            *reinterpret_cast<float4*>(dst) = make_float4(s[0], s[1], s[2], s[3]);
+          }
+        }
+        __syncthreads();
+      }
+      return;
+    }
+  }
   for (int pb = pb0; pb < pb1; ++pb) {
     const int p = pb * 16 + li;
     const int pc = p < M ? p : M - 1;
@@ -119,13 +177,13 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ Fh,
         acc = mma4(a, bv, acc);
       }
     }
-    red[wave][lane] = acc;
+    red[wave][0][lane] = acc;
     __syncthreads();
     if (wave == 0) {
-      floatx4 s = red[0][lane];
+      floatx4 s = red[0][0][lane];
 #pragma unroll
       for (int w = 1; w < 4; ++w) {
-        const floatx4 o = red[w][lane];
+        const floatx4 o = red[w][0][lane];
         s[0] += o[0]; s[1] += o[1]; s[2] += o[2]; s[3] += o[3];
       }
       if (p < M) {
@@ -531,15 +589,18 @@ hipError_t launch_prep(xp_handle* h, int batch, const void* hidden, const uint8_
   const int M = batch * h->B;
   const int npb = (M + 15) / 16;
   const int ksp = prep_ksp(h->H);
-  dim3 grid(h->r / 16, ksp, 2 * ((npb + kPrepPBG - 1) / kPrepPBG));
+  // position blocks per workgroup: kPrepPBG, more for large calls (about
+  // four groups, so a launch has 2 * 16 * ksp * 4 workgroups)
+  const int pbg = std::max(kPrepPBG, (npb + 3) / 4);
+  dim3 grid(h->r / 16, ksp, 2 * ((npb + pbg - 1) / pbg));
   if (h->dtype == XP_BF16)
     hipLaunchKernelGGL((k_prep<uint16_t>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
-                       (const uint16_t*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
-                       h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
+                       (const uint16_t*)hidden, h->H, M, ksp, pbg, h->ws.ppart, batch,
+                       h->ws.iters, h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
   else
     hipLaunchKernelGGL((k_prep<float>), grid, dim3(256), 0, st, h->ws.Fh, h->ws.Fg,
-                       (const float*)hidden, h->H, M, ksp, h->ws.ppart, batch, h->ws.iters,
-                       h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
+                       (const float*)hidden, h->H, M, ksp, pbg, h->ws.ppart, batch,
+                       h->ws.iters, h->ws.ctrl, temp, temperature, h->ws.invT, h->ws.err);
   if (h->B <= 16)
     hipLaunchKernelGGL((k_prep_sum<16>), dim3(batch, 16), dim3(256), 0, st, h->B, M, ksp,
                        h->ws.ppart, h->ws.Pa);
