@@ -336,9 +336,11 @@ const char* xp_layer_last_error(const xp_layer* L);
  * keeps the last call's contents: calls that overlap in time on one GPU (two
  * streams, or two host threads) race and give undefined results; calls
  * ordered on one stream are safe.  Output equals xp_layer_forward's bit for
- * bit when the call's attention partials fit beside its other buffers at the
- * default chunking; otherwise the context is read in longer chunks (fewer
- * partials), which changes only the fp32 summation order.
+ * bit for calls of up to 64 positions whose attention partials fit beside
+ * the other buffers at the default chunking.  Otherwise only the fp32
+ * summation order differs: the context may be read in longer chunks (fewer
+ * partials), and above 64 positions the projections run without the k
+ * splits that xp_layer_forward may use.
  *
  * Limits: batch * B positions whose buffers (about 124 KB per position at
  * the Qwen3-8B shape, plus 1.5 MB of gate/up rows) fit in the array with at
