@@ -196,12 +196,14 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
 
 // One workgroup per sequence.  mode 0: seed Y^(0) from the base logits (or the
 // caller's seed ids); mode 1: the selection of Jacobi pass `pass`.  Greedy
-// rows issue every key load of the wave's positions (and the previous
-// iterate and iteration count) before the first use, so a greedy selection
-// costs one memory round trip.
+// rows take the maximum 64-bit key of every position over the nkeys unit
+// rows: thread t takes position t % PP (PP = 16 or 32 >= B) of rows t / PP,
+// t / PP + NRG, ..., so that one load instruction reads whole runs of
+// consecutive positions of a key row (keys are [row][M]); every load of a
+// thread is issued before its first compare, then lanes and waves holding
+// the same position combine their maxima.  So a greedy selection costs one
+// memory round trip with coalesced loads.
 constexpr int kSelWaves = 8;
-constexpr int kSelKPL = 4;                      // keys per lane and position (256 units)
-constexpr int kSelPPW = 32 / kSelWaves;         // positions per wave (B <= 32)
 
 template <typename T>
 __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
@@ -213,76 +215,71 @@ __global__ __launch_bounds__(kSelWaves * kWave) void k_select(
     int32_t* __restrict__ traj, double* __restrict__ lse, int32_t* __restrict__ iters,
     int32_t* __restrict__ ctrl, uint32_t* __restrict__ err, int early_exit,
     int32_t* __restrict__ out_ids, int32_t* __restrict__ out_iters, int K) {
-  const int b = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int NT = kSelWaves * kWave, kRowsPerRound = 16;
+  const int b = blockIdx.x, t = threadIdx.x;
   __shared__ int changed;
+  __shared__ uint64_t sbest[kSelWaves][32];
   const bool skip = mode == 1 && early_exit && iters[b] != 0;   // at its fixed point
   if (skip) {                                     // the block carries over
-    for (int k = threadIdx.x; k < B; k += kSelWaves * kWave) {
+    for (int k = t; k < B; k += NT) {
       const int p = b * B + k;
       const int y = Yprev[p];
       Ynew[p] = y;
       if (traj) traj[p] = y;
       if (out_ids) out_ids[p] = y;
     }
-    if (threadIdx.x == 0 && out_iters) out_iters[b] = iters[b];
+    if (t == 0 && out_iters) out_iters[b] = iters[b];
     return;
-  }
-  // independent loads first (keys unconditionally: unused ones are harmless)
-  uint64_t kv[kSelPPW][kSelKPL];
-  int yprev[kSelPPW];
-#pragma unroll
-  for (int m = 0; m < kSelPPW; ++m) {
-    const int k = wave + kSelWaves * m;
-    const int p = b * B + (k < B ? k : B - 1);
-#pragma unroll
-    for (int r = 0; r < kSelKPL; ++r) {
-      const int i = lane + kWave * r;
-      kv[m][r] = keys[(size_t)(i < nkeys ? i : nkeys - 1) * M + p];
-    }
-    yprev[m] = mode == 1 ? Yprev[p] : 0;
   }
   const int it0 = iters[b];
   const bool sample = temp != nullptr && temp[b] != 0;
-  if (threadIdx.x == 0) changed = 0;
-  __syncthreads();
+  const bool seeded = mode == 0 && seed_ids != nullptr;
+  if (t == 0) changed = 0;
+  if (!sample && !seeded) {                       // workgroup-uniform
+    const int PP = B <= 16 ? 16 : 32, NRG = NT / PP;
+    const int pos = t % PP, rg = t / PP;
+    const size_t col = (size_t)b * B + (pos < B ? pos : B - 1);
+    uint64_t best = 0;
+    for (int r0 = rg; r0 < nkeys; r0 += kRowsPerRound * NRG) {
+      uint64_t kv[kRowsPerRound];
 #pragma unroll
-  for (int m = 0; m < kSelPPW; ++m) {
-    const int k = wave + kSelWaves * m;
-    if (k >= B) continue;                         // wave-uniform
-    const int p = b * B + k;
-    int y = 0;
-    if (skip) {
-      y = yprev[m];
-    } else if (mode == 0 && seed_ids != nullptr) {
+      for (int j = 0; j < kRowsPerRound; ++j) {
+        const int r = r0 + j * NRG;               // rows past nkeys repeat the last
+        kv[j] = keys[(size_t)(r < nkeys ? r : nkeys - 1) * M + col];
+      }
+#pragma unroll
+      for (int j = 0; j < kRowsPerRound; ++j) best = umax64(best, kv[j]);
+    }
+    for (int o = PP; o < kWave; o <<= 1) best = umax64(best, shfl_xor_u64(best, o));
+    if ((t & (kWave - 1)) < PP) sbest[t / kWave][pos] = best;
+  }
+  __syncthreads();
+  if (t < B) {
+    const int p = b * B + t;
+    int y;
+    if (seeded) {
       y = seed_ids[p];
       if (y < 0 || y >= V) {
-        if (lane == 0) atomicOr(err, XP_DEVERR_TOKEN);
+        atomicOr(err, XP_DEVERR_TOKEN);
         y = 0;
       }
     } else if (!sample) {
-      uint64_t best = kv[m][0];
+      uint64_t bb = sbest[0][t];
 #pragma unroll
-      for (int r = 1; r < kSelKPL; ++r) best = umax64(best, kv[m][r]);
-      for (int i = lane + kWave * kSelKPL; i < nkeys; i += kWave)   // more than 256 units
-        best = umax64(best, keys[(size_t)i * M + p]);
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) best = umax64(best, shfl_xor_u64(best, o));
-      y = (int)key_index(best);
+      for (int w = 1; w < kSelWaves; ++w) bb = umax64(bb, sbest[w][t]);
+      y = (int)key_index(bb);
     } else {
       y = Ynew[p];                                // chosen by k_sample
     }
-    if (lane == 0) {
-      Ynew[p] = y;
-      if (traj) traj[p] = y;
-      if (out_ids) out_ids[p] = y;
-      if (mode == 1 && y != yprev[m]) atomicOr(&changed, 1);
-    }
+    Ynew[p] = y;
+    if (traj) traj[p] = y;
+    if (out_ids) out_ids[p] = y;
+    if (mode == 1 && y != Yprev[p]) atomicOr(&changed, 1);
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (t == 0) {
     int it = it0;
-    if (mode == 1 && !skip && changed == 0 && it == 0) {
+    if (mode == 1 && changed == 0 && it == 0) {
       it = pass + 1;
       iters[b] = it;
       if (atomicAdd(&ctrl[0], 1) + 1 == batch) ctrl[1] = 1;
