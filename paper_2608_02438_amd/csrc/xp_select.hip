@@ -47,7 +47,7 @@ __device__ __forceinline__ float wave_max(float x) {
 // partition's size, not the largest one supported, so no fp64 exponential or
 // scan runs on masked lanes and the registers allow more workgroups per CU.
 constexpr int kSmpWaves = 8;
-constexpr int kSmpChunks = 8;        // 64-unit chunks per wave at most: up to 4096 units
+constexpr int kSmpChunks = 4096 / (kSmpWaves * 64);   // 64-unit chunks per wave at most: 4096 units
 constexpr int kSmpRows = 128;        // rows of the largest unit (8 tiles)
 
 template <typename T, int CH>
@@ -158,17 +158,17 @@ __global__ __launch_bounds__(kSmpWaves * kWave) void k_sample(
   // logits of the unit's rows: mode 1 recomputes l = s + W_r z with the
   // stream's tile code, one wave per tile (a unit of a Read partition has at
   // most kSmpRows / 16 tiles); mode 0 reads s while scanning
-  if (mode == 1 && wave < thi - tlo) {
+  for (int tw = wave; mode == 1 && tw < thi - tlo; tw += kSmpWaves) {   // wave-uniform
     constexpr int NU = ReadTile<T>::NU;
     u32x4 bf[NU], a[NU];
-    const int t = tlo + wave;
+    const int t = tlo + tw;
     ReadTile<T>::load_z(Z, M, p & ~15, lane, bf);
     ReadTile<T>::load_w(W_r, V, t, lane, a);
     const int pl = (p & ~15) + (lane & 15);
     const floatx4 acc = ReadTile<T>::chain(a, bf, ReadTile<T>::load_s(S, Ms, pl, pl < M, t, lane));
     if ((lane & 15) == (p & 15)) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) lrow[kTile * wave + 4 * (lane >> 4) + i] = acc[i];
+      for (int i = 0; i < 4; ++i) lrow[kTile * tw + 4 * (lane >> 4) + i] = acc[i];
     }
   }
   __syncthreads();
@@ -334,7 +334,10 @@ hipError_t launch_select(xp_handle* h, int batch, int pass, int K, uint32_t flag
     case 5: XP_SMP(TT, 5); break;                                                             \
     case 6: XP_SMP(TT, 6); break;                                                             \
     case 7: XP_SMP(TT, 7); break;                                                             \
-    default: XP_SMP(TT, 8);                                                                   \
+    case 8: XP_SMP(TT, 8); break;                                                             \
+    default:                                                                                  \
+      if (ch <= 12) XP_SMP(TT, (kSmpChunks < 12 ? kSmpChunks : 12));                          \
+      else XP_SMP(TT, kSmpChunks);                                                            \
   }
     if (h->dtype == XP_BF16) {
       XP_SMP_CH(uint16_t)
