@@ -94,6 +94,13 @@ __device__ __forceinline__ void wave_lds_order() {
 __device__ __forceinline__ void lds_dma16(const void* g, u32x4* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 }
+// The same with the non-temporal hint (nt), for data streamed once per use
+// (the base logits in the many-position Read): with it the streams leave the
+// reused operands in the caches, and the many-position Read runs about 10%
+// faster.
+__device__ __forceinline__ void lds_dma16_nt(const void* g, u32x4* lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 2);
+}
 
 // Workgroup barrier that publishes LDS writes only.  __syncthreads() also
 // waits for every outstanding global load of the wave (the fence drains the

@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kReadWaves * kWave) void k_read_multi(
     lds_dma16(W + (size_t)row * 256 + 8 * wchunk, stage + kWave * wave);
 #pragma unroll
     for (int pb = 0; pb < P; ++pb)
-      lds_dma16(sbase[pb] + (wdead ? (size_t)0 : (size_t)t * Ms * kTile),
+      lds_dma16_nt(sbase[pb] + (wdead ? (size_t)0 : (size_t)t * Ms * kTile),
                 stage + WSL + kWave * (P * wave + pb));
   };
   // (max, sum) of every unit that ends at or before tile boundary tend
