@@ -77,6 +77,31 @@ __host__ __device__ __forceinline__ size_t s_index(int p, int row, int Ms) {
 }
 
 // ---------------------------------------------------------------------------
+// Exchanges across the 16- and 32-lane halves of the wave on gfx950's lane-swap
+// instructions (v_permlane16_swap, v_permlane32_swap) instead of an LDS round
+// trip.  With x as both operands the instruction returns, in every lane, the
+// values of lanes l and l ^ 16 (l ^ 32), that of the lower half first, so the
+// max or sum of the pair equals x combined with its partner's value bit for
+// bit (both operations commute).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float fmax_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float fmax_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float fadd_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float fadd_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ---------------------------------------------------------------------------
 // Order a wave's LDS writes before its later LDS reads of other lanes' data.
 // A wave's LDS instructions execute in program order, so only the compiler
 // must be kept from moving the accesses across this point.

@@ -590,8 +590,7 @@ __device__ __forceinline__ void attn_step(const u32x4* Ks, const uint16_t* Vs,
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
-  mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+  mx = fmax_xor32(fmax_xor16(mx));
   // with no visible key yet (mx = -inf) every exponent below is -inf: 0
   const float mxs = mx == -INFINITY ? 0.f : mx;
   const float alpha = __builtin_amdgcn_exp2f(m_run - mxs);
@@ -614,8 +613,7 @@ __device__ __forceinline__ void attn_step(const u32x4* Ks, const uint16_t* Vs,
       eh[t][i / 2] = h;
       el[t][i / 2] = lo;
     }
-  lsum += __shfl_xor(lsum, 16, kWave);
-  lsum += __shfl_xor(lsum, 32, kWave);
+  lsum = fadd_xor32(fadd_xor16(lsum));
   l_run = l_run * alpha + lsum;
   const bool moved = __ballot(mx != m_run) != 0;  // wave-uniform: else every alpha is 1
   m_run = mx;
