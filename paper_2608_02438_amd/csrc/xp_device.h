@@ -120,9 +120,9 @@ __device__ __forceinline__ void lds_dma16(const void* g, u32x4* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 }
 // The same with the non-temporal hint (nt), for data streamed once per use
-// (the base logits in the many-position Read): with it the streams leave the
-// reused operands in the caches, and the many-position Read runs about 10%
-// faster.
+// (the base logits in the many-position Read), so that the stream leaves the
+// reused operands (W_r, z) in the caches: 304 instead of 311 us per Read pass
+// at 2048 positions, 70 instead of 81 us at 512.
 __device__ __forceinline__ void lds_dma16_nt(const void* g, u32x4* lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 2);
 }
