@@ -7,10 +7,21 @@
 // A tile is BN weight rows x BM positions, computed by 8 waves: wave w owns
 // rows (w & 1) BN/2 .. + BN/2 and positions (w >> 1) BM/4 .. + BM/4 as
 // 32 x 32 blocks.  k advances 32 per stage through an LDS ring of NS stages
-// filled by global_load_lds_dwordx4 (no staging registers): wave w fills W
-// slots [64 WI w, 64 WI (w + 1)) and X slots [64 HI w, 64 HI (w + 1)) with 1 KB
-// instructions.  A stage row holds 32 k (four 16-byte chunks); chunk c of row r
-// sits in slot 4 r + (c ^ swz(r)), swz(r) = (r / 4) mod 4: four consecutive
+// filled by global_load_lds_dwordx4 (no staging registers).  Only waves 0-3,
+// one per SIMD (a workgroup's wave w runs on SIMD w mod 4), issue the loads:
+// wave w < 4 fills W slots [64 WI w, 64 WI (w + 1)) and X slots
+// [64 HI w, 64 HI (w + 1)) with 1 KB instructions (WI, HI for the 4 loading
+// waves).  A load instruction can wait many cycles at issue while the
+// address units work through the workgroup's 32 KB per stage (timestamps in
+// a copy of the loop: 14% of a wave's time at 2048 positions); with every
+// wave loading, both waves of a SIMD stall there at about the same time,
+// while with one loading wave per SIMD the other one keeps issuing matrix
+// operations.  Measured on the LM-head GEMM: 2% less time at 512 positions,
+// no change at 2048; waves 4-7 as the loading waves, or the loads split over
+// both halves of a stage, were slower.
+//
+// A stage row holds 32 k (four 16-byte chunks); chunk c of row r sits in
+// slot 4 r + (c ^ swz(r)), swz(r) = (r / 4) mod 4: four consecutive
 // rows fill one 256-byte line of the 64 banks and the next three groups of
 // four rotate their chunks, so an operand read (32 rows, one chunk) meets no
 // bank conflict (SQ_LDS_BANK_CONFLICT reads zero; with swz(r) = ((r / 2) xor
@@ -32,6 +43,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kGK = 32;             // k per LDS stage
 constexpr int kGWaves = 8;          // 2 (rows) x 4 (positions) waves
+constexpr int kGLoaders = 4;        // waves that issue the stage loads (0 .. 3)
 constexpr int kGPerXcd = 32;        // workgroups per XCD (one per CU)
 
 __device__ __forceinline__ floatx16 mma32(u32x4 a, u32x4 b, floatx16 c) {
@@ -47,7 +59,7 @@ struct GemmShape {
   static constexpr int RW = BN / 2, PW = BM / 4;                       // rows, positions per wave
   static constexpr int NA = RW / 32, NB = PW / 32;                     // 32 x 32 blocks per wave
   static constexpr int WS = BN * kGK * 2 / 16, HS = BM * kGK * 2 / 16; // slots per operand stage
-  static constexpr int WI = WS / 64 / kGWaves, HI = HS / 64 / kGWaves; // 1 KB loads per wave
+  static constexpr int WI = WS / 64 / kGLoaders, HI = HS / 64 / kGLoaders; // 1 KB loads per loading wave
   static constexpr int NS0 = 163840 / ((WS + HS) * 16);
   static constexpr int NS = NS0 < 8 ? NS0 : 8;                         // ring stages
   static constexpr int SLOTS = NS * (WS + HS);
@@ -79,19 +91,21 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   GemmLane where{wave & 1, wave >> 1, lane & 31, lane >> 5};
+  const bool loader = wave < kGLoaders;                           // wave-uniform
+  const int li = wave & (kGLoaders - 1);
 
   // lane l of a load instruction writes the next slot: LDS row slot / 4,
   // stored chunk l % 4, which holds logical chunk (l % 4) ^ swz(row)
   int wrow[WI], wcol[WI], hrow[HI];
 #pragma unroll
   for (int j = 0; j < WI; ++j) {
-    const int row = (64 * (WI * wave + j) + lane) >> 2;
+    const int row = (64 * (WI * li + j) + lane) >> 2;
     wrow[j] = row;
     wcol[j] = 8 * ((lane & 3) ^ gswz(row));
   }
 #pragma unroll
   for (int j = 0; j < HI; ++j) {
-    const int row = (64 * (HI * wave + j) + lane) >> 2;
+    const int row = (64 * (HI * li + j) + lane) >> 2;
     int hr = p0 + row;
     hr = hr < M ? hr : M - 1;
     hrow[j] = hr * ldx + 8 * ((lane & 3) ^ gswz(row));
@@ -111,11 +125,11 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
     const int st = gs % NS;
 #pragma unroll
     for (int j = 0; j < WI; ++j)
-      lds_dma16(rows.row(wrow[j]) + kc * kGK + wcol[j], &lds[st * (WS + HS) + 64 * (WI * wave + j)]);
+      lds_dma16(rows.row(wrow[j]) + kc * kGK + wcol[j], &lds[st * (WS + HS) + 64 * (WI * li + j)]);
 #pragma unroll
     for (int j = 0; j < HI; ++j)
       lds_dma16(X + (size_t)(unsigned)hrow[j] + rows.xk + kc * kGK,
-                &lds[st * (WS + HS) + WS + 64 * (HI * wave + j)]);
+                &lds[st * (WS + HS) + WS + 64 * (HI * li + j)]);
   };
 
   floatx16 acc[NA][NB];
@@ -146,8 +160,10 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     prep(s);
-    issue(s);
+    if (loader) issue(s);
   }
+  // (the other waves have no loads outstanding; for them the waits below
+  // cover only the epilogue's stores)
   constexpr int kP0 = (WI + HI) * (NS - 1), kP = (WI + HI) * (NS - 2);
   static_assert(kP0 < 64, "vmcnt field");
   // stage 0 landed (this wave's loads), then every wave's
@@ -169,7 +185,7 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
     // one by one between the matrix operations of the current one (the
     // scheduling groups below), so the LDS reads overlap the matrix pipe; the
     // row bookkeeping of stage gs + NS runs before the wait and its loads are
-    // issued after the barrier, behind those reads.
+    // issued after the barrier, behind the second half's matrix operations.
     rd(gs, 1, fa[1], fb[1]);
     mm(fa[0], fb[0]);
 #pragma unroll
@@ -187,15 +203,14 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
     asm volatile("" ::: "memory");
     rd(gs + 1, 0, fa[0], fb[0]);
     mm(fa[1], fb[1]);
-    issue(gs + NS);
 #pragma unroll
     for (int q = 0; q < NA + NB; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (loader) issue(gs + NS);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_sched_barrier(0);
