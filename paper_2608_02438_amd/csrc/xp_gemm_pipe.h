@@ -79,10 +79,12 @@ struct GemmLane {
 // element offset into the X rows); rows.row(r) is then the address of its
 // local row r (0 <= r < BN) at that k.  epi(ti, acc, where) consumes tile
 // ti's accumulators; the pipeline clears them afterwards.  lds holds
-// GemmShape<BN, BM>::SLOTS 16-byte slots.
+// GemmShape<BN, BM>::SLOTS 16-byte slots.  Every tile walks its k chunks
+// starting at chunk kshift (0 <= kshift < K / 32) and wrapping around.
 template <int BN, int BM, class Rows, class Epi>
 __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t* __restrict__ X,
-                                           int ldx, int M, int K, int ntl, int p0, u32x4* lds) {
+                                           int ldx, int M, int K, int ntl, int p0, u32x4* lds,
+                                           int kshift = 0) {
   using G = GemmShape<BN, BM>;
   constexpr int RW = G::RW, PW = G::PW, NA = G::NA, NB = G::NB, WS = G::WS, HS = G::HS;
   constexpr int WI = G::WI, HI = G::HI, NS = G::NS;
@@ -121,7 +123,7 @@ __device__ __forceinline__ void gemm_tiles(Rows& rows, Epi& epi, const uint16_t*
   };
   auto issue = [&](int gs) {                                       // global stage gs (clamped)
     gs = gs < nstages ? gs : nstages - 1;
-    const int ti = gs / nk, kc = gs - ti * nk;
+    const int ti = gs / nk, kq = gs - ti * nk + kshift, kc = kq < nk ? kq : kq - nk;
     const int st = gs % NS;
 #pragma unroll
     for (int j = 0; j < WI; ++j)
