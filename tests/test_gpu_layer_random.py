@@ -16,7 +16,7 @@ import pytest
 
 from test_gpu_layer import _case, _check, _run
 
-N_CASES = 20
+N_CASES = 48
 
 
 def _say(*a):

@@ -22,7 +22,7 @@ import pytest
 from _parity import Tally, custom_problem, make_refiner, run_device, upload
 
 STRESS = dict(W_e=1.0, W_r=0.3, L=0.3, W_in=0.08, W_1=0.08, W_2=0.06)
-N_CASES = 64
+N_CASES = 128
 _TOTAL = Tally()
 
 
