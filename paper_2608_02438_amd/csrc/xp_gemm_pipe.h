@@ -16,9 +16,9 @@
 // a copy of the loop: 14% of a wave's time at 2048 positions); with every
 // wave loading, both waves of a SIMD stall there at about the same time,
 // while with one loading wave per SIMD the other one keeps issuing matrix
-// operations.  Measured on the LM-head GEMM: 2% less time at 512 positions,
-// no change at 2048; waves 4-7 as the loading waves, or the loads split over
-// both halves of a stage, were slower.
+// operations.  Measured on the LM-head GEMM: 2-3% less time at 128 and 512
+// positions, no change at 2048; waves 4-7 as the loading waves, or the loads
+// split over both halves of a stage, were slower.
 //
 // A stage row holds 32 k (four 16-byte chunks); chunk c of row r sits in
 // slot 4 r + (c ^ swz(r)), swz(r) = (r / 4) mod 4: four consecutive
