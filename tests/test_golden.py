@@ -76,3 +76,28 @@ def test_bf16_round_to_nearest_even():
     want = np.asarray([c["bf16"] for c in g["cases"]], dtype=np.float64)
     got = np.asarray(O.round_bf16(x), dtype=np.float64)
     assert np.array_equal(got, want), list(zip(x.tolist(), got.tolist(), want.tolist()))
+
+
+def test_tiny_refiner_by_hand():
+    """Fuse (block order [h | g | token], g the mean, x_{k-1} the previous
+    guess), Mix, Read, Correct and the Jacobi loop at H = r = 1, V = 2, B = 2."""
+    g = _load("refiner_tiny.json")
+    w = {k: np.asarray(v, dtype=np.float64) for k, v in g["weights"].items()}
+    P = O.Params.from_arrays(w, round_z=False)
+    h = np.asarray(g["h"], dtype=np.float64)
+    s = O.base_logits(w["W_lm"], h)
+    assert np.array_equal(s, np.asarray(g["s"]))
+    st = O.fuse_static(P, h)
+    for ps in g["passes"]:
+        x_prev = np.concatenate([[g["anchor"]], np.asarray(ps["Y_prev"])[:-1]])
+        A = O.fuse(P, st, x_prev)
+        C = O.mix(P.L, A)
+        assert np.array_equal(A, np.asarray(ps["A"])) and np.array_equal(C, np.asarray(ps["C"]))
+        delta, _ = O.refiner(P, st, x_prev)
+        assert np.array_equal(delta, np.asarray(ps["delta"]))
+        Y, _, l = O.pass_from(P, s, h, g["anchor"], ps["Y_prev"], False, None)
+        assert np.array_equal(l, np.asarray(ps["l"])) and list(Y) == ps["Y"]
+    r = O.refine_block(P, s, h, g["anchor"], K=3)
+    assert list(r.traj[0]) == g["Y0"]
+    assert list(r.ids) == g["ids"] and r.iters == g["iters"]
+    assert list(O.sequential_decode(P, s, h, g["anchor"])) == g["sequential"]
