@@ -498,9 +498,10 @@ __global__ __launch_bounds__(256) void k_qkrope(
 // i % 4 of the 8-byte reads of lanes 4 j + i / 4, j = 0..3, so when lane s
 // reads 4 columns of key row k0 + s / 4, lane i receives keys k0 .. k0 + 3 of
 // one column); the output lane holds queries 4 (l / 16) + i for
-// d = 16 dt + l % 16.  A new maximum rescales O and l by 2^(m_old - m_new)
-// (scores in base-2 units).  Written per (chunk, query): O (relative to the
-// chunk's final maximum m), m and l.
+// d = 16 dt + l % 16.  The reference m of a query moves only when a score
+// exceeds it by more than 2^8 (scores in base-2 units), and then O and l are
+// rescaled by 2^(m_old - m_new).  Written per (chunk, query): O and l
+// relative to the chunk's final reference m, and m.
 // ---------------------------------------------------------------------------
 constexpr int kSub = 64;                       // keys per sub-chunk (one LDS stage)
 constexpr int kAttnSlots = 2 * kSub * kHd / 8; // 16-byte slots of a stage: K rows, then V rows
@@ -585,15 +586,21 @@ __device__ __forceinline__ void attn_step(const u32x4* Ks, const uint16_t* Vs,
       }
     }
   }
-  float mx = m_run;
+  // The reference maximum m_run of a query moves only when one of its
+  // scores exceeds it by more than kLazy (base-2 units), so most sub-chunks
+  // skip the rescale of O and l; the numerators are then at most 2^kLazy,
+  // well inside fp32, and their bf16 parts keep the same relative precision.
+  constexpr float kLazy = 8.f;
+  float mt = -INFINITY;                           // the sub-chunk's row maximum
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sc[t][i]);
-  mx = fmax_xor32(fmax_xor16(mx));
-  // with no visible key yet (mx = -inf) every exponent below is -inf: 0
-  const float mxs = mx == -INFINITY ? 0.f : mx;
-  const float alpha = __builtin_amdgcn_exp2f(m_run - mxs);
+    for (int i = 0; i < 4; ++i) mt = fmaxf(mt, sc[t][i]);
+  mt = fmax_xor32(fmax_xor16(mt));
+  const bool grow = __ballot(mt > m_run + kLazy) != 0;   // wave-uniform
+  const float mref = grow ? fmaxf(m_run, mt) : m_run;
+  // with no visible key yet (mref = -inf) every exponent below is -inf: 0
+  const float mxs = mref == -INFINITY ? 0.f : mref;
   // numerators as two bf16 parts (hi = bf16(e), lo = bf16(e - hi)); the
   // sum is taken over the same parts
   uint32_t eh[NT][2], el[NT][2];
@@ -614,18 +621,20 @@ __device__ __forceinline__ void attn_step(const u32x4* Ks, const uint16_t* Vs,
       el[t][i / 2] = lo;
     }
   lsum = fadd_xor32(fadd_xor16(lsum));
-  l_run = l_run * alpha + lsum;
-  const bool moved = __ballot(mx != m_run) != 0;  // wave-uniform: else every alpha is 1
-  m_run = mx;
-  // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
-  if (moved) {
+  if (grow) {                                     // wave-uniform
+    const float alpha = __builtin_amdgcn_exp2f(m_run - mxs);
+    l_run = l_run * alpha + lsum;
+    // O rows are queries 4 (l / 16) + i: their factors come from lanes 4 g + i
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float ai = __shfl(alpha, 4 * g + i, kWave);
 #pragma unroll
       for (int dt = 0; dt < kHd / 16; ++dt) o[dt][i] *= ai;
     }
+  } else {
+    l_run += lsum;
   }
+  m_run = mref;
   // V reads: lane (g, li) supplies key row k0 + li / 4 (k0 = 32 u + 4 g,
   // then + 16), columns 16 dt + 4 (li % 4) .. + 3: chunk 2 dt + (li % 4) / 2,
   // half (li % 4) & 1
